@@ -1,0 +1,59 @@
+"""The fp64 exponential used for the sibling softmax of Eq. 1.
+
+The paper fixes no numeric form for the softmax.  Trees are compared bit for
+bit, and bf16 logits make mathematically equal path products common, so both
+sides must produce identical bits for every factor; neither may use its
+platform's libm.  Both implement this one published method:
+
+  Cody & Waite (1980) argument reduction  t = k*ln2 + r,  |r| <= ln2/2,
+  with ln2 split into LN2_HI (ln2 rounded to 32 significant bits, so k*LN2_HI
+  is exact for |k| < 2^21) and LN2_LO = fl(ln2 - LN2_HI);
+  k = rint(fl(t * INV_LN2)) (round half to even);
+  r = fl(fl(t - k*LN2_HI) - fl(k*LN2_LO));
+  p = degree-13 Taylor polynomial of exp(r) by Horner, coefficients fl(1/n!),
+      each step fl(fl(p*r) + c) with no fused multiply-add;
+  result = ldexp(p, k).
+
+Specials (defined for the inputs the method produces, t <= 0):
+  t is NaN -> 0.0;  t < -708 -> 0.0;  t == 0 -> 1.0 exactly.
+
+The truncation error |r|^14/14! < 5e-18 is far below one ulp.
+Constants are derived here from ln 2 computed with exact rationals.
+"""
+from __future__ import annotations
+
+import math
+from fractions import Fraction
+
+
+def _ln2_fraction(terms: int = 80) -> Fraction:
+    # ln 2 = 2*atanh(1/3) = 2 * sum_{k>=0} 1 / ((2k+1) 3^(2k+1)); 80 terms give ~150 digits.
+    s = Fraction(0)
+    for k in range(terms):
+        s += Fraction(1, (2 * k + 1) * 3 ** (2 * k + 1))
+    return 2 * s
+
+
+_LN2 = _ln2_fraction()
+INV_LN2 = float(1 / _LN2)                                  # nearest double to 1/ln2
+LN2_HI = float(Fraction(round(_LN2 * 2 ** 32), 2 ** 32))  # 32 significant bits (ln2 in [1/2, 1))
+LN2_LO = float(_LN2 - Fraction(LN2_HI))                    # nearest double to the remainder
+COEF = [float(Fraction(1, math.factorial(n))) for n in range(14)]  # fl(1/n!), n = 0..13
+
+T_MIN = -708.0
+
+
+def spec_exp(t: float) -> float:
+    """exp(t) for t <= 0 under the shared fp64 contract described above."""
+    t = float(t)
+    if math.isnan(t) or t < T_MIN:
+        return 0.0
+    if t == 0.0:
+        return 1.0
+    k = round(t * INV_LN2)           # Python round(): half to even, exact on doubles
+    kf = float(k)
+    r = (t - kf * LN2_HI) - kf * LN2_LO
+    p = COEF[13]
+    for n in range(12, -1, -1):
+        p = p * r + COEF[n]          # two roundings: Python never fuses
+    return math.ldexp(p, k)
