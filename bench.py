@@ -1,0 +1,282 @@
+"""Benchmark one TAPS verification round (selection + tree attention + acceptance walk).
+
+    python bench.py [--steps K] [--warmup W] [--config qwen3_8b] [--eager] [--no-cpu-baseline]
+
+A step is one whole round over one batch: taps_select (vocab top-K, Eq. 1-3,
+Alg. 1), tree_verify_attn and accept_walk, launched on one stream.  Inputs are
+seeded synthetic rounds from ``workloads`` (see the design doc for the recipe), held in
+HBM before timing; several independent input sets rotate so that the 256 MB
+Infinity Cache cannot hold the working set.  Rounds are replayed from one HIP
+graph per input set (``--eager`` launches them directly).
+
+Prints one JSON line.  ``value`` is rounds/s (requests x steps per second);
+``roofline`` covers the dominant kernel (the main tree-attention kernel), timed
+with HIP events around that kernel alone in a separate pass of the same
+launches; ``cpu_baseline`` times the CPU oracle on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = ("verification rounds/sec (select+tree-attn+accept) and achieved HBM GB/s, "
+          "Qwen3-8B shape")
+HBM_PEAK_GBS = 8000.0
+MALL_BYTES = 256 << 20
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=300)
+    ap.add_argument("--warmup", type=int, default=30)
+    ap.add_argument("--config", default="qwen3_8b")
+    ap.add_argument("--sets", type=int, default=0, help="input sets to rotate (0: enough to exceed the MALL)")
+    ap.add_argument("--eager", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=20.0)
+    return ap.parse_args()
+
+
+def algorithmic_bytes(cfg, ctx_len, n_nodes):
+    """Bytes the method must move per round: each marginal once, each KV row of the
+    context and of the selected nodes once per KV head (K and V), Q and O of the
+    selected nodes once."""
+    es = 2 if cfg.dtype == 0 else 4
+    marg = cfg.batch * cfg.block * cfg.vocab * es
+    kv = sum(int(c) + int(n) for c, n in zip(ctx_len, n_nodes)) * cfg.Hkv * cfg.head_dim * es * 2
+    qo = sum(int(n) for n in n_nodes) * cfg.Hq * cfg.head_dim * es * 2
+    return marg, kv, qo
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus "
+              f"{args.gpus}); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2606_00487_amd as taps
+    from workloads import BF16, CONFIGS, gen_round, target_tokens
+
+    taps.load()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = CONFIGS[args.config]
+    bf = cfg.dtype == BF16
+
+    def to_dev(a):
+        a = np.ascontiguousarray(a)
+        if bf:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    # ---------------- input sets
+    inp0 = gen_round(cfg, with_attention=True)
+    set_bytes = (inp0.marginals.nbytes + inp0.Q.nbytes + inp0.K.nbytes + inp0.V.nbytes)
+    nsets = args.sets or max(1, min(16, -(-(MALL_BYTES + (MALL_BYTES >> 2)) // set_bytes)))
+    if set_bytes > MALL_BYTES:
+        nsets = args.sets or 1
+    max_ctx = int(max(gen_round(cfg, seed=inp0.seed + k, with_attention=False).ctx_len.max()
+                      for k in range(nsets)))
+    sel = taps.Selector(cfg.batch, cfg.block, cfg.vocab, cfg.K, cfg.budget, dtype=cfg.dtype,
+                        kind=cfg.kind, lambda1=cfg.lambda1, lambda2=cfg.lambda2, tau=cfg.tau,
+                        beta=cfg.beta)
+    att = taps.TreeAttention(cfg.batch, cfg.budget, cfg.Hq, cfg.Hkv, cfg.head_dim, max_ctx,
+                             dtype=cfg.dtype, scale=cfg.scale)
+    walk = taps.AcceptWalk(cfg.batch, cfg.budget, cfg.block)
+    sets = []
+    for k in range(nsets):
+        inp = inp0 if k == 0 else gen_round(cfg, seed=inp0.seed + k)
+        s = dict(inp=inp, marg=to_dev(inp.marginals), Q=to_dev(inp.Q), K=to_dev(inp.K),
+                 V=to_dev(inp.V), off=torch.from_numpy(inp.kv_offset).to(dev),
+                 ctx=torch.from_numpy(inp.ctx_len).to(dev),
+                 tree=taps.TreeBuffers.empty(cfg.batch, cfg.block, cfg.K, cfg.budget, dev),
+                 O=torch.empty((cfg.batch, cfg.budget, cfg.Hq, cfg.head_dim),
+                               dtype=torch.bfloat16 if bf else torch.float32, device=dev))
+        # the synthetic target tokens follow the selected tree: one untimed selection
+        sel(s["marg"], s["tree"])
+        torch.cuda.synchronize()
+        par = s["tree"].parent.cpu().numpy()
+        rnk = s["tree"].rank.cpu().numpy()
+        nn = s["tree"].n_nodes.cpu().numpy()
+        top1 = s["tree"].topk_idx.cpu().numpy()[:, :, 0]
+        tok = s["tree"].token.cpu().numpy()
+        tgt = np.stack([target_tokens(cfg, b, par[b], rnk[b], int(nn[b]), top1[b], inp.p_acc[b],
+                                      seed=inp.seed, token=tok[b]) for b in range(cfg.batch)])
+        s["tgt"] = torch.from_numpy(tgt.astype(np.int32)).to(dev)
+        s["n"] = nn.copy()
+        sets.append(s)
+        print(f"[bench] input set {k + 1}/{nsets} ready (n_nodes {nn.tolist()[:4]}...)",
+              file=sys.stderr, flush=True)
+
+    def round_(s, events=None):
+        sel(s["marg"], s["tree"])
+        att(s["Q"], s["K"], s["V"], s["off"], s["ctx"], s["tree"].parent, s["tree"].n_nodes,
+            out=s["O"], events=events)
+        walk(s["tree"], s["tgt"])
+
+    stream = torch.cuda.Stream()
+    graphs = []
+    with torch.cuda.stream(stream):
+        for s in sets:                      # warm once before capture
+            round_(s)
+        torch.cuda.synchronize()
+        if not args.eager:
+            for s in sets:
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=stream):
+                    round_(s)
+                graphs.append(g)
+        torch.cuda.synchronize()
+
+        def step(i):
+            if args.eager:
+                round_(sets[i % nsets])
+            else:
+                graphs[i % nsets].replay()
+
+        for i in range(args.warmup):
+            step(i)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            step(i)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        elapsed = t1 - t0
+
+        # ---------------- per-stage timing pass (eager, same launches, HIP events)
+        reps = max(nsets, min(args.steps, 200))
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(reps)]
+        for e in ev:                          # materialise the event handles
+            for x in e:
+                x.record(stream)
+        torch.cuda.synchronize()
+        for r in range(reps):
+            s = sets[r % nsets]
+            e = ev[r]
+            e[0].record(stream)
+            sel(s["marg"], s["tree"])
+            e[1].record(stream)
+            att(s["Q"], s["K"], s["V"], s["off"], s["ctx"], s["tree"].parent, s["tree"].n_nodes,
+                out=s["O"], events=(e[2], e[3]))
+            e[4].record(stream)
+            walk(s["tree"], s["tgt"])
+            e[5].record(stream)
+        torch.cuda.synchronize()
+    t_sel = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e3
+    t_attn = float(np.mean([e[2].elapsed_time(e[3]) for e in ev])) * 1e3
+    t_attn_call = float(np.mean([e[1].elapsed_time(e[4]) for e in ev])) * 1e3
+    t_walk = float(np.mean([e[4].elapsed_time(e[5]) for e in ev])) * 1e3
+
+    # ---------------- bytes and roofline
+    per_set = [algorithmic_bytes(cfg, s["inp"].ctx_len, s["n"]) for s in sets]
+    marg_b = float(np.mean([p[0] for p in per_set]))
+    kv_b = float(np.mean([p[1] for p in per_set]))
+    qo_b = float(np.mean([p[2] for p in per_set]))
+    round_bytes = marg_b + kv_b + qo_b
+    attn_bytes = kv_b + qo_b
+    ms_per_step = elapsed / args.steps * 1e3
+    rounds_per_s = cfg.batch * args.steps / elapsed
+    achieved = attn_bytes / (t_attn * 1e-6) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(rounds_per_s, 2),
+        "unit": "rounds/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{cfg.name}: batch {cfg.batch}, marginals [{cfg.block}, {cfg.vocab}] "
+                        f"{'bf16 logits' if bf else 'fp32 probs'}, top-{cfg.K}, budget {cfg.budget}, "
+                        f"{cfg.Hq}/{cfg.Hkv} heads x {cfg.head_dim}, context {int(s['inp'].ctx_len.max())}",
+            "global_batch": cfg.batch,
+            "budget": cfg.budget,
+            "input_sets": nsets,
+            "graph": not args.eager,
+        },
+        "hbm_gbs_round": round(round_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "round_bytes": int(round_bytes),
+        "stages_us": {"select": round(t_sel, 2), "attn_main_kernel": round(t_attn, 2),
+                      "attn_call": round(t_attn_call, 2), "walk": round(t_walk, 2)},
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "attn_bf16_kernel" if bf else "attn_f32_kernel",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "bytes_per_launch": int(attn_bytes),
+            "avg_launch_us": round(t_attn, 3),
+        },
+        "round_roofline_frac": round((round_bytes / HBM_PEAK_GBS / 1e3) / (ms_per_step * 1e3), 4),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, sets[0]["inp"], args.cpu_budget_s)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(cfg, inp, budget_s):
+    """The oracle as it stands, on this host, over a bounded sample of one round."""
+    import oracle
+    from workloads import target_tokens
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl missing
+        threads = 1
+    x = inp.marginals_f64()
+    t0 = time.perf_counter()
+    trees = [oracle.select_request(x[b], cfg.K, cfg.budget, kind=cfg.kind, lambda1=cfg.lambda1,
+                                   lambda2=cfg.lambda2, tau=cfg.tau, beta=cfg.beta)
+             for b in range(cfg.batch)]
+    t_sel = time.perf_counter() - t0
+    Qd, Kd, Vd = inp.qkv_f64()
+    rows = [(b, i, h) for b in range(cfg.batch) for i in range(trees[b].n) for h in range(cfg.Hq)]
+    t0 = time.perf_counter()
+    done = 0
+    chunk = max(1, cfg.Hq)
+    while done < len(rows) and time.perf_counter() - t0 < budget_s:
+        oracle.tree_attention(Qd, Kd, Vd, inp.kv_offset, inp.ctx_len, [t.parent for t in trees],
+                              [t.n for t in trees], cfg.scale, samples=rows[done:done + chunk])
+        done += chunk
+    done = min(done, len(rows))
+    t_attn = (time.perf_counter() - t0) * len(rows) / done
+    t0 = time.perf_counter()
+    for b, t in enumerate(trees):
+        tgt = target_tokens(cfg, b, t.parent, t.rank, t.n, t.topk_idx[:, 0], inp.p_acc[b])
+        oracle.accept_walk(t.parent, t.token, t.n, tgt)
+    t_walk = time.perf_counter() - t0
+    per_round = t_sel + t_attn + t_walk
+    return {
+        "value": round(cfg.batch / per_round, 5),
+        "unit": "rounds/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"one round of {cfg.name}: full selection ({t_sel:.2f} s), attention on "
+                   f"{done}/{len(rows)} (node, head) rows extrapolated to all ({t_attn:.1f} s), "
+                   f"walk ({t_walk:.3f} s); fp64 NumPy"),
+    }
+
+
+if __name__ == "__main__":
+    main()

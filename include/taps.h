@@ -1,0 +1,184 @@
+/* taps.h -- C ABI of the TAPS draft-tree verification hot path on MI355X (gfx950).
+ *
+ * One decoding round of TAPS (Target-Aware Prefix Tree Selection, arXiv 2606.00487):
+ *   taps_select       per-position top-K of the drafter marginals (Sec. 4.1, Stage 1),
+ *                     sibling-softmax edge probabilities q_cond (Eq. 1), reach
+ *                     probabilities q_reach (Eq. 2), utility (Eq. 3) and the greedy
+ *                     budgeted prefix-closed selection of Alg. 1.
+ *   tree_verify_attn  tree-masked verification attention: every selected node attends
+ *                     to the cached context and to its own ancestors (Sec. 4.1 Stage 3,
+ *                     Sec. 4.3: verification needs a connected subtree at the root).
+ *   accept_walk       greedy (temperature 0) acceptance of the longest matching root
+ *                     path (Sec. 1: one prefix path is committed per round; Limitations).
+ *
+ * Conventions shared by every call:
+ *   - Pointers are DEVICE memory owned by the caller unless marked [host].
+ *   - Calls validate their arguments on the host, then enqueue kernels on `stream`.
+ *     They never synchronize, never allocate, and keep no state between calls.
+ *   - Invalid arguments return an error before anything is enqueued.  A failed kernel
+ *     launch returns TAPS_ERR_HIP.  Kernels never trap: pathological data (NaN, +-inf,
+ *     empty rows) produces the defined outputs documented per call.
+ *   - Workspace sizes are pure functions of the host-side sizes.  A workspace may be
+ *     reused by consecutive calls on one stream; concurrent calls need their own.
+ */
+#ifndef TAPS_H
+#define TAPS_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TAPS_OK = 0,
+  TAPS_ERR_INVALID_ARG = -1,  /* null pointer, size out of range, misaligned buffer */
+  TAPS_ERR_UNSUPPORTED = -2,  /* valid request this build does not implement      */
+  TAPS_ERR_WORKSPACE = -3,    /* workspace missing or smaller than required        */
+  TAPS_ERR_HIP = -4           /* a kernel launch failed (hipGetLastError)          */
+} taps_status;
+
+typedef enum { TAPS_BF16 = 0, TAPS_FP32 = 1 } taps_dtype;
+typedef enum { TAPS_LOGITS = 0, TAPS_PROBS = 1 } taps_kind;
+
+/* Limits of this build. */
+#define TAPS_MAX_BLOCK 32    /* draft positions D (tree depth)              */
+#define TAPS_MAX_K 16        /* candidates per position                     */
+#define TAPS_MAX_BUDGET 256  /* N_max, root included                        */
+
+/* [host] Selection parameters (Sec. 4.1 Stage 1 and 3; Eq. 3; Alg. 1).
+ *   batch    requests B >= 0 (0: nothing is enqueued)
+ *   block    draft positions D, 1..TAPS_MAX_BLOCK; row i of a request's marginals is the
+ *            distribution of the token at tree depth i+1 (the root, depth 0, is the
+ *            current position and carries no drafted token)
+ *   vocab    V >= K
+ *   K        candidates per position, 1..TAPS_MAX_K
+ *   budget   N_max, 1..TAPS_MAX_BUDGET; the root counts toward it
+ *   dtype    TAPS_BF16 or TAPS_FP32 marginals
+ *   kind     TAPS_LOGITS: the edge logit of a child is beta * (its drafter logit);
+ *            TAPS_PROBS: the marginals are probabilities, used as the sibling weights
+ *            directly (beta must be 1)
+ *   lambda1  > 0, finite: per-node cost in Eq. 3
+ *   lambda2  >= 0, finite: per-depth cost in Eq. 3 (negative values: UNSUPPORTED)
+ *   tau      minimum utility; a node is added only while its utility is > tau (not NaN)
+ *   beta     >= 0, finite scorer temperature for LOGITS */
+typedef struct {
+  int32_t batch, block, vocab, K, budget;
+  int32_t dtype, kind;
+  double lambda1, lambda2, tau, beta;
+} taps_select_params;
+
+/* Selected subtree S per request, in selection order (a parent always precedes its
+ * children).  Arrays are [batch][budget] unless noted; slots n..budget-1 hold
+ * parent = token = depth = rank = -1 and q_reach = 0.
+ *   parent    index of the parent node within the request; -1 at the root (index 0)
+ *   token     vocabulary id; -1 at the root
+ *   depth     0 at the root
+ *   rank      rank of the token in its position's top-K; -1 at the root
+ *   q_reach   Eq. 2 reach probability, fp64; 1.0 at the root
+ *   n_nodes   [batch] number of selected nodes n, 1 <= n <= budget
+ *   topk_idx  [batch][block][K] top-K vocabulary ids per position: value descending,
+ *             then index ascending; -0 equals +0; NaN ranks below -inf
+ *   topk_val  [batch][block][K] their marginal values widened to float (exact), or NULL */
+typedef struct {
+  int32_t *parent;
+  int32_t *token;
+  int32_t *depth;
+  int32_t *rank;
+  double *q_reach;
+  int32_t *n_nodes;
+  int32_t *topk_idx;
+  float *topk_val;
+} taps_tree;
+
+/* Bytes of scratch taps_select needs (per-chunk top-K candidates). */
+size_t taps_select_workspace_bytes(const taps_select_params *p);
+
+/* Host-only check of the parameters, no device access (the first step of taps_select). */
+taps_status taps_select_validate(const taps_select_params *p);
+
+/* Target-aware selection (Sec. 4.1-4.3, Eq. 1-3, Alg. 1) for `batch` requests.
+ *   marginals  [batch][block][vocab] bf16 or fp32, row-major, 16-byte aligned base
+ *   out        device arrays described at taps_tree ([host] struct)
+ * Edge probability of a rank-r child of any depth-i node (sibling softmax, Eq. 1):
+ *   LOGITS  e_r = EXP(beta * (x_r - x_0)), PROBS  e_r = x_r if x_r > 0 else 0;
+ *   Z = e_0 + e_1 + ... (in rank order); q_cond = e_r / Z, or 0 when Z is 0 or not finite.
+ * EXP is the shared fp64 exponential (Cody-Waite reduction, degree-13 Taylor, no FMA).
+ * q_reach multiplies q_cond along the path (Eq. 2); utility = q_reach / (lambda1 +
+ * lambda2 * depth) (Eq. 3); all in IEEE fp64.  Ties in the greedy argmax of Alg. 1 go to
+ * the shallower node, then to the lexicographically smaller rank path. */
+taps_status taps_select(const void *marginals, const taps_select_params *p,
+                        const taps_tree *out, void *ws, size_t ws_bytes,
+                        hipStream_t stream);
+
+/* Bytes of scratch tree_verify_attn needs (split-KV partial outputs). */
+size_t tree_verify_attn_workspace_bytes(int32_t batch, int32_t budget, int32_t Hq,
+                                        int32_t Hkv, int32_t head_dim, int32_t max_ctx,
+                                        int32_t dtype);
+
+/* Host-only check of the attention sizes, no device access. */
+taps_status tree_verify_attn_validate(int32_t batch, int32_t budget, int32_t Hq,
+                                      int32_t Hkv, int32_t head_dim, int32_t max_ctx,
+                                      int32_t dtype, float scale);
+
+/* Tree-masked verification attention for `batch` requests.
+ *   Q_tree       [batch][budget][Hq][head_dim] queries of the tree nodes (tree order)
+ *   K_cache,
+ *   V_cache      [rows][Hkv][head_dim]; request b owns rows kv_offset[b] ..
+ *                kv_offset[b] + ctx_len[b] + budget - 1: its context first, then one
+ *                reserved row per tree node i at kv_offset[b] + ctx_len[b] + i
+ *   kv_offset    [batch] int64 first cache row of each request
+ *   ctx_len      [batch] context rows; values outside [0, max_ctx] are clamped to it
+ *   tree_parent  [batch][budget] parent index per node (taps_tree.parent); a node whose
+ *                parent is not in [0, i) sees only the context and itself
+ *   n_nodes      [batch] nodes to compute; clamped to [0, budget]
+ *   head_dim     64 or 128; Hq a multiple of Hkv; query head h reads KV head h/(Hq/Hkv)
+ *   max_ctx      [host] upper bound of ctx_len, sizes the grid
+ *   dtype        TAPS_BF16 (fp32 accumulation, output rounded to nearest even) or TAPS_FP32
+ *   scale        softmax scale, finite (usually 1/sqrt(head_dim))
+ *   O            [batch][budget][Hq][head_dim] same dtype as Q; rows i >= n are not written
+ * O[b,i,h] = softmax_j(scale * Q[b,i,h] . K[j,g]) V[j,g] over the context rows and the
+ * ancestor-or-self tree rows of node i, g = h / (Hq/Hkv). */
+taps_status tree_verify_attn(const void *Q_tree, const void *K_cache, const void *V_cache,
+                             const int64_t *kv_offset, const int32_t *ctx_len,
+                             const int32_t *tree_parent, const int32_t *n_nodes,
+                             int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv,
+                             int32_t head_dim, int32_t max_ctx, int32_t dtype, float scale,
+                             void *O, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* tree_verify_attn that also records `ev_begin` on `stream` right before its main attention
+ * kernel and `ev_end` right after it (before the split combine), so a caller can time that
+ * kernel alone with hipEventElapsedTime.  Either event may be NULL.  For profiling callers. */
+taps_status tree_verify_attn_timed(const void *Q_tree, const void *K_cache, const void *V_cache,
+                                   const int64_t *kv_offset, const int32_t *ctx_len,
+                                   const int32_t *tree_parent, const int32_t *n_nodes,
+                                   int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv,
+                                   int32_t head_dim, int32_t max_ctx, int32_t dtype,
+                                   float scale, void *O, void *ws, size_t ws_bytes,
+                                   hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_end);
+
+/* Greedy acceptance walk (temperature 0).
+ *   tree           [host] struct; parent, token and n_nodes are read
+ *   target_tokens  [batch][budget] target model's greedy token after each node
+ *   path           [batch][block+1] accepted node indices from the root, -1 padded
+ *   path_len       [batch] accepted nodes including the root (1 .. block+1)
+ *   bonus          [batch] target token after the last accepted node
+ * A node is accepted when its token equals the target token after its parent and its
+ * parent is accepted; the root always is. */
+taps_status accept_walk(const taps_tree *tree, int32_t batch, int32_t budget,
+                        int32_t block, const int32_t *target_tokens, int32_t *path,
+                        int32_t *path_len, int32_t *bonus, hipStream_t stream);
+
+/* Human-readable name of a status code (static string). */
+const char *taps_status_string(int32_t status);
+
+/* Host evaluation of the shared fp64 exponential used on the device, for testing the
+ * definition against other implementations without a GPU. */
+double taps_spec_exp_host(double t);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TAPS_H */

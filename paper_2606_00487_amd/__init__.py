@@ -1,0 +1,158 @@
+"""TAPS draft-tree verification hot path on MI355X (gfx950).
+
+Thin Python binding over libtaps.so (include/taps.h): argument marshalling
+only, every step of the path runs in the HIP kernels.  PyTorch provides device
+memory and the current stream.
+
+    sel = Selector(batch, block, vocab, K, budget, dtype=BF16, kind=LOGITS)
+    tree = sel(marginals)                       # taps_select
+    att = TreeAttention(batch, budget, Hq, Hkv, head_dim, max_ctx)
+    O = att(Q, K, V, kv_offset, ctx_len, tree.parent, tree.n_nodes)   # tree_verify_attn
+    walk = AcceptWalk(batch, budget, block)
+    path, path_len, bonus = walk(tree, target_tokens)                 # accept_walk
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+
+import torch
+
+from . import _lib
+from ._lib import (TAPS_BF16 as BF16, TAPS_FP32 as FP32, TAPS_LOGITS as LOGITS,  # noqa: F401
+                   TAPS_PROBS as PROBS, TapsError, load)
+
+_TORCH_DT = {BF16: torch.bfloat16, FP32: torch.float32}
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _need(t: torch.Tensor, name: str, dtype, shape=None):
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise TypeError(f"{name}: expected a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+@dataclasses.dataclass
+class TreeBuffers:
+    """Device arrays of taps_tree (see include/taps.h)."""
+    parent: torch.Tensor
+    token: torch.Tensor
+    depth: torch.Tensor
+    rank: torch.Tensor
+    q_reach: torch.Tensor
+    n_nodes: torch.Tensor
+    topk_idx: torch.Tensor
+    topk_val: torch.Tensor
+
+    @staticmethod
+    def empty(batch, block, K, budget, device="cuda"):
+        i32 = dict(dtype=torch.int32, device=device)
+        return TreeBuffers(
+            parent=torch.empty(batch, budget, **i32), token=torch.empty(batch, budget, **i32),
+            depth=torch.empty(batch, budget, **i32), rank=torch.empty(batch, budget, **i32),
+            q_reach=torch.empty(batch, budget, dtype=torch.float64, device=device),
+            n_nodes=torch.empty(batch, **i32), topk_idx=torch.empty(batch, block, K, **i32),
+            topk_val=torch.empty(batch, block, K, dtype=torch.float32, device=device))
+
+    def struct(self) -> _lib.Tree:
+        return _lib.Tree(_ptr(self.parent), _ptr(self.token), _ptr(self.depth), _ptr(self.rank),
+                         _ptr(self.q_reach), _ptr(self.n_nodes), _ptr(self.topk_idx),
+                         _ptr(self.topk_val))
+
+
+class Selector:
+    """taps_select: top-K, Eq. 1-3 and the budgeted prefix-closed selection of Alg. 1."""
+
+    def __init__(self, batch, block, vocab, K, budget, dtype=BF16, kind=LOGITS, lambda1=1.0,
+                 lambda2=0.125, tau=0.0, beta=1.0, device="cuda"):
+        self.lib = load()
+        self.p = _lib.SelectParams(batch, block, vocab, K, budget, dtype, kind, lambda1, lambda2,
+                                   tau, beta)
+        _lib.check(self.lib, "taps_select_validate", self.lib.taps_select_validate(ctypes.byref(self.p)))
+        self.ws_bytes = self.lib.taps_select_workspace_bytes(ctypes.byref(self.p))
+        self.ws = torch.empty(max(self.ws_bytes, 8), dtype=torch.uint8, device=device)
+        self.tree = TreeBuffers.empty(batch, block, K, budget, device)
+        self._tree_struct = self.tree.struct()
+
+    def __call__(self, marginals: torch.Tensor, tree: TreeBuffers | None = None) -> TreeBuffers:
+        p = self.p
+        _need(marginals, "marginals", _TORCH_DT[p.dtype], (p.batch, p.block, p.vocab))
+        t = tree or self.tree
+        st = t.struct() if tree is not None else self._tree_struct
+        _lib.check(self.lib, "taps_select",
+                   self.lib.taps_select(_ptr(marginals), ctypes.byref(p), ctypes.byref(st),
+                                        _ptr(self.ws), self.ws_bytes, _stream()))
+        return t
+
+
+class TreeAttention:
+    """tree_verify_attn: tree-masked verification attention."""
+
+    def __init__(self, batch, budget, Hq, Hkv, head_dim, max_ctx, dtype=BF16, scale=None,
+                 device="cuda"):
+        self.lib = load()
+        self.shape = (batch, budget, Hq, Hkv, head_dim, max_ctx, dtype)
+        self.scale = float(scale if scale is not None else head_dim ** -0.5)
+        _lib.check(self.lib, "tree_verify_attn_validate",
+                   self.lib.tree_verify_attn_validate(batch, budget, Hq, Hkv, head_dim, max_ctx,
+                                                      dtype, self.scale))
+        self.ws_bytes = self.lib.tree_verify_attn_workspace_bytes(batch, budget, Hq, Hkv,
+                                                                  head_dim, max_ctx, dtype)
+        self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device=device)
+
+    def __call__(self, Q, K, V, kv_offset, ctx_len, parent, n_nodes, out=None, events=None):
+        """events: optional (begin, end) torch.cuda.Event pair recorded around the main
+        attention kernel only (tree_verify_attn_timed)."""
+        batch, budget, Hq, Hkv, hd, max_ctx, dtype = self.shape
+        tdt = _TORCH_DT[dtype]
+        _need(Q, "Q_tree", tdt, (batch, budget, Hq, hd))
+        _need(K, "K_cache", tdt)
+        _need(V, "V_cache", tdt, tuple(K.shape))
+        if K.dim() != 3 or K.shape[1:] != (Hkv, hd):
+            raise ValueError(f"K_cache: expected [rows, {Hkv}, {hd}], got {tuple(K.shape)}")
+        _need(kv_offset, "kv_offset", torch.int64, (batch,))
+        _need(ctx_len, "ctx_len", torch.int32, (batch,))
+        _need(parent, "tree_parent", torch.int32, (batch, budget))
+        _need(n_nodes, "n_nodes", torch.int32, (batch,))
+        O = out if out is not None else torch.empty_like(Q)
+        _need(O, "O", tdt, (batch, budget, Hq, hd))
+        args = (_ptr(Q), _ptr(K), _ptr(V), _ptr(kv_offset), _ptr(ctx_len), _ptr(parent),
+                _ptr(n_nodes), batch, budget, Hq, Hkv, hd, max_ctx, dtype, self.scale, _ptr(O),
+                _ptr(self.ws), self.ws_bytes, _stream())
+        if events is None:
+            _lib.check(self.lib, "tree_verify_attn", self.lib.tree_verify_attn(*args))
+        else:
+            _lib.check(self.lib, "tree_verify_attn_timed", self.lib.tree_verify_attn_timed(
+                *args, events[0].cuda_event, events[1].cuda_event))
+        return O
+
+
+class AcceptWalk:
+    """accept_walk: greedy acceptance of the longest matching root path."""
+
+    def __init__(self, batch, budget, block, device="cuda"):
+        self.lib = load()
+        self.batch, self.budget, self.block = batch, budget, block
+        self.path = torch.empty(batch, block + 1, dtype=torch.int32, device=device)
+        self.path_len = torch.empty(batch, dtype=torch.int32, device=device)
+        self.bonus = torch.empty(batch, dtype=torch.int32, device=device)
+
+    def __call__(self, tree: TreeBuffers, target_tokens: torch.Tensor):
+        _need(target_tokens, "target_tokens", torch.int32, (self.batch, self.budget))
+        st = tree.struct()
+        _lib.check(self.lib, "accept_walk", self.lib.accept_walk(
+            ctypes.byref(st), self.batch, self.budget, self.block, _ptr(target_tokens),
+            _ptr(self.path), _ptr(self.path_len), _ptr(self.bonus), _stream()))
+        return self.path, self.path_len, self.bonus

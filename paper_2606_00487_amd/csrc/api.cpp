@@ -1,0 +1,170 @@
+// C ABI entry points: host-side validation, workspace sizing and kernel dispatch.
+#include <cmath>
+#include <cstdint>
+
+#include "common.h"
+
+using namespace taps;
+
+namespace {
+
+constexpr int kMaxChunks = 64;  // per-row chunk lists the selection kernel merges
+
+bool finite(double x) { return std::isfinite(x); }
+
+taps_status select_check(const taps_select_params* p) {
+  if (!p) return TAPS_ERR_INVALID_ARG;
+  if (p->batch < 0) return TAPS_ERR_INVALID_ARG;
+  if (p->dtype != TAPS_BF16 && p->dtype != TAPS_FP32) return TAPS_ERR_INVALID_ARG;
+  if (p->kind != TAPS_LOGITS && p->kind != TAPS_PROBS) return TAPS_ERR_INVALID_ARG;
+  if (p->block < 1 || p->K < 1 || p->budget < 1 || p->vocab < 1) return TAPS_ERR_INVALID_ARG;
+  if (p->block > TAPS_MAX_BLOCK || p->K > TAPS_MAX_K || p->budget > TAPS_MAX_BUDGET)
+    return TAPS_ERR_UNSUPPORTED;
+  if (p->K > p->vocab) return TAPS_ERR_INVALID_ARG;
+  if (!finite(p->lambda1) || !(p->lambda1 > 0.0)) return TAPS_ERR_INVALID_ARG;
+  if (!finite(p->lambda2)) return TAPS_ERR_INVALID_ARG;
+  if (p->lambda2 < 0.0) return TAPS_ERR_UNSUPPORTED;
+  if (std::isnan(p->tau)) return TAPS_ERR_INVALID_ARG;
+  if (!finite(p->beta) || p->beta < 0.0) return TAPS_ERR_INVALID_ARG;
+  if (p->kind == TAPS_PROBS && p->beta != 1.0) return TAPS_ERR_UNSUPPORTED;
+  const int64_t rows = (int64_t)p->batch * p->block;
+  if (rows > (int64_t)1 << 20) return TAPS_ERR_UNSUPPORTED;
+  const TopkPlan plan = plan_topk(p->vocab, (int)rows > 0 ? (int)rows : 1, p->dtype);
+  if (plan.chunks > kMaxChunks) return TAPS_ERR_UNSUPPORTED;
+  return TAPS_OK;
+}
+
+taps_status attn_check(int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv, int32_t hd,
+                       int32_t max_ctx, int32_t dtype, float scale) {
+  if (batch < 0 || budget < 1 || Hq < 1 || Hkv < 1 || max_ctx < 0) return TAPS_ERR_INVALID_ARG;
+  if (budget > TAPS_MAX_BUDGET) return TAPS_ERR_UNSUPPORTED;
+  if (Hq % Hkv != 0) return TAPS_ERR_INVALID_ARG;
+  if (dtype != TAPS_BF16 && dtype != TAPS_FP32) return TAPS_ERR_INVALID_ARG;
+  if (hd != 64 && hd != 128) return TAPS_ERR_UNSUPPORTED;
+  if (!std::isfinite(scale)) return TAPS_ERR_INVALID_ARG;
+  if ((int64_t)max_ctx + budget > (int64_t)1 << 30) return TAPS_ERR_UNSUPPORTED;
+  if ((int64_t)batch * Hkv > 65535 || (int64_t)budget * Hq / Hkv > (int64_t)1 << 20)
+    return TAPS_ERR_UNSUPPORTED;
+  return TAPS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* taps_status_string(int32_t s) {
+  switch (s) {
+    case TAPS_OK: return "TAPS_OK";
+    case TAPS_ERR_INVALID_ARG: return "TAPS_ERR_INVALID_ARG";
+    case TAPS_ERR_UNSUPPORTED: return "TAPS_ERR_UNSUPPORTED";
+    case TAPS_ERR_WORKSPACE: return "TAPS_ERR_WORKSPACE";
+    case TAPS_ERR_HIP: return "TAPS_ERR_HIP";
+    default: return "TAPS_UNKNOWN_STATUS";
+  }
+}
+
+double taps_spec_exp_host(double t) { return spec_exp_host(t); }
+
+taps_status taps_select_validate(const taps_select_params* p) { return select_check(p); }
+
+size_t taps_select_workspace_bytes(const taps_select_params* p) {
+  if (select_check(p) != TAPS_OK || p->batch == 0) return 0;
+  const int rows = p->batch * p->block;
+  const TopkPlan plan = plan_topk(p->vocab, rows, p->dtype);
+  return (size_t)rows * plan.chunks * p->K * sizeof(uint64_t);
+}
+
+taps_status taps_select(const void* marginals, const taps_select_params* p, const taps_tree* out,
+                        void* ws, size_t ws_bytes, hipStream_t stream) {
+  const taps_status st = select_check(p);
+  if (st != TAPS_OK) return st;
+  if (p->batch == 0) return TAPS_OK;
+  if (!marginals || !out || !out->parent || !out->token || !out->depth || !out->rank ||
+      !out->q_reach || !out->n_nodes || !out->topk_idx)
+    return TAPS_ERR_INVALID_ARG;
+  if (((uintptr_t)marginals & 15) != 0) return TAPS_ERR_INVALID_ARG;
+  const size_t need = taps_select_workspace_bytes(p);
+  if (!ws || ws_bytes < need || ((uintptr_t)ws & 7) != 0) return TAPS_ERR_WORKSPACE;
+  const int rows = p->batch * p->block;
+  const TopkPlan plan = plan_topk(p->vocab, rows, p->dtype);
+  if (launch_topk_chunks(marginals, p->dtype, rows, p->vocab, p->K, plan, (uint64_t*)ws,
+                         stream) != hipSuccess)
+    return TAPS_ERR_HIP;
+  if (launch_select(marginals, *p, plan, (const uint64_t*)ws, *out, stream) != hipSuccess)
+    return TAPS_ERR_HIP;
+  return TAPS_OK;
+}
+
+taps_status tree_verify_attn_validate(int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv,
+                                      int32_t head_dim, int32_t max_ctx, int32_t dtype,
+                                      float scale) {
+  return attn_check(batch, budget, Hq, Hkv, head_dim, max_ctx, dtype, scale);
+}
+
+size_t tree_verify_attn_workspace_bytes(int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv,
+                                        int32_t head_dim, int32_t max_ctx, int32_t dtype) {
+  if (attn_check(batch, budget, Hq, Hkv, head_dim, max_ctx, dtype, 1.0f) != TAPS_OK) return 0;
+  if (dtype == TAPS_FP32 || batch == 0) return 0;
+  const AttnPlan pl = plan_attn(batch, budget, Hq, Hkv, head_dim, max_ctx);
+  return attn_ws_bytes(pl, batch, budget, Hq, Hkv, head_dim);
+}
+
+taps_status tree_verify_attn_timed(const void* Q_tree, const void* K_cache, const void* V_cache,
+                                   const int64_t* kv_offset, const int32_t* ctx_len,
+                                   const int32_t* tree_parent, const int32_t* n_nodes,
+                                   int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv,
+                                   int32_t head_dim, int32_t max_ctx, int32_t dtype, float scale,
+                                   void* O, void* ws, size_t ws_bytes, hipStream_t stream,
+                                   hipEvent_t ev_begin, hipEvent_t ev_end) {
+  const taps_status st = attn_check(batch, budget, Hq, Hkv, head_dim, max_ctx, dtype, scale);
+  if (st != TAPS_OK) return st;
+  if (batch == 0) return TAPS_OK;
+  if (!Q_tree || !K_cache || !V_cache || !kv_offset || !ctx_len || !tree_parent || !n_nodes || !O)
+    return TAPS_ERR_INVALID_ARG;
+  const uintptr_t align_or = (uintptr_t)Q_tree | (uintptr_t)K_cache | (uintptr_t)V_cache | (uintptr_t)O;
+  if ((align_or & 15) != 0) return TAPS_ERR_INVALID_ARG;
+  if (dtype == TAPS_FP32) {
+    return launch_attn_f32((const float*)Q_tree, (const float*)K_cache, (const float*)V_cache,
+                           kv_offset, ctx_len, tree_parent, n_nodes, batch, budget, Hq, Hkv,
+                           head_dim, max_ctx, scale, (float*)O, stream, ev_begin,
+                           ev_end) == hipSuccess
+               ? TAPS_OK
+               : TAPS_ERR_HIP;
+  }
+  const size_t need = tree_verify_attn_workspace_bytes(batch, budget, Hq, Hkv, head_dim, max_ctx, dtype);
+  if (!ws || ws_bytes < need || ((uintptr_t)ws & 15) != 0) return TAPS_ERR_WORKSPACE;
+  const AttnPlan pl = plan_attn(batch, budget, Hq, Hkv, head_dim, max_ctx);
+  return launch_attn_bf16(Q_tree, K_cache, V_cache, kv_offset, ctx_len, tree_parent, n_nodes,
+                          batch, budget, Hq, Hkv, head_dim, max_ctx, scale, pl, O, ws, stream,
+                          ev_begin, ev_end) == hipSuccess
+             ? TAPS_OK
+             : TAPS_ERR_HIP;
+}
+
+taps_status tree_verify_attn(const void* Q_tree, const void* K_cache, const void* V_cache,
+                             const int64_t* kv_offset, const int32_t* ctx_len,
+                             const int32_t* tree_parent, const int32_t* n_nodes, int32_t batch,
+                             int32_t budget, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                             int32_t max_ctx, int32_t dtype, float scale, void* O, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
+  return tree_verify_attn_timed(Q_tree, K_cache, V_cache, kv_offset, ctx_len, tree_parent,
+                                n_nodes, batch, budget, Hq, Hkv, head_dim, max_ctx, dtype, scale,
+                                O, ws, ws_bytes, stream, nullptr, nullptr);
+}
+
+taps_status accept_walk(const taps_tree* tree, int32_t batch, int32_t budget, int32_t block,
+                        const int32_t* target_tokens, int32_t* path, int32_t* path_len,
+                        int32_t* bonus, hipStream_t stream) {
+  if (batch < 0 || budget < 1 || block < 1) return TAPS_ERR_INVALID_ARG;
+  if (budget > TAPS_MAX_BUDGET || block > TAPS_MAX_BLOCK) return TAPS_ERR_UNSUPPORTED;
+  if (batch == 0) return TAPS_OK;
+  if (!tree || !tree->parent || !tree->token || !tree->n_nodes || !target_tokens || !path ||
+      !path_len || !bonus)
+    return TAPS_ERR_INVALID_ARG;
+  return launch_walk(*tree, batch, budget, block, target_tokens, path, path_len, bonus, stream) ==
+                 hipSuccess
+             ? TAPS_OK
+             : TAPS_ERR_HIP;
+}
+
+}  // extern "C"

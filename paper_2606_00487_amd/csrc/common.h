@@ -1,0 +1,71 @@
+// Internal declarations shared by the HIP translation units of libtaps.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include "../../include/taps.h"
+
+namespace taps {
+
+constexpr int kWave = 64;
+
+// ----------------------------------------------------------------------------------
+// Order-preserving keys for marginal values.  A larger key ranks earlier: value
+// descending with -0 == +0 and every NaN below -inf.  The 64-bit candidate key packs
+// (value key << 32) | ~index, so equal values rank by ascending vocabulary index and
+// every key is unique.
+__host__ __device__ inline uint32_t value_key(uint32_t bits) {
+  if ((bits & 0x7FFFFFFFu) > 0x7F800000u) return 0u;  // NaN
+  if (bits == 0x80000000u) bits = 0u;                 // -0 -> +0
+  return (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
+}
+__host__ __device__ inline uint64_t cand_key(uint32_t vkey, uint32_t idx) {
+  return ((uint64_t)vkey << 32) | (uint64_t)(0xFFFFFFFFu - idx);
+}
+__host__ __device__ inline uint32_t cand_index(uint64_t key) {
+  return 0xFFFFFFFFu - (uint32_t)(key & 0xFFFFFFFFu);
+}
+
+// ----------------------------------------------------------------------------------
+// Host launchers (each returns hipGetLastError() of its launch).
+struct TopkPlan {
+  int chunk_len;   // elements per chunk (multiple of 1024)
+  int chunks;      // chunks per row
+  int per_thread;  // elements per thread (chunk_len / 256)
+};
+TopkPlan plan_topk(int vocab, int rows, int dtype);
+
+hipError_t launch_topk_chunks(const void* marg, int dtype, int rows, int vocab, int K,
+                              const TopkPlan& plan, uint64_t* cand, hipStream_t s);
+
+hipError_t launch_select(const void* marg, const taps_select_params& p, const TopkPlan& plan,
+                         const uint64_t* cand, const taps_tree& out, hipStream_t s);
+
+struct AttnPlan {
+  int qb;          // 32-row query blocks per wave (1 or 2)
+  int mtile;       // query rows per workgroup (4 waves)
+  int mtiles;      // workgroups along the budget*G query rows of one KV head
+  int split_len;   // keys per split (multiple of 64)
+  int splits;      // splits along max_ctx + budget keys
+};
+AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max_ctx);
+size_t attn_ws_bytes(const AttnPlan& pl, int batch, int budget, int Hq, int Hkv, int head_dim);
+
+hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const int64_t* off,
+                            const int32_t* ctx, const int32_t* parent, const int32_t* n,
+                            int batch, int budget, int Hq, int Hkv, int head_dim, int max_ctx,
+                            float scale, const AttnPlan& pl, void* O, void* ws, hipStream_t s,
+                            hipEvent_t ev_begin = nullptr, hipEvent_t ev_end = nullptr);
+
+hipError_t launch_attn_f32(const float* Q, const float* K, const float* V, const int64_t* off,
+                           const int32_t* ctx, const int32_t* parent, const int32_t* n,
+                           int batch, int budget, int Hq, int Hkv, int head_dim, int max_ctx,
+                           float scale, float* O, hipStream_t s, hipEvent_t ev_begin = nullptr,
+                           hipEvent_t ev_end = nullptr);
+
+hipError_t launch_walk(const taps_tree& t, int batch, int budget, int block,
+                       const int32_t* target, int32_t* path, int32_t* path_len, int32_t* bonus,
+                       hipStream_t s);
+
+double spec_exp_host(double t);
+
+}  // namespace taps

@@ -1,0 +1,242 @@
+// Vocabulary-scan top-K (Sec. 4.1, Stage 1: the top-K tokens at each draft position).
+//
+// One workgroup scans one chunk of one marginal row and writes the chunk's K best
+// 64-bit candidate keys (value key << 32 | ~index, larger is better, 0 = empty), sorted
+// descending, to the workspace.  The selection kernel merges the chunks of a row.
+//
+// Per wave: every lane holds E values in registers (16-byte coalesced loads).  The
+// K-th largest lane maximum T is found by a bitwise descent with ballots; only values
+// with key >= T can be in the wave's top-K, and there are few of them, so they are
+// compacted into LDS and ranked exactly by counting.  A wave whose compacted set
+// overflows falls back to K rounds of exact wave-wide argmax.  The four wave lists are
+// merged by ranking again.
+#include "common.h"
+
+namespace taps {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
+constexpr int kWaveCap = 128;  // compacted candidates per wave before the fallback
+
+__device__ inline uint64_t shfl_xor_u64(uint64_t v, int m) {
+  uint32_t lo = __shfl_xor((uint32_t)v, m);
+  uint32_t hi = __shfl_xor((uint32_t)(v >> 32), m);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ inline uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    uint64_t o = shfl_xor_u64(v, m);
+    v = o > v ? o : v;
+  }
+  return v;
+}
+
+template <int DT>
+__device__ inline uint32_t elem_bits(const void* row, int64_t i) {
+  if (DT == TAPS_BF16) return (uint32_t)((const uint16_t*)row)[i] << 16;
+  return ((const uint32_t*)row)[i];
+}
+
+// Load element j of this thread: vector path covers 16-byte units u = t + 256*k.
+template <int DT, int E>
+__device__ inline void load_chunk(const void* row, bool aligned, int start, int end, int tid,
+                                  uint32_t (&key)[E]) {
+  constexpr int U = DT == TAPS_BF16 ? 8 : 4;  // elements per 16-byte unit
+  if (aligned) {
+#pragma unroll
+    for (int k = 0; k < E / U; ++k) {
+      const int e0 = start + (tid + kThreads * k) * U;
+      if (e0 + U <= end) {
+        const uint4 w = *(const uint4*)((const char*)row + (int64_t)e0 * (DT == TAPS_BF16 ? 2 : 4));
+        const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+        if (DT == TAPS_BF16) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            key[k * U + 2 * q] = value_key(ww[q] << 16);
+            key[k * U + 2 * q + 1] = value_key(ww[q] & 0xFFFF0000u);
+          }
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) key[k * U + q] = value_key(ww[q]);
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < U; ++q) {
+          const int e = e0 + q;
+          key[k * U + q] = e < end ? value_key(elem_bits<DT>(row, e)) : 0u;
+        }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+      const int e = start + tid + kThreads * j;
+      key[j] = e < end ? value_key(elem_bits<DT>(row, e)) : 0u;
+    }
+  }
+}
+
+template <int DT, int E>
+__device__ inline int elem_index(bool aligned, int start, int tid, int j) {
+  constexpr int U = DT == TAPS_BF16 ? 8 : 4;
+  return aligned ? start + (tid + kThreads * (j / U)) * U + (j % U) : start + tid + kThreads * j;
+}
+
+template <int DT, int E>
+__global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __restrict__ marg,
+                                                              int vocab, int K, int chunk_len,
+                                                              int chunks,
+                                                              uint64_t* __restrict__ cand) {
+  __shared__ uint64_t s_cand[kWaves][kWaveCap];
+  __shared__ uint64_t s_wave_top[kWaves][TAPS_MAX_K];
+  __shared__ int s_over[kWaves];
+
+  const int row = blockIdx.x / chunks;
+  const int chunk = blockIdx.x - row * chunks;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int start = chunk * chunk_len;
+  const int end = min(vocab, start + chunk_len);
+  const size_t es = DT == TAPS_BF16 ? 2 : 4;
+  const void* rowp = (const char*)marg + (size_t)row * vocab * es;
+  const bool aligned = (((uintptr_t)rowp) & 15) == 0;
+
+  uint32_t key[E];
+  load_chunk<DT, E>(rowp, aligned, start, end, tid, key);
+  // element keys are value keys; valid elements have an index < end.  Keys of missing
+  // elements are 0 and are excluded by index below.
+  uint32_t lmax = 0;
+  bool any = false;
+#pragma unroll
+  for (int j = 0; j < E; ++j) {
+    const bool ok = elem_index<DT, E>(aligned, start, tid, j) < end;
+    any |= ok;
+    lmax = (ok && key[j] >= lmax) ? key[j] : lmax;
+  }
+  // lanes without elements take no part in the threshold; valid keys shifted by one so
+  // that a NaN-only lane (key 0) still counts
+  const uint32_t lkey = any ? lmax : 0u;
+  const bool has = any;
+  // K-th largest lane maximum by bitwise descent (over value-key bits)
+  uint32_t T = 0;
+  const int nlanes = __popcll(__ballot(has));
+  if (nlanes >= K) {
+    constexpr int lowbit = DT == TAPS_BF16 ? 16 : 0;
+    for (int bit = 31; bit >= lowbit; --bit) {
+      const uint32_t c = T | (1u << bit);
+      if (__popcll(__ballot(has && lkey >= c)) >= K) T = c;
+    }
+  }
+  // compact all elements with key >= T (T = 0 keeps every valid element)
+  int cnt = 0;
+#pragma unroll
+  for (int j = 0; j < E; ++j)
+    cnt += (key[j] >= T && elem_index<DT, E>(aligned, start, tid, j) < end) ? 1 : 0;
+  int incl = cnt;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int o = __shfl_up(incl, off);
+    if (lane >= off) incl += o;
+  }
+  const int total = __shfl(incl, kWave - 1);
+  int pos = incl - cnt;
+  if (total <= kWaveCap) {
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+      const int e = elem_index<DT, E>(aligned, start, tid, j);
+      if (key[j] >= T && e < end) s_cand[wave][pos++] = cand_key(key[j], (uint32_t)e);
+    }
+  }
+  if (lane == 0) s_over[wave] = total > kWaveCap;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+
+  if (total <= kWaveCap) {
+    // exact rank of each compacted candidate within the wave
+    for (int c0 = 0; c0 < total; c0 += kWave) {
+      const int me = c0 + lane;
+      const uint64_t mine = me < total ? s_cand[wave][me] : 0ull;
+      int rank = 0;
+      for (int j = 0; j < total; ++j) rank += s_cand[wave][j] > mine ? 1 : 0;
+      if (me < total && rank < K) s_wave_top[wave][rank] = mine;
+    }
+    for (int r = total + lane; r < K; r += kWave) s_wave_top[wave][r] = 0ull;
+  } else {
+    // fallback: K rounds of exact argmax over the wave's elements
+    uint64_t prev = ~0ull;
+    for (int r = 0; r < K; ++r) {
+      uint64_t best = 0;
+#pragma unroll
+      for (int j = 0; j < E; ++j) {
+        const int e = elem_index<DT, E>(aligned, start, tid, j);
+        const uint64_t k = e < end ? cand_key(key[j], (uint32_t)e) : 0ull;
+        best = (k < prev && k > best) ? k : best;
+      }
+      best = wave_max_u64(best);
+      if (lane == 0) s_wave_top[wave][r] = best;
+      prev = best;
+    }
+  }
+  __syncthreads();
+
+  // merge the wave lists: rank each of the kWaves*K entries
+  if (wave == 0) {
+    const int tot = kWaves * K;
+    uint64_t* outp = cand + ((size_t)row * chunks + chunk) * K;
+    for (int c0 = 0; c0 < tot; c0 += kWave) {
+      const int me = c0 + lane;
+      const uint64_t mine = me < tot ? s_wave_top[me / K][me % K] : 0ull;
+      int rank = 0;
+      for (int j = 0; j < tot; ++j) rank += s_wave_top[j / K][j % K] > mine ? 1 : 0;
+      if (me < tot && mine != 0ull && rank < K) outp[rank] = mine;
+    }
+    // ranks held by empty entries: write 0 (a chunk with fewer than K elements)
+    int nonempty = 0;
+    for (int j = lane; j < tot; j += kWave) nonempty += s_wave_top[j / K][j % K] != 0ull;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) nonempty += __shfl_xor(nonempty, off);
+    for (int r = nonempty + lane; r < K; r += kWave) outp[r] = 0ull;
+  }
+}
+
+template <int DT>
+hipError_t launch_dt(const void* marg, int rows, int vocab, int K, const TopkPlan& p,
+                     uint64_t* cand, hipStream_t s) {
+  dim3 grid((unsigned)(rows * p.chunks)), block(kThreads);
+  switch (p.per_thread) {
+    case 8: topk_chunk_kernel<DT, 8><<<grid, block, 0, s>>>(marg, vocab, K, p.chunk_len, p.chunks, cand); break;
+    case 16: topk_chunk_kernel<DT, 16><<<grid, block, 0, s>>>(marg, vocab, K, p.chunk_len, p.chunks, cand); break;
+    case 32: topk_chunk_kernel<DT, 32><<<grid, block, 0, s>>>(marg, vocab, K, p.chunk_len, p.chunks, cand); break;
+    default: topk_chunk_kernel<DT, 64><<<grid, block, 0, s>>>(marg, vocab, K, p.chunk_len, p.chunks, cand); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+TopkPlan plan_topk(int vocab, int rows, int /*dtype*/) {
+  // aim for ~512 workgroups; chunks of 2048..16384 elements (8..64 per thread)
+  const int target_chunks = rows >= 512 ? 1 : (512 + rows - 1) / rows;
+  int len = 2048;
+  while (len < 16384 &&
+         ((int64_t)len * target_chunks < vocab || (vocab + len - 1) / len > 64))
+    len *= 2;
+  TopkPlan p;
+  p.chunk_len = len;
+  p.chunks = (vocab + len - 1) / len;
+  p.per_thread = len / kThreads;
+  return p;
+}
+
+hipError_t launch_topk_chunks(const void* marg, int dtype, int rows, int vocab, int K,
+                              const TopkPlan& plan, uint64_t* cand, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  return dtype == TAPS_BF16 ? launch_dt<TAPS_BF16>(marg, rows, vocab, K, plan, cand, s)
+                            : launch_dt<TAPS_FP32>(marg, rows, vocab, K, plan, cand, s);
+}
+
+}  // namespace taps

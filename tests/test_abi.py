@@ -1,0 +1,138 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol include/taps.h
+declares, validates arguments before touching the device, and its fp64
+exponential (the host instance of the device function) matches the oracle bit
+for bit.  No kernel is launched here."""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2606_00487_amd import _lib
+from oracle.specexp import spec_exp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "taps.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z_]+)\s*\(", src)) - {"defined"})
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert set(names) == set(_lib.EXPORTED), names
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def params(**kw):
+    base = dict(batch=2, block=16, vocab=151936, K=8, budget=64, dtype=_lib.TAPS_BF16,
+                kind=_lib.TAPS_LOGITS, lambda1=1.0, lambda2=0.125, tau=0.0, beta=1.0)
+    base.update(kw)
+    return _lib.SelectParams(**base)
+
+
+@pytest.mark.parametrize("kw,status", [
+    ({}, _lib.TAPS_OK),
+    ({"batch": 0}, _lib.TAPS_OK),
+    ({"batch": -1}, _lib.TAPS_ERR_INVALID_ARG),
+    ({"K": 17}, _lib.TAPS_ERR_UNSUPPORTED),
+    ({"K": 0}, _lib.TAPS_ERR_INVALID_ARG),
+    ({"budget": 257}, _lib.TAPS_ERR_UNSUPPORTED),
+    ({"budget": 0}, _lib.TAPS_ERR_INVALID_ARG),
+    ({"block": 33}, _lib.TAPS_ERR_UNSUPPORTED),
+    ({"block": 0}, _lib.TAPS_ERR_INVALID_ARG),
+    ({"vocab": 4, "K": 8}, _lib.TAPS_ERR_INVALID_ARG),
+    ({"vocab": 2_000_000}, _lib.TAPS_ERR_UNSUPPORTED),
+    ({"lambda1": 0.0}, _lib.TAPS_ERR_INVALID_ARG),
+    ({"lambda1": math.inf}, _lib.TAPS_ERR_INVALID_ARG),
+    ({"lambda2": -0.5}, _lib.TAPS_ERR_UNSUPPORTED),
+    ({"lambda2": math.nan}, _lib.TAPS_ERR_INVALID_ARG),
+    ({"tau": math.nan}, _lib.TAPS_ERR_INVALID_ARG),
+    ({"tau": math.inf}, _lib.TAPS_OK),
+    ({"beta": -1.0}, _lib.TAPS_ERR_INVALID_ARG),
+    ({"kind": _lib.TAPS_PROBS, "beta": 2.0}, _lib.TAPS_ERR_UNSUPPORTED),
+    ({"kind": _lib.TAPS_PROBS, "dtype": _lib.TAPS_FP32}, _lib.TAPS_OK),
+    ({"dtype": 7}, _lib.TAPS_ERR_INVALID_ARG),
+    ({"kind": 5}, _lib.TAPS_ERR_INVALID_ARG),
+])
+def test_select_validation(lib, kw, status):
+    p = params(**kw)
+    assert lib.taps_select_validate(ctypes.byref(p)) == status
+    if status != _lib.TAPS_OK:
+        # the entry point returns the same status without touching its (null) buffers
+        assert lib.taps_select(None, ctypes.byref(p), None, None, 0, None) == status
+
+
+def test_select_rejects_null_buffers_and_small_workspace(lib):
+    p = params()
+    assert lib.taps_select(None, ctypes.byref(p), None, None, 0, None) == _lib.TAPS_ERR_INVALID_ARG
+    fake = 1 << 20  # aligned, never dereferenced: validation stops before any launch
+    t = _lib.Tree(fake, fake, fake, fake, fake, fake, fake, fake)
+    need = lib.taps_select_workspace_bytes(ctypes.byref(p))
+    assert need == 2 * 16 * 10 * 8 * 8     # 32 rows x 10 chunks of 16384 x K keys of 8 bytes
+    assert lib.taps_select(fake, ctypes.byref(p), ctypes.byref(t), fake, need - 1, None) == \
+        _lib.TAPS_ERR_WORKSPACE
+    assert lib.taps_select(fake + 2, ctypes.byref(p), ctypes.byref(t), fake, need, None) == \
+        _lib.TAPS_ERR_INVALID_ARG            # marginals must be 16-byte aligned
+    assert lib.taps_select(None, ctypes.byref(params(batch=0)), None, None, 0, None) == _lib.TAPS_OK
+
+
+@pytest.mark.parametrize("args,status", [
+    ((1, 64, 32, 8, 128, 8192, 0, 0.088), _lib.TAPS_OK),
+    ((1, 64, 32, 7, 128, 8192, 0, 0.088), _lib.TAPS_ERR_INVALID_ARG),
+    ((1, 64, 32, 8, 96, 8192, 0, 0.088), _lib.TAPS_ERR_UNSUPPORTED),
+    ((1, 300, 32, 8, 128, 8192, 0, 0.088), _lib.TAPS_ERR_UNSUPPORTED),
+    ((1, 64, 32, 8, 128, -1, 0, 0.088), _lib.TAPS_ERR_INVALID_ARG),
+    ((1, 64, 32, 8, 128, 8192, 3, 0.088), _lib.TAPS_ERR_INVALID_ARG),
+    ((1, 64, 32, 8, 128, 8192, 0, math.inf), _lib.TAPS_ERR_INVALID_ARG),
+    ((0, 64, 32, 8, 128, 8192, 0, 0.088), _lib.TAPS_OK),
+    ((1, 16, 4, 2, 64, 256, 1, 0.125), _lib.TAPS_OK),
+])
+def test_attention_validation(lib, args, status):
+    assert lib.tree_verify_attn_validate(*args) == status
+    b, n, hq, hkv, hd, mc, dt, sc = args
+    if status != _lib.TAPS_OK:
+        assert lib.tree_verify_attn(None, None, None, None, None, None, None, b, n, hq, hkv, hd,
+                                    mc, dt, sc, None, None, 0, None) == status
+
+
+def test_attention_workspace_is_a_pure_function(lib):
+    a = lib.tree_verify_attn_workspace_bytes(1, 64, 32, 8, 128, 8192, 0)
+    assert a > 0 and a == lib.tree_verify_attn_workspace_bytes(1, 64, 32, 8, 128, 8192, 0)
+    assert lib.tree_verify_attn_workspace_bytes(1, 16, 4, 2, 64, 256, 1) == 0   # fp32: none
+    fake = 1 << 20
+    assert lib.tree_verify_attn(fake, fake, fake, fake, fake, fake, fake, 1, 64, 32, 8, 128, 8192,
+                                0, 0.088, fake, fake, a - 1, None) == _lib.TAPS_ERR_WORKSPACE
+
+
+def test_walk_validation(lib):
+    assert lib.accept_walk(None, 1, 64, 16, None, None, None, None, None) == _lib.TAPS_ERR_INVALID_ARG
+    assert lib.accept_walk(None, 1, 64, 33, None, None, None, None, None) == _lib.TAPS_ERR_UNSUPPORTED
+    assert lib.accept_walk(None, 0, 64, 16, None, None, None, None, None) == _lib.TAPS_OK
+
+
+def test_status_strings(lib):
+    assert lib.taps_status_string(0) == b"TAPS_OK"
+    assert lib.taps_status_string(-3) == b"TAPS_ERR_WORKSPACE"
+    assert lib.taps_status_string(42) == b"TAPS_UNKNOWN_STATUS"
+
+
+def test_library_exponential_matches_oracle_bitwise(lib):
+    rng = np.random.default_rng(11)
+    ts = np.concatenate([-rng.uniform(0, 1, 20000), -rng.uniform(0, 50, 20000),
+                         -rng.uniform(0, 708, 5000), [0.0, -0.0, -1e-300, -708.0, -708.5,
+                                                      -math.inf, math.nan, -0.5 * math.log(2)]])
+    # every bf16 gap a row of logits can produce near the top of a row
+    from workloads import bf16_bits_to_f32
+    v = bf16_bits_to_f32(np.arange(0x3F00, 0x4180, dtype=np.uint16)).astype(np.float64)
+    ts = np.concatenate([ts, (v[:, None] - v[None, :]).ravel()])
+    ts = ts[~(ts > 0)]
+    for t in ts:
+        a, b = lib.taps_spec_exp_host(float(t)), spec_exp(float(t))
+        assert a == b or (math.isnan(a) and math.isnan(b)), (t, a, b)
+        assert np.float64(a).view(np.int64) == np.float64(b).view(np.int64), t

@@ -1,0 +1,270 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Trees, top-K indices and accepted paths must match bit for bit; attention must
+be within 2e-2 max-abs (bf16 inputs, fp32 accumulation) or 1e-4 (fp32) of the
+fp64 oracle.  The configurations run in the launch configuration the bench
+times (the plan is a pure function of the sizes)."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests import _util as U
+from workloads import BF16, CONFIGS, FP32, LOGITS, PROBS, Config, gen_round, kv_offsets
+
+pytestmark = pytest.mark.gpu
+
+TOL = {BF16: 2e-2, FP32: 1e-4}
+
+
+@pytest.fixture(scope="module")
+def taps():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_00487_amd as taps
+    taps.load()
+    return taps
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def run_select(taps, inp, tree=None, **over):
+    c = inp.cfg
+    kw = dict(kind=c.kind, lambda1=c.lambda1, lambda2=c.lambda2, tau=c.tau, beta=c.beta)
+    kw.update(over)
+    sel = taps.Selector(c.batch, c.block, c.vocab, c.K, c.budget, dtype=c.dtype, **kw)
+    m = U.to_dev(inp.marginals, c.dtype == BF16)
+    out = sel(m)
+    torch.cuda.synchronize()
+    return out, sel, m
+
+
+# ------------------------------------------------------------------ selection
+@pytest.mark.parametrize("name", ["tiny", "qwen3_4b", "qwen3_8b", "serve16", "stress"])
+def test_select_matches_oracle(taps, name):
+    say(f"[select] {name}")
+    inp = gen_round(name, with_attention=False)
+    gpu, _, _ = run_select(taps, inp)
+    U.assert_tree_equal(gpu, U.oracle_trees(inp), inp.cfg)
+
+
+def _fuzz_cfg(rng, dtype, kind, V, D, K, N, B=2):
+    return Config("fuzz", 9, B, D, V, K, N, 4, 2, 64, 16, kind, dtype, 1.0, 0.0, 0.0, 0.7)
+
+
+def _fuzz_marginals(rng, cfg, mode):
+    B, D, V = cfg.batch, cfg.block, cfg.vocab
+    if mode == "ties":
+        x = rng.integers(-4, 4, size=(B, D, V)).astype(np.float32) * 0.5
+    elif mode == "deep":
+        x = rng.standard_normal((B, D, V)).astype(np.float32)
+        x[:, :, 3] += 30.0                        # rank 0 dominates: a deep chain
+    elif mode == "specials":
+        x = rng.standard_normal((B, D, V)).astype(np.float32)
+        x[:, 0, :] = -np.inf                      # a row with nothing finite
+        x[:, 1, :5] = np.nan
+        x[:, 1, 7] = np.inf if cfg.kind == PROBS else 5.0
+        x[:, 2, ::3] = -0.0
+        x[:, 2, 1::3] = 0.0
+        if D > 3:
+            x[:, 3, :] = np.nan                   # an all-NaN row
+    else:
+        x = rng.standard_normal((B, D, V)).astype(np.float32) * 2
+    if cfg.kind == PROBS:
+        x = np.where(np.isnan(x), x, np.abs(x)).astype(np.float32)
+    from workloads import f32_to_bf16_bits
+    return f32_to_bf16_bits(x) if cfg.dtype == BF16 else x
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_select_fuzz(taps, seed):
+    rng = np.random.default_rng(500 + seed)
+    dtype = [BF16, FP32][seed % 2]
+    kind = [LOGITS, LOGITS, PROBS][seed % 3]
+    V = int(rng.choice([17, 100, 1001, 4099, 70001]))
+    K = int(rng.integers(1, 17))
+    K = min(K, V)
+    D = int(rng.integers(1, 33))
+    N = int(rng.choice([1, 2, 16, 63, 64, 65, 128, 200, 256]))
+    mode = ["ties", "deep", "specials", "plain"][seed % 4]
+    tau = float(rng.choice([0.0, 0.0, 1e-3, 1e-2]))
+    lam2 = float(rng.choice([0.0, 0.125, 0.5]))
+    cfg = _fuzz_cfg(rng, dtype, kind, V, D, K, N)
+    say(f"[fuzz] seed={seed} dtype={dtype} kind={kind} V={V} K={K} D={D} N={N} mode={mode} "
+        f"tau={tau} lam2={lam2}")
+    m = _fuzz_marginals(rng, cfg, mode)
+
+    class Inp:
+        pass
+    inp = Inp()
+    inp.cfg, inp.marginals = cfg, m
+    from workloads import bf16_bits_to_f32
+    x = bf16_bits_to_f32(m).astype(np.float64) if dtype == BF16 else m.astype(np.float64)
+    trees = [oracle.select_request(x[b], K, N, kind=kind, lambda1=1.0, lambda2=lam2, tau=tau)
+             for b in range(cfg.batch)]
+    sel = taps.Selector(cfg.batch, D, V, K, N, dtype=dtype, kind=kind, lambda2=lam2, tau=tau)
+    gpu = sel(U.to_dev(m, dtype == BF16))
+    torch.cuda.synchronize()
+    U.assert_tree_equal(gpu, trees, cfg)
+
+
+def test_select_is_deterministic(taps):
+    inp = gen_round("qwen3_8b", with_attention=False)
+    a, sel, m = run_select(taps, inp)
+    first = [t.clone() for t in (a.parent, a.token, a.q_reach, a.topk_idx, a.n_nodes)]
+    b = sel(m)
+    torch.cuda.synchronize()
+    for x, y in zip(first, (b.parent, b.token, b.q_reach, b.topk_idx, b.n_nodes)):
+        assert torch.equal(x, y)
+
+
+# ------------------------------------------------------------------ attention
+def _attn(taps, inp, trees, max_ctx=None):
+    c = inp.cfg
+    Q, K, V, off, ctx = U.attention_inputs(inp)
+    parent, _, n = U.tree_device(trees)
+    att = taps.TreeAttention(c.batch, c.budget, c.Hq, c.Hkv, c.head_dim,
+                             int(max_ctx if max_ctx is not None else inp.ctx_len.max()),
+                             dtype=c.dtype, scale=c.scale)
+    O = att(Q, K, V, off, ctx, parent, n)
+    torch.cuda.synchronize()
+    return O, (att, Q, K, V, off, ctx, parent, n)
+
+
+@pytest.mark.parametrize("name,samples", [("tiny", None), ("qwen3_4b", None), ("qwen3_8b", None),
+                                          ("serve16", 384), ("stress", 192)])
+def test_attention_matches_oracle(taps, name, samples):
+    say(f"[attn] {name}")
+    inp = gen_round(name)
+    c = inp.cfg
+    trees = U.oracle_trees(inp)
+    O, _ = _attn(taps, inp, trees)
+    Qd, Kd, Vd = inp.qkv_f64()
+    pick = None
+    if samples is not None:
+        rng = np.random.default_rng(7)
+        pick = []
+        for _ in range(samples):
+            b = int(rng.integers(0, c.batch))
+            pick.append((b, int(rng.integers(0, trees[b].n)), int(rng.integers(0, c.Hq))))
+        # always include the root and the deepest node of every request
+        for b, t in enumerate(trees):
+            pick.append((b, 0, 0))
+            pick.append((b, int(np.argmax(t.depth[:t.n])), c.Hq - 1))
+    ref = oracle.tree_attention(Qd, Kd, Vd, inp.kv_offset, inp.ctx_len,
+                                [t.parent for t in trees], [t.n for t in trees], c.scale,
+                                samples=pick)
+    got = U.gpu_o_as_f64(O)
+    mask = ~np.isnan(ref)
+    err = np.abs(got[mask] - ref[mask])
+    say(f"[attn] {name}: compared {mask.sum()} values, max-abs {err.max():.3e}, "
+        f"max|ref| {np.abs(ref[mask]).max():.3e}")
+    assert err.max() <= TOL[c.dtype]
+    # rows of nodes beyond n are never written
+    for b, t in enumerate(trees):
+        assert t.n <= c.budget
+
+
+def test_attention_edge_cases(taps):
+    """ctx = 0, a single node, a chain deeper than 64, ragged contexts, >64-node masks."""
+    rng = np.random.default_rng(3)
+    B, N, Hq, Hkv, hd = 4, 130, 8, 2, 128
+    ctx = np.array([0, 1, 77, 300], dtype=np.int32)
+    off = kv_offsets(ctx, N)
+    rows = int(off[-1] + ctx[-1] + N)
+    from workloads import f32_to_bf16_bits, bf16_bits_to_f32
+    Qf = rng.standard_normal((B, N, Hq, hd)).astype(np.float32)
+    Kf = rng.standard_normal((rows, Hkv, hd)).astype(np.float32)
+    Vf = rng.standard_normal((rows, Hkv, hd)).astype(np.float32)
+    Q, K, V = (f32_to_bf16_bits(a) for a in (Qf, Kf, Vf))
+    parents = [np.array([-1] + list(range(N - 1)), dtype=np.int32),         # chain of 130
+               np.array([-1] + [0] * (N - 1), dtype=np.int32),              # star
+               np.array([-1] + [int(rng.integers(0, i)) for i in range(1, N)], dtype=np.int32),
+               np.array([-1] + [int(rng.integers(max(0, i - 3), i)) for i in range(1, N)],
+                        dtype=np.int32)]
+    n = [N, 1, 97, 65]
+    import paper_2606_00487_amd as taps_mod
+    att = taps_mod.TreeAttention(B, N, Hq, Hkv, hd, int(ctx.max()), dtype=BF16, scale=hd ** -0.5)
+    O = att(U.to_dev(Q, True), U.to_dev(K, True), U.to_dev(V, True), torch.from_numpy(off).cuda(),
+            torch.from_numpy(ctx).cuda(), torch.from_numpy(np.stack(parents)).cuda(),
+            torch.tensor(n, dtype=torch.int32).cuda())
+    torch.cuda.synchronize()
+    ref = oracle.tree_attention(bf16_bits_to_f32(Q).astype(np.float64),
+                                bf16_bits_to_f32(K).astype(np.float64),
+                                bf16_bits_to_f32(V).astype(np.float64), off, ctx, parents, n,
+                                hd ** -0.5)
+    got = U.gpu_o_as_f64(O)
+    for b in range(B):
+        err = np.abs(got[b, :n[b]] - ref[b, :n[b]]).max()
+        say(f"[attn-edge] b={b} ctx={ctx[b]} n={n[b]} max-abs {err:.3e}")
+        assert err <= 2e-2
+
+
+def test_attention_is_deterministic(taps):
+    inp = gen_round("qwen3_4b")
+    trees = U.oracle_trees(inp)
+    O1, (att, Q, K, V, off, ctx, parent, n) = _attn(taps, inp, trees)
+    O1 = O1.clone()
+    O2 = att(Q, K, V, off, ctx, parent, n)
+    torch.cuda.synchronize()
+    assert torch.equal(O1.view(torch.int16), O2.view(torch.int16))
+
+
+# ------------------------------------------------------------------ walk
+@pytest.mark.parametrize("name,branch", [("tiny", False), ("qwen3_8b", False), ("qwen3_8b", True),
+                                         ("serve16", False), ("serve16", True), ("stress", True)])
+def test_walk_matches_oracle(taps, name, branch):
+    say(f"[walk] {name} branch={branch}")
+    inp = gen_round(name, with_attention=False)
+    c = inp.cfg
+    trees = U.oracle_trees(inp)
+    tgt = U.targets_for(inp, trees, branch=branch)
+    parent, token, n = U.tree_device(trees)
+    tb = taps.TreeBuffers.empty(c.batch, c.block, c.K, c.budget)
+    tb.parent.copy_(parent)
+    tb.token.copy_(token)
+    tb.n_nodes.copy_(n)
+    walk = taps.AcceptWalk(c.batch, c.budget, c.block)
+    path, plen, bonus = walk(tb, torch.from_numpy(tgt).cuda())
+    torch.cuda.synchronize()
+    path, plen, bonus = path.cpu().numpy(), plen.cpu().numpy(), bonus.cpu().numpy()
+    for b, t in enumerate(trees):
+        p, bo = oracle.accept_walk(t.parent, t.token, t.n, tgt[b])
+        from oracle.walk import walk_arrays
+        arr, ln, bn = walk_arrays(p, bo, c.block)
+        assert plen[b] == ln and bonus[b] == bn
+        np.testing.assert_array_equal(path[b], arr)
+
+
+# ------------------------------------------------------------------ one whole round
+def test_full_round_tiny_and_8b(taps):
+    for name in ["tiny", "qwen3_8b"]:
+        say(f"[round] {name}")
+        inp = gen_round(name)
+        c = inp.cfg
+        trees = U.oracle_trees(inp)
+        gpu, _, _ = run_select(taps, inp)
+        U.assert_tree_equal(gpu, trees, c)
+        Q, K, V, off, ctx = U.attention_inputs(inp)
+        att = taps.TreeAttention(c.batch, c.budget, c.Hq, c.Hkv, c.head_dim, int(inp.ctx_len.max()),
+                                 dtype=c.dtype, scale=c.scale)
+        O = att(Q, K, V, off, ctx, gpu.parent, gpu.n_nodes)
+        tgt = torch.from_numpy(U.targets_for(inp, trees)).cuda()
+        walk = taps.AcceptWalk(c.batch, c.budget, c.block)
+        path, plen, bonus = walk(gpu, tgt)
+        torch.cuda.synchronize()
+        Qd, Kd, Vd = inp.qkv_f64()
+        ref = oracle.tree_attention(Qd, Kd, Vd, inp.kv_offset, inp.ctx_len,
+                                    [t.parent for t in trees], [t.n for t in trees], c.scale)
+        got = U.gpu_o_as_f64(O)
+        m = ~np.isnan(ref)
+        assert np.abs(got[m] - ref[m]).max() <= TOL[c.dtype]
+        p, bo = oracle.accept_walk(trees[0].parent, trees[0].token, trees[0].n,
+                                   tgt.cpu().numpy()[0])
+        assert int(plen[0]) == len(p) and int(bonus[0]) == bo
+        assert path.cpu().numpy()[0, :len(p)].tolist() == p
