@@ -137,7 +137,7 @@ taps_status tree_verify_attn_validate(int32_t batch, int32_t budget, int32_t Hq,
  *   head_dim     64 or 128; Hq a multiple of Hkv; query head h reads KV head h/(Hq/Hkv)
  *   max_ctx      [host] upper bound of ctx_len, sizes the grid
  *   dtype        TAPS_BF16 (fp32 accumulation, output rounded to nearest even) or TAPS_FP32
- *   scale        softmax scale, finite (usually 1/sqrt(head_dim))
+ *   scale        softmax scale, finite and > 0 (usually 1/sqrt(head_dim))
  *   O            [batch][budget][Hq][head_dim] same dtype as Q; rows i >= n are not written
  * O[b,i,h] = softmax_j(scale * Q[b,i,h] . K[j,g]) V[j,g] over the context rows and the
  * ancestor-or-self tree rows of node i, g = h / (Hq/Hkv). */

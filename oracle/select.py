@@ -36,7 +36,8 @@ PROBS = 1
 
 @dataclasses.dataclass
 class Tree:
-    """Selected subtree S of one request, in selection order (parent before child).
+    """Selected subtree S of one request, breadth first: nodes ordered by depth, then by
+    rank path (so every parent precedes its children).
 
     Slots n..budget-1 hold parent = token = depth = rank = -1 and q_reach = 0.
     """
@@ -115,7 +116,8 @@ def select_request(marg_rows: np.ndarray, K: int, budget: int, kind: int = LOGIT
     denominator make u(child) <= u(parent) in floating point, and the depth
     tie-break puts a parent first on equal u.  So every iteration adds exactly
     one node whose ancestors are already in S; this loop keeps all children of
-    selected nodes in a priority queue and pops the best one.
+    selected nodes in a priority queue and pops the best one.  Alg. 1 returns a
+    set; it is emitted breadth first (depth, then rank path).
     """
     D = marg_rows.shape[0]
     idx = np.zeros((D, K), dtype=np.int32)
@@ -164,16 +166,20 @@ def select_request(marg_rows: np.ndarray, K: int, budget: int, kind: int = LOGIT
         paths.append(p)
         push_children(len(parent) - 1)
 
+    # emit S breadth first: by depth, then by rank path (parents still precede children)
     n = len(parent)
+    order = sorted(range(n), key=lambda i: (depth[i], paths[i]))
+    new = {old: k for k, old in enumerate(order)}
     pad = budget - n
     return Tree(
-        parent=np.array(parent + [-1] * pad, dtype=np.int32),
-        token=np.array(token + [-1] * pad, dtype=np.int32),
-        depth=np.array(depth + [-1] * pad, dtype=np.int32),
-        rank=np.array(rank + [-1] * pad, dtype=np.int32),
-        q_reach=np.array(q + [0.0] * pad, dtype=np.float64),
+        parent=np.array([-1 if parent[i] < 0 else new[parent[i]] for i in order] + [-1] * pad,
+                        dtype=np.int32),
+        token=np.array([token[i] for i in order] + [-1] * pad, dtype=np.int32),
+        depth=np.array([depth[i] for i in order] + [-1] * pad, dtype=np.int32),
+        rank=np.array([rank[i] for i in order] + [-1] * pad, dtype=np.int32),
+        q_reach=np.array([q[i] for i in order] + [0.0] * pad, dtype=np.float64),
         n=n, topk_idx=idx, topk_val=val,
-        utility=np.array(util + [0.0] * pad, dtype=np.float64),
+        utility=np.array([util[i] for i in order] + [0.0] * pad, dtype=np.float64),
     )
 
 

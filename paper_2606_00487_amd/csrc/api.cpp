@@ -41,7 +41,7 @@ taps_status attn_check(int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv, i
   if (Hq % Hkv != 0) return TAPS_ERR_INVALID_ARG;
   if (dtype != TAPS_BF16 && dtype != TAPS_FP32) return TAPS_ERR_INVALID_ARG;
   if (hd != 64 && hd != 128) return TAPS_ERR_UNSUPPORTED;
-  if (!std::isfinite(scale)) return TAPS_ERR_INVALID_ARG;
+  if (!std::isfinite(scale) || !(scale > 0.f)) return TAPS_ERR_INVALID_ARG;
   if ((int64_t)max_ctx + budget > (int64_t)1 << 30) return TAPS_ERR_UNSUPPORTED;
   if ((int64_t)batch * Hkv > 65535 || (int64_t)budget * Hq / Hkv > (int64_t)1 << 20)
     return TAPS_ERR_UNSUPPORTED;

@@ -17,6 +17,9 @@
 //   * fp32 online softmax in base 2; each split writes unnormalised O, its running max
 //     and its sum; a second kernel combines the splits and rounds to bf16.
 // fp32 path: a plain VALU kernel, one workgroup per (request, node, query head).
+#include <cstdio>
+#include <cstdlib>
+
 #include "common.h"
 
 namespace taps {
@@ -31,7 +34,6 @@ constexpr int kWavesA = 4;
 constexpr int kKT = 64;  // keys per tile
 constexpr float kLog2e = 1.4426950408889634f;
 
-__device__ inline int swz_v(int d) { return (d ^ (d >> 3)) & 7; }
 
 // word w (0..3) of a 256-bit mask held in registers, without dynamic register indexing
 __device__ inline uint64_t mask_word(const uint64_t (&a)[4], int w) {
@@ -59,27 +61,84 @@ __device__ inline void ancestor_mask(int i, F par, uint64_t (&a)[4]) {
   }
 }
 
-template <int QB, int HD>
-__global__ __launch_bounds__(kThreads) void attn_bf16_kernel(
+// 64 keys of the 256-bit ancestor-or-self mask a[], starting at bit t0 (t0 may be negative:
+// bits below 0 read as 0)
+__device__ inline uint64_t mask_window(const uint64_t (&a)[4], int t0) {
+  if (t0 <= -64 || t0 >= 256) return 0ull;
+  if (t0 < 0) return a[0] << (-t0);
+  const int w = t0 >> 6, sh = t0 & 63;
+  const uint64_t lo = mask_word(a, w);
+  const uint64_t hi = w < 3 ? mask_word(a, w + 1) : 0ull;
+  return sh ? (lo >> sh) | (hi << (64 - sh)) : lo;
+}
+
+// bits j of a 64-bit window for j < 64 (0 for j <= 0, all ones for j >= 64)
+__device__ inline uint64_t low_bits(int j) {
+  return j <= 0 ? 0ull : (j >= 64 ? ~0ull : ((1ull << j) - 1ull));
+}
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// s_waitcnt that waits until at most `n` vector-memory operations are outstanding
+// (expcnt and lgkmcnt left at their maxima, i.e. not waited on)
+#define TAPS_WAIT_VMCNT(n) \
+  __builtin_amdgcn_s_waitcnt(((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (7 << 4) | (15 << 8))
+
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+// permutation of a key row's low three bits that XORs its 16-byte chunks: the 8 rows a
+// K read touches at once, and the 4 rows x 2 chunk pairs a transposing V read touches
+// at once, land on distinct LDS banks
+__device__ inline int kswz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+
+// QB: 32-row query blocks per wave; WK: key groups (each iteration stages WK tiles, wave
+// group kg = wave / 4 works on tile kg; the groups merge their results in LDS at the end).
+// K and V tiles go from global memory straight into LDS (16 bytes per lane), row-major
+// with the 16-byte chunks of key row r XOR-permuted by kswz(r); two stages alternate so
+// the next iteration's tiles load while the current ones are used.  V^T operands are
+// read with the transposing LDS read: in each 16-lane group, lane i gets element i % 4
+// of the 8 bytes read by lanes 4t + i/4 (t = 0..3), i.e. 4 consecutive keys at its d.
+// The grid is one-dimensional: the query-row tiles of one (request, KV head, split) get
+// block ids that differ by multiples of 8, so they run on the same XCD and share its L2.
+template <int QB, int WK, int HD>
+__global__ __launch_bounds__(256 * WK) void attn_bf16_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc,
     const uint16_t* __restrict__ Vc, const int64_t* __restrict__ offp,
     const int32_t* __restrict__ ctxp, const int32_t* __restrict__ parentp,
     const int32_t* __restrict__ nnp, int N, int Hq, int Hkv, int max_ctx, float scale_log2,
-    int split_len, int splits, int mrows_pad, float* __restrict__ wsO,
+    int split_len, int splits, int mtiles, int pairs, int mrows_pad, float* __restrict__ wsO,
     float2* __restrict__ wsML) {
-  constexpr int DC = HD / 8;          // 16-byte chunks per K/V row
-  constexpr int MT = kWavesA * 32 * QB;
+  constexpr int NT = 256 * WK;
+  constexpr int NW = 4 * WK;
+  constexpr int ROWB = HD * 2;        // bytes per K/V row
+  constexpr int MT = 4 * 32 * QB;     // query rows per workgroup
   constexpr int NDB = HD / 32;        // 32-row blocks of O^T
   constexpr int NKK = HD / 16;        // MFMA k-steps over head_dim
-  __shared__ __attribute__((aligned(16))) uint16_t s_k[kKT * HD];
-  __shared__ __attribute__((aligned(16))) uint16_t s_vt[HD * kKT];
+  constexpr int TILEB = kKT * ROWB;   // bytes of one staged K (or V) tile
+  constexpr int STAGEB = 2 * WK * TILEB;  // K and V tiles of the WK key groups
+  constexpr int BLK = kWave * 16;     // bytes one wave writes per direct load
+  constexpr int LPW = STAGEB / BLK / NW;  // direct loads per wave per stage
+  constexpr int XBYTES = 4 * QB * NDB * 16 * 64 * 4;  // key-group exchange of O
+  constexpr int SBYTES = (WK > 1 && XBYTES > 2 * STAGEB) ? XBYTES : 2 * STAGEB;
+  static_assert(STAGEB % (BLK * NW) == 0, "stage must split evenly over the waves");
+  static_assert(LPW <= 8, "direct loads per wave");
+  __shared__ __attribute__((aligned(16))) unsigned char s_raw[SBYTES];
   __shared__ uint64_t s_anc[TAPS_MAX_BUDGET][4];
   __shared__ int s_par[TAPS_MAX_BUDGET];
+  __shared__ float2 s_ml[WK > 1 ? 4 * QB * 64 : 1];
 
-  const int split = blockIdx.x, mt = blockIdx.y, bg = blockIdx.z;
+  // ---- which (request, KV head, split, row tile) this workgroup owns
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int mt = slot % mtiles, pair = (slot / mtiles) * 8 + xcd;
+  if (pair >= pairs) return;
+  const int split = pair % splits, bg = pair / splits;
   const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
   const int G = Hq / Hkv;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rg = wave & 3, kg = wave >> 2;
   const int l32 = lane & 31, hl = lane >> 5;
 
   const int ctx = min(max(ctxp[b], 0), max_ctx);
@@ -90,13 +149,45 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(
   const int row0 = mt * MT;
   if (k_begin >= k_end || row0 >= n * G) return;
   const int64_t kv0 = offp[b];
+  const size_t row_stride = (size_t)Hkv * HD;  // elements between consecutive cache rows
+  const uint16_t* kbase = Kc + (size_t)kv0 * row_stride + (size_t)g * HD;
+  const uint16_t* vbase = Vc + (size_t)kv0 * row_stride + (size_t)g * HD;
+
+  // ---- per-lane pieces of the direct loads: block j of this wave covers 4 key rows
+  int ld_row[LPW], ld_off[LPW];   // row within the stage's tile, element offset in the row
+#pragma unroll
+  for (int j = 0; j < LPW; ++j) {
+    const int byte = (wave * LPW + j) * BLK + lane * 16;
+    const int within = byte % (WK * TILEB);
+    const int t = within / TILEB;
+    const int rb = within - t * TILEB;
+    const int kr = rb / ROWB;
+    const int pc = (rb - kr * ROWB) / 16;
+    ld_row[j] = t * kKT + kr;
+    ld_off[j] = (pc ^ kswz(kr)) * 8;
+  }
+  auto issue_stage = [&](int stage, int base) {
+    unsigned char* sb = s_raw + stage * STAGEB;
+    const bool full = base + kKT * WK <= k_end;
+#pragma unroll
+    for (int j = 0; j < LPW; ++j) {
+      const int blk = wave * LPW + j;
+      const bool isv = blk * BLK >= WK * TILEB;   // uniform per wave and j
+      int key = base + ld_row[j];
+      if (!full) key = key < k_end ? key : k_begin;   // a real row; masked out later
+      const uint16_t* src = (isv ? vbase : kbase) + (size_t)key * row_stride + ld_off[j];
+      __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(sb + blk * BLK), 16, 0, 0);
+    }
+  };
+  constexpr int STEP = kKT * WK;
+  issue_stage(0, k_begin);   // the first tiles load while the queries and masks are set up
 
   // ---- queries of this lane (B operand of S^T = K Q^T)
   bf16x8 q[QB][NKK];
   int qnode[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    int qr = row0 + wave * 32 * QB + qb * 32 + l32;
+    int qr = row0 + rg * 32 * QB + qb * 32 + l32;
     qr = min(qr, N * G - 1);
     const int node = qr / G, hq = g * G + (qr - node * G);
     qnode[qb] = node;
@@ -106,12 +197,11 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(
   }
 
   // ---- ancestor masks, only when this split reaches the tree rows
-  const bool tree_part = k_end > ctx;
   uint64_t anc[QB][4];
-  if (tree_part) {
-    for (int i = tid; i < n; i += kThreads) s_par[i] = parentp[(size_t)b * N + i];
+  if (k_end > ctx) {
+    for (int i = tid; i < n; i += NT) s_par[i] = parentp[(size_t)b * N + i];
     __syncthreads();
-    for (int i = tid; i < n; i += kThreads) {
+    for (int i = tid; i < n; i += NT) {
       uint64_t a[4];
       ancestor_mask(i, [&](int j) { return s_par[j]; }, a);
 #pragma unroll
@@ -129,6 +219,21 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(
       for (int w = 0; w < 4; ++w) anc[qb][w] = 0ull;
   }
 
+  // ---- per-lane LDS read offsets (constant over iterations)
+  // K: key row l32 (+32 per key block), chunk (2kk + hl) ^ kswz(l32)
+  const int fk = kswz(l32);
+  int koff[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) koff[j] = l32 * ROWB + 32 * (j ^ (fk >> 1)) + 16 * (hl ^ (fk & 1));
+  // V^T: lanes 4t + q of each 16-lane group read row 4*hl + t, 8 bytes at d = 16*g16 + 4*q
+  const int g16 = (lane >> 4) & 1, tq = (lane & 15) >> 2, qq = lane & 3;
+  const int fv = kswz(4 * hl + tq);
+  int voff[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+    voff[j] = (4 * hl + tq) * ROWB + 8 * (qq & 1) + 16 * ((g16 * 2 + (qq >> 1)) ^ (fv & 3)) +
+              64 * (j ^ (fv >> 2));
+
   f32x16 o[NDB][QB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
@@ -136,142 +241,155 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(
     for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) o[db][qb][v] = 0.f;
-  float m_run[QB], l_run[QB];
+  float m_ref[QB], l_run[QB];
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) { m_run[qb] = -INFINITY; l_run[qb] = 0.f; }
+  for (int qb = 0; qb < QB; ++qb) { m_ref[qb] = -INFINITY; l_run[qb] = 0.f; }
 
-  const size_t row_stride = (size_t)Hkv * HD;  // elements between consecutive cache rows
-  const uint16_t* kbase = Kc + (size_t)kv0 * row_stride + (size_t)g * HD;
-  const uint16_t* vbase = Vc + (size_t)kv0 * row_stride + (size_t)g * HD;
-
-  for (int k0 = k_begin; k0 < k_end; k0 += kKT) {
-    // ---- stage K (row-major, chunk-swizzled) and V^T (transposed, permuted keys)
-#pragma unroll
-    for (int c = 0; c < kKT * DC / kThreads; ++c) {
-      const int id = tid + kThreads * c;
-      const int kr = id / DC, dc = id - (id / DC) * DC;
-      uint4 w = {0u, 0u, 0u, 0u};
-      if (k0 + kr < k_end) w = *(const uint4*)(kbase + (size_t)(k0 + kr) * row_stride + dc * 8);
-      *(uint4*)(s_k + kr * HD + ((dc ^ (kr & 7)) * 8)) = w;
+  int stage = 0;
+  for (int base = k_begin; base < k_end; base += STEP, stage ^= 1) {
+    const bool more = base + STEP < k_end;
+    if (more) {
+      issue_stage(stage ^ 1, base + STEP);
+      TAPS_WAIT_VMCNT(LPW);          // this stage's loads are done, the next may fly
+    } else {
+      TAPS_WAIT_VMCNT(0);
     }
-    if (tid < 16 * DC) {
-      const int a = tid / DC, dc = tid - (tid / DC) * DC;
-      uint4 w[4];
+    __builtin_amdgcn_s_barrier();
+    const int k0 = base + kg * kKT;
+    if (k0 < k_end) {
+      const unsigned char* tk = s_raw + stage * STAGEB + kg * TILEB;
+      const unsigned char* tv = s_raw + stage * STAGEB + WK * TILEB + kg * TILEB;
+      // ---- S^T = K Q^T for the two 32-key blocks
+      f32x16 s[2][QB];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int kr = 4 * a + j;
-        w[j] = make_uint4(0u, 0u, 0u, 0u);
-        if (k0 + kr < k_end) w[j] = *(const uint4*)(vbase + (size_t)(k0 + kr) * row_stride + dc * 8);
-      }
-      const int as = a & 7;
-      const int pos = 32 * (a >> 3) + ((as & 1) << 4) + ((as >> 1) << 2);
-      const int chunk = pos >> 3, half = (pos >> 2) & 1;
+      for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-      for (int dd = 0; dd < 8; ++dd) {
-        const int d = dc * 8 + dd;
-        const int sh = (dd & 1) * 16;
-        uint32_t e[4];
+        for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t ww = dd < 2 ? w[j].x : dd < 4 ? w[j].y : dd < 6 ? w[j].z : w[j].w;
-          e[j] = (ww >> sh) & 0xFFFFu;
+          for (int v = 0; v < 16; ++v) s[kb][qb][v] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < NKK; ++kk) {
+          const bf16x8 a = *(const bf16x8*)(tk + kb * 32 * ROWB + 32 * (kk & ~3) + koff[kk & 3]);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            s[kb][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, q[qb][kk], s[kb][qb], 0, 0, 0);
         }
-        uint2 pk;
-        pk.x = e[0] | (e[1] << 16);
-        pk.y = e[2] | (e[3] << 16);
-        *(uint2*)(s_vt + d * kKT + ((chunk ^ swz_v(d)) * 8) + half * 4) = pk;
+      }
+      // ---- mask (only tiles that reach the tree rows or the split end), online softmax
+      const bool need_mask = k0 + kKT > ctx || k0 + kKT > k_end;
+      bf16x8 p[2][QB][2];
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        if (need_mask) {
+          uint64_t A = (low_bits(ctx - k0) | mask_window(anc[qb], k0 - ctx)) & low_bits(k_end - k0);
+          A >>= 4 * hl;   // this lane's keys are kb*32 + 8*(v/4) + 4*hl + v%4
+          const uint32_t mlo = (uint32_t)A, mhi = (uint32_t)(A >> 32);
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+              const uint32_t word = kb ? mhi : mlo;
+              if (!((word >> (8 * (v >> 2) + (v & 3))) & 1u)) s[kb][qb][v] = -INFINITY;
+            }
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kb][qb][v]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;   // scale > 0
+        // move the reference max only when it is exceeded by more than 2^8
+        const bool upd = mx > m_ref[qb] + 8.f;
+        if (__ballot(upd)) {
+          const float nref = upd ? mx : m_ref[qb];
+          const float alpha = upd ? __builtin_amdgcn_exp2f(m_ref[qb] - nref) : 1.f;
+          l_run[qb] *= alpha;
+#pragma unroll
+          for (int db = 0; db < NDB; ++db)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) o[db][qb][v] *= alpha;
+          m_ref[qb] = nref;
+        }
+        const float nref = m_ref[qb] == -INFINITY ? 0.f : -m_ref[qb];
+        float sum = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int hf = 0; hf < 2; ++hf) {
+            bf16x8 pk8;
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+              const float e = __builtin_amdgcn_exp2f(fmaf(s[kb][qb][hf * 8 + t], scale_log2, nref));
+              sum += e;
+              pk8[t] = (__bf16)e;
+            }
+            p[kb][qb][hf] = pk8;
+          }
+        l_run[qb] += sum;
+      }
+      // ---- O^T += V^T P^T; V^T operands by transposing reads of the row-major V tile
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const int vo = voff[db & 1] + 64 * (db & ~1);
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int hf = 0; hf < 2; ++hf) {
+            const unsigned char* va = tv + (kb * 32 + 16 * hf) * ROWB + vo;
+            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)va);
+            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va + 8 * ROWB));
+            const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb)
+              o[db][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p[kb][qb][hf], o[db][qb], 0, 0, 0);
+          }
+      }
+    }
+    __builtin_amdgcn_s_barrier();    // the stage is free for the loads issued next iteration
+  }
+
+  float lsum[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) lsum[qb] = l_run[qb] + __shfl_xor(l_run[qb], 32);
+
+  // ---- merge the key groups through LDS (the stage buffers are free now)
+  if (WK > 1) {
+    float* xo = (float*)s_raw;
+    if (kg == 1) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            xo[(((rg * QB + qb) * NDB + db) * 16 + v) * 64 + lane] = o[db][qb][v];
+        s_ml[(rg * QB + qb) * 64 + lane] = make_float2(m_ref[qb], lsum[qb]);
       }
     }
     __syncthreads();
-
-    // ---- S^T = K Q^T for the two 32-key blocks
-    f32x16 s[2][QB];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) s[kb][qb][v] = 0.f;
-      const int kr = kb * 32 + l32;
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) {
-        const bf16x8 a = *(const bf16x8*)(s_k + kr * HD + (((2 * kk + hl) ^ (kr & 7)) * 8));
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-          s[kb][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, q[qb][kk], s[kb][qb], 0, 0, 0);
-      }
-    }
-
-    // ---- mask, online softmax (base 2), P^T in bf16
-    bf16x8 p[2][QB][2];
+    if (kg != 0) return;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = k0 + kb * 32 + 8 * (v >> 2) + 4 * hl + (v & 3);
-          bool ok = key < k_end;
-          if (key >= ctx) {
-            const int t = key - ctx;
-            ok = ok && ((mask_word(anc[qb], (t >> 6) & 3) >> (t & 63)) & 1ull);
-          }
-          const float x = ok ? s[kb][qb][v] * scale_log2 : -INFINITY;
-          s[kb][qb][v] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run[qb], mx);
-      const float ref = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = exp2f(m_run[qb] - ref);
-      float sum = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          bf16x8 pk;
-#pragma unroll
-          for (int t = 0; t < 8; ++t) {
-            const float e = exp2f(s[kb][qb][hf * 8 + t] - ref);
-            sum += e;
-            pk[t] = (__bf16)e;
-          }
-          p[kb][qb][hf] = pk;
-        }
-      l_run[qb] = l_run[qb] * alpha + sum;
-      m_run[qb] = m_new;
+      const float2 ml = s_ml[(rg * QB + qb) * 64 + lane];
+      const float M = fmaxf(m_ref[qb], ml.x);
+      const float a0 = m_ref[qb] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref[qb] - M);
+      const float a1 = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - M);
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) o[db][qb][v] *= alpha;
+        for (int v = 0; v < 16; ++v)
+          o[db][qb][v] = o[db][qb][v] * a0 + xo[(((rg * QB + qb) * NDB + db) * 16 + v) * 64 + lane] * a1;
+      lsum[qb] = lsum[qb] * a0 + ml.y * a1;
+      m_ref[qb] = M;
     }
-
-    // ---- O^T += V^T P^T
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      const int d = db * 32 + l32;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          const int chunk = 4 * kb + 2 * hl + hf;
-          const bf16x8 a = *(const bf16x8*)(s_vt + d * kKT + ((chunk ^ swz_v(d)) * 8));
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb)
-            o[db][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p[kb][qb][hf], o[db][qb], 0, 0, 0);
-        }
-    }
-    __syncthreads();
   }
 
-  // ---- write this split's unnormalised partial output, max and sum
-  const size_t base = ((size_t)bg * splits + split) * mrows_pad;
+  // ---- write this split's unnormalised partial output, reference max and sum
+  const size_t obase = ((size_t)bg * splits + split) * mrows_pad;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    const int qr = row0 + wave * 32 * QB + qb * 32 + l32;
-    const float lsum = l_run[qb] + __shfl_xor(l_run[qb], 32);
-    float* op = wsO + (base + qr) * HD;
+    const int qr = row0 + rg * 32 * QB + qb * 32 + l32;
+    float* op = wsO + (obase + qr) * HD;
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -280,7 +398,7 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(
         *(float4*)(op + d) = make_float4(o[db][qb][4 * r4], o[db][qb][4 * r4 + 1],
                                          o[db][qb][4 * r4 + 2], o[db][qb][4 * r4 + 3]);
       }
-    if (hl == 0) wsML[base + qr] = make_float2(m_run[qb], lsum);
+    if (hl == 0) wsML[obase + qr] = make_float2(m_ref[qb], lsum[qb]);
   }
 }
 
@@ -303,16 +421,34 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
   const int qr = i * G + (hq - g * G);
   const int nspl = (R + split_len - 1) / split_len;
   const size_t base = (size_t)(b * Hkv + g) * splits;
+  // loads are issued eight splits at a time so their latencies overlap
   float M = -INFINITY;
-  for (int s = 0; s < nspl; ++s) M = fmaxf(M, wsML[(base + s) * mrows_pad + qr].x);
+  for (int s0 = 0; s0 < nspl; s0 += 8) {
+    float mv[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      mv[t] = s0 + t < nspl ? wsML[(base + s0 + t) * mrows_pad + qr].x : -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) M = fmaxf(M, mv[t]);
+  }
   float L = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s = 0; s < nspl; ++s) {
-    const float2 ml = wsML[(base + s) * mrows_pad + qr];
-    const float w = exp2f(ml.x - M);
-    L += w * ml.y;
-    const float4 v = *(const float4*)(wsO + ((base + s) * mrows_pad + qr) * HD + d);
-    acc.x += w * v.x; acc.y += w * v.y; acc.z += w * v.z; acc.w += w * v.w;
+  for (int s0 = 0; s0 < nspl; s0 += 8) {
+    float2 ml[8];
+    float4 ov[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const bool ok = s0 + t < nspl;
+      ml[t] = ok ? wsML[(base + s0 + t) * mrows_pad + qr] : make_float2(-INFINITY, 0.f);
+      ov[t] = ok ? *(const float4*)(wsO + ((base + s0 + t) * mrows_pad + qr) * HD + d)
+                 : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const float w = ml[t].x == -INFINITY ? 0.f : exp2f(ml[t].x - M);
+      L += w * ml[t].y;
+      acc.x += w * ov[t].x; acc.y += w * ov[t].y; acc.z += w * ov[t].z; acc.w += w * ov[t].w;
+    }
   }
   const float inv = 1.f / L;
   __bf16 r0 = (__bf16)(acc.x * inv), r1 = (__bf16)(acc.y * inv), r2 = (__bf16)(acc.z * inv),
@@ -412,16 +548,28 @@ AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max
   AttnPlan p;
   const int G = Hq / Hkv;
   const int mrows = budget * G;
-  p.qb = mrows > 128 ? 2 : 1;
-  p.mtile = kWavesA * 32 * p.qb;
+  // two waves per SIMD (32 query rows each, two key groups) by default; TAPS_ATTN_PLAN=
+  // "qb,wk" selects another instantiation (qb in {1,2}, wk in {1,2}) for tuning
+  p.qb = 1;
+  p.wk = 2;
+  if (const char* e = getenv("TAPS_ATTN_PLAN")) {
+    int qb = 0, wk = 0;
+    if (sscanf(e, "%d,%d", &qb, &wk) == 2 && (qb == 1 || qb == 2) && (wk == 1 || wk == 2) &&
+        !(qb == 2 && wk == 2)) {
+      p.qb = qb;
+      p.wk = wk;
+    }
+  }
+  p.mtile = 4 * 32 * p.qb;
   p.mtiles = (mrows + p.mtile - 1) / p.mtile;
-  // split the keys so that roughly 256-512 workgroups run, with at least 4 tiles each
+  // split the keys so that about 256 workgroups run, each with >= 2 iterations
   const int keys = max_ctx + budget;
+  const int step = kKT * p.wk;
   const long long base = (long long)batch * Hkv * p.mtiles;
-  int splits = (int)((512 + base - 1) / base);
+  const int splits = (int)((256 + base - 1) / base);
   int len = (keys + splits - 1) / splits;
-  len = ((len + kKT - 1) / kKT) * kKT;
-  if (len < 4 * kKT) len = 4 * kKT;
+  len = ((len + step - 1) / step) * step;
+  if (len < 2 * step) len = 2 * step;
   p.split_len = len;
   p.splits = (keys + len - 1) / len;
   (void)head_dim;
@@ -444,18 +592,25 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
   const size_t rows = (size_t)batch * Hkv * pl.splits * mrows_pad;
   float* wsO = (float*)ws;
   float2* wsML = (float2*)((char*)ws + rows * head_dim * sizeof(float));
-  dim3 grid((unsigned)pl.splits, (unsigned)pl.mtiles, (unsigned)(batch * Hkv)), block(kThreads);
+  const int pairs = pl.splits * batch * Hkv;
+  dim3 grid((unsigned)(8 * pl.mtiles * ((pairs + 7) / 8)));
+  dim3 block((unsigned)(256 * pl.wk));
   const float sl2 = scale * kLog2e;
   const uint16_t *q = (const uint16_t*)Q, *k = (const uint16_t*)K, *v = (const uint16_t*)V;
   if (ev_begin && hipEventRecord(ev_begin, s) != hipSuccess) return hipErrorInvalidValue;
-#define TAPS_ATT(QB, HD)                                                                       \
-  attn_bf16_kernel<QB, HD><<<grid, block, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv, \
-                                                  max_ctx, sl2, pl.split_len, pl.splits,       \
-                                                  mrows_pad, wsO, wsML)
+#define TAPS_ATT(QB, WK, HD)                                                                  \
+  attn_bf16_kernel<QB, WK, HD><<<grid, block, 0, s>>>(q, k, v, off, ctx, parent, n, budget,   \
+                                                      Hq, Hkv, max_ctx, sl2, pl.split_len,    \
+                                                      pl.splits, pl.mtiles, pairs, mrows_pad, \
+                                                      wsO, wsML)
   if (head_dim == 128) {
-    if (pl.qb == 2) TAPS_ATT(2, 128); else TAPS_ATT(1, 128);
+    if (pl.qb == 2) TAPS_ATT(2, 1, 128);
+    else if (pl.wk == 2) TAPS_ATT(1, 2, 128);
+    else TAPS_ATT(1, 1, 128);
   } else {
-    if (pl.qb == 2) TAPS_ATT(2, 64); else TAPS_ATT(1, 64);
+    if (pl.qb == 2) TAPS_ATT(2, 1, 64);
+    else if (pl.wk == 2) TAPS_ATT(1, 2, 64);
+    else TAPS_ATT(1, 1, 64);
   }
 #undef TAPS_ATT
   hipError_t e = hipGetLastError();
@@ -464,12 +619,12 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
   const int rows_out = batch * budget * Hq;
   if (head_dim == 128) {
     const int rpb = kThreads / 32;
-    attn_combine_kernel<128><<<dim3((unsigned)((rows_out + rpb - 1) / rpb)), block, 0, s>>>(
+    attn_combine_kernel<128><<<dim3((unsigned)((rows_out + rpb - 1) / rpb)), dim3(kThreads), 0, s>>>(
         wsO, wsML, ctx, n, batch, budget, Hq, Hkv, max_ctx, pl.split_len, pl.splits, mrows_pad,
         (uint16_t*)O);
   } else {
     const int rpb = kThreads / 16;
-    attn_combine_kernel<64><<<dim3((unsigned)((rows_out + rpb - 1) / rpb)), block, 0, s>>>(
+    attn_combine_kernel<64><<<dim3((unsigned)((rows_out + rpb - 1) / rpb)), dim3(kThreads), 0, s>>>(
         wsO, wsML, ctx, n, batch, budget, Hq, Hkv, max_ctx, pl.split_len, pl.splits, mrows_pad,
         (uint16_t*)O);
   }

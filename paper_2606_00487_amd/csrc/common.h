@@ -42,6 +42,7 @@ hipError_t launch_select(const void* marg, const taps_select_params& p, const To
 
 struct AttnPlan {
   int qb;          // 32-row query blocks per wave (1 or 2)
+  int wk;          // key groups per workgroup (1 or 2): 256 * wk threads
   int mtile;       // query rows per workgroup (4 waves)
   int mtiles;      // workgroups along the budget*G query rows of one KV head
   int split_len;   // keys per split (multiple of 64)

@@ -5,14 +5,21 @@
 //          entries that can still be in the top-K; those are ranked exactly.
 // Phase B  sibling-softmax edge probabilities c[i][r] (Eq. 1) in IEEE fp64 and the
 //          utility denominators lambda1 + lambda2*d (Eq. 3).
-// Phase C  greedy selection (Alg. 1) by one wave.  Because q_cond <= 1 and the
-//          denominators do not decrease with depth, a child never beats its parent,
-//          so the argmax of Alg. 1 always lies among the not-yet-selected children of
-//          selected nodes.  Children of one node are offered in rank order (their
-//          utilities do not increase with rank), so the candidates form one sorted list
-//          per selected node; every pop takes the best list head.  Ties go to the
-//          shallower node, then to the lexicographically smaller rank path.
-// Phase D  write the tree.
+// Phase C  the selected set of Alg. 1.  Because q_cond <= 1 and the denominators do not
+//          decrease with depth, a child never beats its parent (ties go to the shallower
+//          node), so Alg. 1 adds exactly one node per iteration and its result is the
+//          first N-1 nodes of the trie in the order "utility descending, then depth
+//          ascending, then rank path ascending" among those with utility > tau.
+//          The trie is expanded one depth at a time, all candidates of a depth in
+//          parallel.  A histogram of utilities over fixed bins (exponent and 3 mantissa
+//          bits) gives a bin b* such that at least N-1 expanded nodes lie in bins >= b*;
+//          any node below b* is beaten by N-1 others and so are its descendants, so it is
+//          pruned.  At the end only the members of bin b* need an exact ranking.
+//          Nodes are stored depth by depth, each depth in rank-path order, so the stored
+//          index breaks ties between equal utilities exactly like the rank path does.
+//          If the expansion outgrows its LDS capacity, a sequential best-first loop
+//          computes the same set.
+// Phase D  write the tree breadth first (depth, then rank path).
 //
 // This file is compiled with -ffp-contract=off: every product and sum is rounded on
 // its own, as in the definition both sides of the parity test implement.
@@ -25,6 +32,9 @@ namespace {
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kRowCap = TAPS_MAX_K * TAPS_MAX_K;  // entries >= the threshold, at most K*K
+constexpr int kCap = 3072;                        // expanded nodes held in LDS
+constexpr int kBins = 1024;
+constexpr int kBinBase = (1023 - 110) * 8;        // bin 0 holds u < 2^-110
 
 // ------------------------------------------------------------------ shared exponential
 // Cody & Waite (1980) reduction t = k ln2 + r with ln2 = LN2_HI + LN2_LO (LN2_HI has 32
@@ -49,10 +59,64 @@ __host__ __device__ inline double spec_exp(double t) {
   return ldexp(p, (int)kf);
 }
 
-__device__ inline uint64_t shfl_u64(uint64_t v, int src) {
-  uint32_t lo = __shfl((uint32_t)v, src), hi = __shfl((uint32_t)(v >> 32), src);
-  return ((uint64_t)hi << 32) | lo;
+// ------------------------------------------------------------------ wave helpers
+__device__ inline int lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
+
+__device__ inline void wave_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// exclusive prefix of a small non-negative count (< 2^bits) over the lanes of a wave
+template <int BITS>
+__device__ inline int wave_prefix_small(int v, int& total) {
+  int pre = 0, tot = 0;
+#pragma unroll
+  for (int b = 0; b < BITS; ++b) {
+    const uint64_t m = __ballot((v >> b) & 1);
+    pre += lanes_below(m) << b;
+    tot += __popcll(m) << b;
+  }
+  total = tot;
+  return pre;
+}
+
+// exclusive prefix over the whole workgroup (values < 2^BITS); s_w holds kWaves ints
+template <int BITS>
+__device__ inline int block_prefix(int v, int* s_w, int& total) {
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  int wt;
+  const int pre = wave_prefix_small<BITS>(v, wt);
+  if (lane == 0) s_w[wave] = wt;
+  __syncthreads();
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const int x = s_w[w];
+    base += w < wave ? x : 0;
+    tot += x;
+  }
+  __syncthreads();
+  total = tot;
+  return base + pre;
+}
+
+// utility key: order-preserving bits of a non-negative double
+__device__ inline uint64_t ubits(double u) { return (uint64_t)__double_as_longlong(u); }
+__device__ inline int ubin(double u) {
+  const int b = (int)(ubits(u) >> 49) - kBinBase;
+  return b < 0 ? 0 : (b >= kBins ? kBins - 1 : b);
+}
+
+__device__ inline float value_from_key(uint32_t vk) {
+  if (vk == 0u) return __uint_as_float(0x7FC00000u);
+  return __uint_as_float((vk & 0x80000000u) ? (vk & 0x7FFFFFFFu) : ~vk);
+}
+
 __device__ inline uint64_t wave_max_u64(uint64_t v) {
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) {
@@ -71,140 +135,69 @@ __device__ inline uint32_t wave_min_u32(uint32_t v) {
   return v;
 }
 
-// utility key: order-preserving bits of a non-negative double, shifted so 0 means "none"
-__device__ inline uint64_t ukey(double u) { return (uint64_t)__double_as_longlong(u) + 1ull; }
+// ------------------------------------------------------------------ shared memory layout
+struct PhaseA {
+  uint64_t heads[kWaves][64];
+  uint64_t rowc[kWaves][kRowCap];
+};
+struct Level {                 // expanded trie nodes, stored depth by depth
+  double q[kCap];
+  uint64_t u[kCap];            // utility bits
+  int meta[kCap];              // parent index << 16 | depth << 8 | rank
+  int newidx[kCap];
+  int mlist[kCap];             // members of the boundary bin, in stored order
+  alignas(16) int hist[kBins];
+  int lvl_start[TAPS_MAX_BLOCK + 2];
+  int bsum[64];
+};
+struct Seq {                   // sequential fallback: candidate children per selected node
+  uint64_t U[TAPS_MAX_BUDGET][TAPS_MAX_K];
+  double Q[TAPS_MAX_BUDGET][TAPS_MAX_K];
+  uint32_t path[TAPS_MAX_BUDGET][4];
+  int depth[TAPS_MAX_BUDGET], par[TAPS_MAX_BUDGET], rank[TAPS_MAX_BUDGET];
+  int order[TAPS_MAX_BUDGET];
+};
+union Scratch {
+  PhaseA a;
+  Level l;
+  Seq s;
+};
 
-__device__ inline float value_from_key(uint32_t vk) {
-  if (vk == 0u) return __uint_as_float(0x7FC00000u);
-  return __uint_as_float((vk & 0x80000000u) ? (vk & 0x7FFFFFFFu) : ~vk);
-}
+struct Shared {
+  uint64_t top[TAPS_MAX_BLOCK][TAPS_MAX_K];
+  double e[TAPS_MAX_BLOCK][TAPS_MAX_K];
+  double c[TAPS_MAX_BLOCK][TAPS_MAX_K];
+  double den[TAPS_MAX_BLOCK + 1];
+  int wsum[kWaves];
+  int flag, bstar, n, total;
+  Scratch x;
+};
 
+// ------------------------------------------------------------------ Phase C fallback
+// Sequential best-first selection (one wave) for expansions larger than kCap; emits
+// S through sh.x.s in breadth-first order and returns n.
 template <int SLOTS>
-__global__ __launch_bounds__(kThreads) void select_kernel(
-    int D, int K, int N, int kind, double lambda1, double lambda2, double tau, double beta,
-    int chunks, const uint64_t* __restrict__ cand, int32_t* __restrict__ o_parent,
-    int32_t* __restrict__ o_token, int32_t* __restrict__ o_depth, int32_t* __restrict__ o_rank,
-    double* __restrict__ o_q, int32_t* __restrict__ o_n, int32_t* __restrict__ o_tidx,
-    float* __restrict__ o_tval) {
-  __shared__ uint64_t s_row[kWaves][kRowCap];
-  __shared__ uint64_t s_top[TAPS_MAX_BLOCK][TAPS_MAX_K];
-  __shared__ double s_e[TAPS_MAX_BLOCK][TAPS_MAX_K];
-  __shared__ double s_c[TAPS_MAX_BLOCK][TAPS_MAX_K];
-  __shared__ double s_den[TAPS_MAX_BLOCK + 1];
-  // per selected node: candidate children keys and q, path digits, depth
-  __shared__ uint64_t s_U[TAPS_MAX_BUDGET][TAPS_MAX_K];
-  __shared__ double s_Q[TAPS_MAX_BUDGET][TAPS_MAX_K];
-  __shared__ uint32_t s_path[TAPS_MAX_BUDGET][4];
-  __shared__ int s_depth[TAPS_MAX_BUDGET], s_par[TAPS_MAX_BUDGET], s_rank[TAPS_MAX_BUDGET];
-  __shared__ int s_n;
-
-  const int b = blockIdx.x;
+__device__ int select_sequential(Shared& sh, int D, int K, int N, double tau) {
+  Seq& S = sh.x.s;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-
-  // ---------------- Phase A: row merge
-  for (int i = wave; i < D; i += kWaves) {
-    const uint64_t* rc = cand + ((size_t)b * D + i) * chunks * K;
-    // K-th largest chunk head (chunks <= 64, one per lane)
-    const uint64_t head = lane < chunks ? rc[(size_t)lane * K] : 0ull;
-    int beat = 0;
-    for (int j = 0; j < chunks; ++j) beat += shfl_u64(head, j) > head ? 1 : 0;
-    const int nheads = __popcll(__ballot(head != 0ull));
-    uint64_t T;
-    if (nheads >= K) {
-      const uint64_t sel = __ballot(head != 0ull && beat == K - 1);
-      T = shfl_u64(head, __ffsll((long long)sel) - 1);
-    } else {
-      T = 1ull;  // fewer non-empty chunks than K: every entry is a candidate
-    }
-    // gather entries >= T (each chunk list is sorted, at most K*K survive)
-    int cnt = 0;
-    for (int e = lane; e < chunks * K; e += kWave) cnt += rc[e] >= T ? 1 : 0;
-    int incl = cnt;
-    for (int off = 1; off < kWave; off <<= 1) {
-      const int o = __shfl_up(incl, off);
-      if (lane >= off) incl += o;
-    }
-    const int total = min(__shfl(incl, kWave - 1), kRowCap);
-    int pos = incl - cnt;
-    for (int e = lane; e < chunks * K; e += kWave) {
-      const uint64_t v = rc[e];
-      if (v >= T) {
-        if (pos < kRowCap) s_row[wave][pos] = v;
-        ++pos;
-      }
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-    for (int c0 = 0; c0 < total; c0 += kWave) {
-      const int me = c0 + lane;
-      const uint64_t mine = me < total ? s_row[wave][me] : 0ull;
-      int rank = 0;
-      for (int j = 0; j < total; ++j) rank += s_row[wave][j] > mine ? 1 : 0;
-      if (me < total && rank < K) s_top[i][rank] = mine;
-    }
-    for (int r = total + lane; r < K; r += kWave) s_top[i][r] = 0ull;
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-    if (lane < K) {
-      const uint64_t k = s_top[i][lane];
-      const size_t o = ((size_t)b * D + i) * K + lane;
-      o_tidx[o] = k ? (int32_t)cand_index(k) : -1;
-      if (o_tval) o_tval[o] = value_from_key((uint32_t)(k >> 32));
-    }
-  }
-  __syncthreads();
-
-  // ---------------- Phase B: Eq. 1 edge probabilities, Eq. 3 denominators
-  if (tid < D * K) {
-    const int i = tid / K, r = tid - (tid / K) * K;
-    const uint64_t k = s_top[i][r];
-    const double x = k ? (double)value_from_key((uint32_t)(k >> 32)) : (double)__uint_as_float(0x7FC00000u);
-    double e;
-    if (kind == TAPS_LOGITS) {
-      const uint64_t k0 = s_top[i][0];
-      const double x0 = k0 ? (double)value_from_key((uint32_t)(k0 >> 32)) : x;
-      e = spec_exp(beta * (x - x0));
-    } else {
-      e = x > 0.0 ? x : 0.0;
-    }
-    s_e[i][r] = e;
-  }
-  if (tid <= D) s_den[tid] = lambda1 + lambda2 * (double)tid;
-  __syncthreads();
-  if (tid < D * K) {
-    const int i = tid / K, r = tid - (tid / K) * K;
-    double Z = 0.0;
-    for (int j = 0; j < K; ++j) Z = Z + s_e[i][j];
-    const bool ok = Z > 0.0 && Z <= 1.7976931348623157e308;
-    s_c[i][r] = ok ? s_e[i][r] / Z : 0.0;
-  }
-  __syncthreads();
-
-  // ---------------- Phase C: greedy selection (wave 0)
   if (wave == 0) {
-    // root (node 0): its K children form list 0
     if (lane < K) {
-      const double q = 1.0 * s_c[0][lane];
-      s_Q[0][lane] = q;
-      s_U[0][lane] = ukey(q / s_den[1]);
+      const double q = 1.0 * sh.c[0][lane];
+      S.Q[0][lane] = q;
+      S.U[0][lane] = ubits(q / sh.den[1]) + 1ull;
     }
     if (lane == 0) {
-      s_depth[0] = 0; s_par[0] = -1; s_rank[0] = -1;
-      s_path[0][0] = s_path[0][1] = s_path[0][2] = s_path[0][3] = 0u;
+      S.depth[0] = 0; S.par[0] = -1; S.rank[0] = -1;
+      S.path[0][0] = S.path[0][1] = S.path[0][2] = S.path[0][3] = 0u;
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    wave_fence();
     uint64_t head[SLOTS];
     int nxt[SLOTS];
 #pragma unroll
     for (int s = 0; s < SLOTS; ++s) { head[s] = 0ull; nxt[s] = 0; }
-    if (lane == 0) head[0] = s_U[0][0];
+    if (lane == 0) head[0] = S.U[0][0];
     int m = 1;
     while (m < N) {
-      // lane-local best list head
       uint64_t best = 0ull;
 #pragma unroll
       for (int s = 0; s < SLOTS; ++s) best = head[s] > best ? head[s] : best;
@@ -212,7 +205,6 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
       if (mx == 0ull) break;
       const double umax = __longlong_as_double((long long)(mx - 1ull));
       if (!(umax > tau)) break;
-      // entries holding the maximum; pick by (depth asc, rank path asc) on ties
       int ntie = 0, myslot = -1;
 #pragma unroll
       for (int s = 0; s < SLOTS; ++s) {
@@ -224,29 +216,26 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
       if (ntie == 1) {
         const uint64_t bal = __ballot(myslot >= 0);
         const int wl = __ffsll((long long)bal) - 1;
-        const int ws = __shfl(myslot, wl);
-        win = ws * kWave + wl;
+        win = __shfl(myslot, wl) * kWave + wl;
       } else {
-        // candidate child of entry j = node j's next rank: compare depth, then path words
         uint32_t key[SLOTS][5];
+        bool alive[SLOTS];
 #pragma unroll
         for (int s = 0; s < SLOTS; ++s) {
           const int j = s * kWave + lane;
-          if (head[s] == mx) {
-            const int d = s_depth[j] + 1;
+          alive[s] = head[s] == mx;
+          if (alive[s]) {
+            const int d = S.depth[j] + 1;
             key[s][0] = (uint32_t)d;
 #pragma unroll
-            for (int w = 0; w < 4; ++w) key[s][w + 1] = s_path[j][w];
-            const int lvl = d - 1;  // digit position (0-based level)
+            for (int w = 0; w < 4; ++w) key[s][w + 1] = S.path[j][w];
+            const int lvl = d - 1;
             key[s][1 + lvl / 8] |= (uint32_t)nxt[s] << (28 - 4 * (lvl % 8));
           } else {
 #pragma unroll
             for (int w = 0; w < 5; ++w) key[s][w] = 0xFFFFFFFFu;
           }
         }
-        bool alive[SLOTS];
-#pragma unroll
-        for (int s = 0; s < SLOTS; ++s) alive[s] = head[s] == mx;
 #pragma unroll
         for (int w = 0; w < 5; ++w) {
           uint32_t mn = 0xFFFFFFFFu;
@@ -263,67 +252,394 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
         const int wl = __ffsll((long long)bal) - 1;
         win = __shfl(ws, wl) * kWave + wl;
       }
-      // emit node m = child (win, nxt[win]) and build its children list
       const int wlane = win % kWave, wslot = win / kWave;
       int r_w = 0;
 #pragma unroll
       for (int s = 0; s < SLOTS; ++s) if (s == wslot) r_w = nxt[s];
       r_w = __shfl(r_w, wlane);
-      const double qm = s_Q[win][r_w];
-      const int dm = s_depth[win] + 1;
+      const double qm = S.Q[win][r_w];
+      const int dm = S.depth[win] + 1;
       if (lane == 0) {
-        s_depth[m] = dm; s_par[m] = win; s_rank[m] = r_w;
+        S.depth[m] = dm; S.par[m] = win; S.rank[m] = r_w;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) s_path[m][w] = s_path[win][w];
+        for (int w = 0; w < 4; ++w) S.path[m][w] = S.path[win][w];
         const int lvl = dm - 1;
-        s_path[m][lvl / 8] |= (uint32_t)r_w << (28 - 4 * (lvl % 8));
+        S.path[m][lvl / 8] |= (uint32_t)r_w << (28 - 4 * (lvl % 8));
       }
       if (lane < K) {
         if (dm < D) {
-          const double q = qm * s_c[dm][lane];
-          s_Q[m][lane] = q;
-          s_U[m][lane] = ukey(q / s_den[dm + 1]);
+          const double q = qm * sh.c[dm][lane];
+          S.Q[m][lane] = q;
+          S.U[m][lane] = ubits(q / sh.den[dm + 1]) + 1ull;
         } else {
-          s_Q[m][lane] = 0.0;
-          s_U[m][lane] = 0ull;
+          S.Q[m][lane] = 0.0;
+          S.U[m][lane] = 0ull;
         }
       }
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-      // advance the winner's list, open the new node's list
+      wave_fence();
       const int mlane = m % kWave, mslot = m / kWave;
 #pragma unroll
       for (int s = 0; s < SLOTS; ++s) {
         if (lane == wlane && s == wslot) {
           nxt[s] = r_w + 1;
-          head[s] = nxt[s] < K ? s_U[win][nxt[s]] : 0ull;
+          head[s] = nxt[s] < K ? S.U[win][nxt[s]] : 0ull;
         }
         if (lane == mlane && s == mslot) {
           nxt[s] = 0;
-          head[s] = s_U[m][0];
+          head[s] = S.U[m][0];
         }
       }
       ++m;
     }
-    if (lane == 0) s_n = m;
+    if (lane == 0) sh.n = m;
+  }
+  __syncthreads();
+  const int n = sh.n;
+  // breadth-first position of every selected node: (depth, path) ascending
+  for (int i = tid; i < n; i += kThreads) {
+    int pos = 0;
+    for (int j = 0; j < n; ++j) {
+      bool less = S.depth[j] < S.depth[i];
+      if (S.depth[j] == S.depth[i]) {
+        int w = 0;
+        while (w < 3 && S.path[j][w] == S.path[i][w]) ++w;
+        less = S.path[j][w] < S.path[i][w];
+      }
+      pos += less ? 1 : 0;
+    }
+    S.order[i] = pos;
+  }
+  __syncthreads();
+  return n;
+}
+
+template <int SLOTS>
+__global__ __launch_bounds__(kThreads) void select_kernel(
+    int D, int K, int N, int kind, double lambda1, double lambda2, double tau, double beta,
+    int chunks, const uint64_t* __restrict__ cand, int32_t* __restrict__ o_parent,
+    int32_t* __restrict__ o_token, int32_t* __restrict__ o_depth, int32_t* __restrict__ o_rank,
+    double* __restrict__ o_q, int32_t* __restrict__ o_n, int32_t* __restrict__ o_tidx,
+    float* __restrict__ o_tval) {
+  __shared__ Shared sh;
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+
+  // ---------------- Phase A: row merge (one wave per row)
+  {
+    PhaseA& A = sh.x.a;
+    const int CK = chunks * K;
+    for (int i = wave; i < D; i += kWaves) {
+      const uint64_t* rc = cand + ((size_t)b * D + i) * CK;
+      uint64_t v[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int e = j * kWave + lane;
+        v[j] = e < CK ? rc[e] : 0ull;
+      }
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int e = j * kWave + lane;
+        if (e < CK && e % K == 0) A.heads[wave][e / K] = v[j];
+      }
+      wave_fence();
+      uint64_t head = lane < chunks ? A.heads[wave][lane] : 0ull;
+      int beat = 0;
+      for (int j0 = 0; j0 < chunks; j0 += 8) {
+        uint64_t hv[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) hv[t] = j0 + t < chunks ? A.heads[wave][j0 + t] : 0ull;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) beat += hv[t] > head ? 1 : 0;
+      }
+      const int nheads = __popcll(__ballot(head != 0ull));
+      uint64_t T = 1ull;  // fewer non-empty chunks than K: every entry is a candidate
+      if (nheads >= K) {
+        const uint64_t sel = __ballot(head != 0ull && beat == K - 1);
+        T = A.heads[wave][__ffsll((long long)sel) - 1];
+      }
+      // compact the entries >= T (at most K*K of them) in order
+      int total = 0;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const uint64_t m = __ballot(v[j] >= T);
+        const int pos = total + lanes_below(m);
+        if (v[j] >= T && pos < kRowCap) A.rowc[wave][pos] = v[j];
+        total += __popcll(m);
+      }
+      total = total < kRowCap ? total : kRowCap;
+      wave_fence();
+      for (int c0 = 0; c0 < total; c0 += kWave) {
+        const int me = c0 + lane;
+        const uint64_t mine = me < total ? A.rowc[wave][me] : 0ull;
+        int rank = 0;
+        for (int j0 = 0; j0 < total; j0 += 8) {
+          uint64_t rv[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) rv[t] = j0 + t < total ? A.rowc[wave][j0 + t] : 0ull;
+#pragma unroll
+          for (int t = 0; t < 8; ++t) rank += rv[t] > mine ? 1 : 0;
+        }
+        if (me < total && rank < K) sh.top[i][rank] = mine;
+      }
+      for (int r = total + lane; r < K; r += kWave) sh.top[i][r] = 0ull;
+      wave_fence();
+      if (lane < K) {
+        const uint64_t k = sh.top[i][lane];
+        const size_t o = ((size_t)b * D + i) * K + lane;
+        o_tidx[o] = k ? (int32_t)cand_index(k) : -1;
+        if (o_tval) o_tval[o] = value_from_key((uint32_t)(k >> 32));
+      }
+      wave_fence();
+    }
   }
   __syncthreads();
 
-  // ---------------- Phase D: write the tree
-  const int n = s_n;
-  for (int j = tid; j < N; j += kThreads) {
-    const size_t o = (size_t)b * N + j;
-    if (j < n) {
-      const int d = s_depth[j];
-      o_parent[o] = s_par[j];
-      o_depth[o] = d;
-      o_rank[o] = s_rank[j];
-      o_token[o] = j == 0 ? -1 : (int32_t)cand_index(s_top[d - 1][s_rank[j]]);
-      o_q[o] = j == 0 ? 1.0 : s_Q[s_par[j]][s_rank[j]];
+  // ---------------- Phase B: Eq. 1 edge probabilities, Eq. 3 denominators
+  if (tid < D * K) {
+    const int i = tid / K, r = tid - (tid / K) * K;
+    const uint64_t k = sh.top[i][r];
+    const double x = k ? (double)value_from_key((uint32_t)(k >> 32)) : (double)__uint_as_float(0x7FC00000u);
+    double e;
+    if (kind == TAPS_LOGITS) {
+      const uint64_t k0 = sh.top[i][0];
+      const double x0 = k0 ? (double)value_from_key((uint32_t)(k0 >> 32)) : x;
+      e = spec_exp(beta * (x - x0));
     } else {
-      o_parent[o] = -1; o_depth[o] = -1; o_rank[o] = -1; o_token[o] = -1; o_q[o] = 0.0;
+      e = x > 0.0 ? x : 0.0;
     }
+    sh.e[i][r] = e;
+  }
+  if (tid <= D) sh.den[tid] = lambda1 + lambda2 * (double)tid;
+  if (tid < kWaves) sh.wsum[tid] = 0;
+  __syncthreads();
+  if (tid < D * K) {
+    const int i = tid / K, r = tid - (tid / K) * K;
+    double Z = 0.0;
+    for (int j = 0; j < K; ++j) Z = Z + sh.e[i][j];
+    const bool ok = Z > 0.0 && Z <= 1.7976931348623157e308;
+    sh.c[i][r] = ok ? sh.e[i][r] / Z : 0.0;
+  }
+  __syncthreads();
+
+  // ---------------- Phase C: depth-by-depth expansion with a safe pruning bin
+  Level& L = sh.x.l;
+  for (int j = tid; j < kBins; j += kThreads) L.hist[j] = 0;
+  if (tid == 0) {
+    L.q[0] = 1.0;
+    L.u[0] = ubits(1.0 / sh.den[0]);
+    L.meta[0] = (0xFFFF << 16) | 0;
+    L.lvl_start[0] = 0;
+    L.lvl_start[1] = 1;
+    sh.total = 1;
+    sh.bstar = 0;
+    sh.flag = 0;
+  }
+  __syncthreads();
+  int d = 0;
+  for (; d < D && N > 1; ++d) {
+    const int p0 = L.lvl_start[d], p1 = L.lvl_start[d + 1];
+    const int items = (p1 - p0) * K;
+    if (items == 0) break;
+    const int bstar = sh.bstar;
+    const int per = (items + kThreads - 1) / kThreads;  // contiguous items per thread
+    if (per > 4) {                                       // too wide a level: sequential path
+      if (tid == 0) sh.flag = 1;
+      __syncthreads();
+      break;
+    }
+    // evaluate this thread's candidates once: child r of stored node p at depth d
+    double qv[4], uv[4];
+    int mv[4], bv[4];
+    bool okv[4];
+    int cnt = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int it = tid * per + k;
+      okv[k] = false;
+      qv[k] = uv[k] = 0.0;
+      mv[k] = bv[k] = 0;
+      if (k < per && it < items) {
+        const int p = p0 + it / K, r = it - (it / K) * K;
+        const uint64_t pu = L.u[p];
+        if (ubin(__longlong_as_double((long long)pu)) >= bstar) {
+          const double q = L.q[p] * sh.c[d][r];
+          const double u = q / sh.den[d + 1];
+          const int bn = ubin(u);
+          okv[k] = u > tau && bn >= bstar;
+          qv[k] = q;
+          uv[k] = u;
+          bv[k] = bn;
+          mv[k] = (p << 16) | ((d + 1) << 8) | r;
+        }
+      }
+      cnt += okv[k] ? 1 : 0;
+    }
+    int total;
+    const int pre = block_prefix<3>(cnt, sh.wsum, total);
+    const int base = sh.total;
+    if (base + total > kCap) {
+      if (tid == 0) sh.flag = 1;
+      __syncthreads();
+      break;
+    }
+    int pos = base + pre;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (okv[k]) {
+        L.q[pos] = qv[k];
+        L.u[pos] = ubits(uv[k]);
+        L.meta[pos] = mv[k];
+        atomicAdd(&L.hist[bv[k]], 1);
+        ++pos;
+      }
+    }
+    __syncthreads();
+    if (tid == 0) {
+      sh.total = base + total;
+      L.lvl_start[d + 2] = base + total;
+    }
+    // new b*: the highest bin whose suffix count reaches N-1 (0 while fewer nodes exist)
+    if (wave == 0) {
+      constexpr int BPL = kBins / kWave;  // bins per lane
+      int hv[BPL];
+#pragma unroll
+      for (int j = 0; j < BPL / 4; ++j) {
+        const int4 h4 = *(const int4*)&L.hist[lane * BPL + 4 * j];
+        hv[4 * j] = h4.x; hv[4 * j + 1] = h4.y; hv[4 * j + 2] = h4.z; hv[4 * j + 3] = h4.w;
+      }
+      int sl = 0;
+#pragma unroll
+      for (int j = 0; j < BPL; ++j) sl += hv[j];
+      int tot_all;
+      const int below = wave_prefix_small<12>(sl, tot_all);
+      const int suffix = tot_all - below;            // nodes in this lane's bins and above
+      const uint64_t ok = __ballot(N > 1 && suffix >= N - 1);
+      if (ok != 0ull) {
+        const int Ls = 63 - __clzll((long long)ok);
+        if (lane == Ls) {
+          // the highest bin j of this lane whose suffix count reaches N-1
+          int run = suffix - sl;
+          int bsel = Ls * BPL;
+          bool found = false;
+#pragma unroll
+          for (int j = BPL - 1; j >= 0; --j) {
+            run += hv[j];
+            if (!found && run >= N - 1) { bsel = Ls * BPL + j; found = true; }
+          }
+          sh.bstar = bsel;
+        }
+      } else if (lane == 0) {
+        sh.bstar = 0;
+      }
+    }
+    __syncthreads();
+  }
+  int n;
+  const bool fallback = sh.flag != 0;
+  if (!fallback) {
+    // ---- final cut: keep bins > b*, rank the members of bin b* exactly
+    const int tot = sh.total, bstar = sh.bstar;
+    const int per = (tot + kThreads - 1) / kThreads;   // <= 3
+    int above = 0, inb = 0;
+    for (int k = 0; k < per; ++k) {
+      const int j = tid * per + k;
+      if (j >= 1 && j < tot) {
+        const int bn = ubin(__longlong_as_double((long long)L.u[j]));
+        above += bn > bstar ? 1 : 0;
+        inb += bn == bstar ? 1 : 0;
+      }
+    }
+    int c_hi, c_b;
+    block_prefix<2>(above, sh.wsum, c_hi);
+    int mpos = block_prefix<2>(inb, sh.wsum, c_b);
+    for (int k = 0; k < per; ++k) {
+      const int j = tid * per + k;
+      if (j >= 1 && j < tot && ubin(__longlong_as_double((long long)L.u[j])) == bstar)
+        L.mlist[mpos++] = j;
+    }
+    const int room = N - 1 - c_hi;   // places left for members of bin b*
+    __syncthreads();
+    for (int j = tid; j < tot; j += kThreads) {
+      int keep = 0;
+      if (j == 0) {
+        keep = 1;
+      } else {
+        const int bn = ubin(__longlong_as_double((long long)L.u[j]));
+        keep = bn > bstar || (bn == bstar && c_b <= room);
+      }
+      L.newidx[j] = keep;
+    }
+    if (c_b > room) {
+      // members ranked by (u desc, stored index asc); the stored index orders equal
+      // utilities exactly like (depth, rank path)
+      for (int i = tid; i < c_b; i += kThreads) {
+        const int j = L.mlist[i];
+        const uint64_t uj = L.u[j];
+        int rank = 0;
+        for (int k0 = 0; k0 < c_b; k0 += 8) {
+          uint64_t ukv[8];
+          int jk[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) {
+            jk[t] = k0 + t < c_b ? L.mlist[k0 + t] : 0x7FFFFFFF;
+            ukv[t] = k0 + t < c_b ? L.u[jk[t]] : 0ull;
+          }
+#pragma unroll
+          for (int t = 0; t < 8; ++t)
+            rank += (k0 + t < c_b && (ukv[t] > uj || (ukv[t] == uj && jk[t] < j))) ? 1 : 0;
+        }
+        L.newidx[j] = rank < room ? 1 : 0;
+      }
+    }
+    __syncthreads();
+    // breadth-first compaction: stored order is already (depth, rank path)
+    int cnt = 0;
+    for (int k = 0; k < per; ++k) {
+      const int j = tid * per + k;
+      cnt += j < tot ? L.newidx[j] : 0;
+    }
+    int total;
+    int pre = block_prefix<4>(cnt, sh.wsum, total);
+    for (int k = 0; k < per; ++k) {
+      const int j = tid * per + k;
+      if (j < tot) {
+        const int keep = L.newidx[j];
+        L.newidx[j] = keep ? pre : -1;
+        pre += keep;
+      }
+    }
+    __syncthreads();
+    n = total;
+    for (int j = tid; j < tot; j += kThreads) {
+      const int o = L.newidx[j];
+      if (o >= 0) {
+        const size_t g = (size_t)b * N + o;
+        const int meta = L.meta[j];
+        const int dj = (meta >> 8) & 0xFF, rj = meta & 0xFF, pj = meta >> 16;
+        o_parent[g] = j == 0 ? -1 : L.newidx[pj];
+        o_depth[g] = dj;
+        o_rank[g] = j == 0 ? -1 : rj;
+        o_token[g] = j == 0 ? -1 : (int32_t)cand_index(sh.top[dj - 1][rj]);
+        o_q[g] = L.q[j];
+      }
+    }
+  } else {
+    __syncthreads();
+    n = select_sequential<SLOTS>(sh, D, K, N, tau);
+    Seq& S = sh.x.s;
+    for (int j = tid; j < n; j += kThreads) {
+      const size_t g = (size_t)b * N + S.order[j];
+      o_parent[g] = j == 0 ? -1 : S.order[S.par[j]];
+      o_depth[g] = S.depth[j];
+      o_rank[g] = S.rank[j];
+      o_token[g] = j == 0 ? -1 : (int32_t)cand_index(sh.top[S.depth[j] - 1][S.rank[j]]);
+      o_q[g] = j == 0 ? 1.0 : S.Q[S.par[j]][S.rank[j]];
+    }
+  }
+  // ---------------- Phase D: pad the unused slots
+  for (int j = n + tid; j < N; j += kThreads) {
+    const size_t g = (size_t)b * N + j;
+    o_parent[g] = -1; o_depth[g] = -1; o_rank[g] = -1; o_token[g] = -1; o_q[g] = 0.0;
   }
   if (tid == 0) o_n[b] = n;
 }

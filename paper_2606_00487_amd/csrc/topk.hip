@@ -93,7 +93,6 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __rest
                                                               uint64_t* __restrict__ cand) {
   __shared__ uint64_t s_cand[kWaves][kWaveCap];
   __shared__ uint64_t s_wave_top[kWaves][TAPS_MAX_K];
-  __shared__ int s_over[kWaves];
 
   const int row = blockIdx.x / chunks;
   const int chunk = blockIdx.x - row * chunks;
@@ -130,27 +129,21 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __rest
       if (__popcll(__ballot(has && lkey >= c)) >= K) T = c;
     }
   }
-  // compact all elements with key >= T (T = 0 keeps every valid element)
-  int cnt = 0;
+  // compact all elements with key >= T (T = 0 keeps every valid element), in element
+  // order, with one ballot per register slot
+  int total = 0;
 #pragma unroll
-  for (int j = 0; j < E; ++j)
-    cnt += (key[j] >= T && elem_index<DT, E>(aligned, start, tid, j) < end) ? 1 : 0;
-  int incl = cnt;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int o = __shfl_up(incl, off);
-    if (lane >= off) incl += o;
-  }
-  const int total = __shfl(incl, kWave - 1);
-  int pos = incl - cnt;
-  if (total <= kWaveCap) {
-#pragma unroll
-    for (int j = 0; j < E; ++j) {
-      const int e = elem_index<DT, E>(aligned, start, tid, j);
-      if (key[j] >= T && e < end) s_cand[wave][pos++] = cand_key(key[j], (uint32_t)e);
+  for (int j = 0; j < E; ++j) {
+    const int e = elem_index<DT, E>(aligned, start, tid, j);
+    const bool c = key[j] >= T && e < end;
+    const uint64_t m = __ballot(c);
+    if (m) {
+      const int pos = total + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      if (c && pos < kWaveCap) s_cand[wave][pos] = cand_key(key[j], (uint32_t)e);
+      total += __popcll(m);
     }
   }
-  if (lane == 0) s_over[wave] = total > kWaveCap;
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");

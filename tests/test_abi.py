@@ -90,6 +90,8 @@ def test_select_rejects_null_buffers_and_small_workspace(lib):
     ((1, 64, 32, 8, 128, -1, 0, 0.088), _lib.TAPS_ERR_INVALID_ARG),
     ((1, 64, 32, 8, 128, 8192, 3, 0.088), _lib.TAPS_ERR_INVALID_ARG),
     ((1, 64, 32, 8, 128, 8192, 0, math.inf), _lib.TAPS_ERR_INVALID_ARG),
+    ((1, 64, 32, 8, 128, 8192, 0, 0.0), _lib.TAPS_ERR_INVALID_ARG),
+    ((1, 64, 32, 8, 128, 8192, 0, -0.5), _lib.TAPS_ERR_INVALID_ARG),
     ((0, 64, 32, 8, 128, 8192, 0, 0.088), _lib.TAPS_OK),
     ((1, 16, 4, 2, 64, 256, 1, 0.125), _lib.TAPS_OK),
 ])

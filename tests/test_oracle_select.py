@@ -12,7 +12,8 @@ import numpy as np
 import pytest
 
 from oracle.select import (LOGITS, PROBS, topk_row, edge_factors, denominators,
-                           select_request, select_literal_alg1, brute_force_best_set)
+                           select_request, select_literal_alg1, brute_force_best_set,
+                           enumerate_trie)
 from workloads import CONFIGS, gen_marginals, bf16_bits_to_f32
 
 
@@ -110,6 +111,7 @@ def _check_invariants(tree, D, K, budget, tau):
     assert 1 <= n <= budget
     assert tree.parent[0] == -1 and tree.depth[0] == 0 and tree.q_reach[0] == 1.0
     seen = set()
+    paths = tree.paths()
     for i in range(1, n):
         p = int(tree.parent[i])
         assert 0 <= p < i                                   # topological, prefix-closed
@@ -121,7 +123,8 @@ def _check_invariants(tree, D, K, budget, tau):
         assert tree.q_reach[i] <= tree.q_reach[p]           # Eq. 2 never grows along a path
         assert tree.utility[i] <= tree.utility[p]
         assert tree.utility[i] > tau
-        assert tree.utility[i] <= tree.utility[i - 1] or i == 1   # emitted in best-first order
+        prev = (int(tree.depth[i - 1]), paths[i - 1])
+        assert prev < (int(tree.depth[i]), paths[i])      # emitted breadth first
     assert np.all(tree.parent[n:] == -1) and np.all(tree.q_reach[n:] == 0.0)
 
 
@@ -158,7 +161,7 @@ def test_selection_equals_brute_force(seed):
     order = sorted((p for p in nodes if p),
                    key=lambda p: (-nodes[p][1], len(p), p))
     above = [p for p in order if nodes[p][1] > tau]
-    assert tree.paths()[1:] == above[:budget - 1]
+    assert sorted(tree.paths()[1:]) == sorted(above[:budget - 1])
 
 
 @pytest.mark.parametrize("seed", range(8))
@@ -172,7 +175,10 @@ def test_selection_equals_literal_alg1(seed):
     den = denominators(D, 1.0, 0.125)
     S, added_ancestor = select_literal_alg1(c, den, budget, tau)
     assert not added_ancestor
-    assert S == tree.paths()
+    assert sorted(S) == sorted(tree.paths())
+    # Alg. 1 adds nodes in non-increasing utility
+    u = {p: enumerate_trie(c, den)[p][1] for p in S}
+    assert all(u[a] >= u[b] for a, b in zip(S[1:], S[2:]))
 
 
 def test_selection_tiny_config_literal_alg1():
@@ -182,7 +188,7 @@ def test_selection_tiny_config_literal_alg1():
     c = edge_factors(tree.topk_val, cfg.kind, 1.0)
     den = denominators(cfg.block, 1.0, 0.125)
     S, added = select_literal_alg1(c, den, cfg.budget, 0.0)    # 4-ary trie of depth 8: 87,381 nodes
-    assert not added and S == tree.paths()
+    assert not added and sorted(S) == sorted(tree.paths())
     _check_invariants(tree, cfg.block, cfg.K, cfg.budget, 0.0)
 
 
@@ -195,7 +201,7 @@ def test_uniform_marginals_give_breadth_first_lex(K, D, budget):
     bfs = [()]
     for d in range(1, D + 1):
         bfs += list(itertools.product(range(K), repeat=d))
-    assert tree.paths() == bfs[:budget]
+    assert tree.paths() == bfs[:budget]          # here the best-first order is breadth first too
 
 
 @pytest.mark.parametrize("D,budget", [(5, 3), (5, 6), (5, 40)])
@@ -246,10 +252,12 @@ def test_hand_worked_depth_penalty_decides_between_branches():
     # PROBS rows: depth-1 weights 3/4, 1/4; depth-2 weights 0.6, 0.4; lambda1 = lambda2 = 1,
     # so den = (1, 2, 3) and u(0) = 3/8, u(1) = 1/8, u(0,0) = 0.45/3 = 0.15, u(0,1) = 0.1
     rows = np.array([[0.75, 0.25, 0.0], [0.6, 0.4, 0.0]])
+    t = select_request(rows, 2, 3, kind=PROBS, lambda1=1.0, lambda2=1.0)
+    assert t.paths() == [(), (0,), (0, 0)]       # (0,0) beats (1,): 0.15 > 0.125
+    assert t.utility[1] == 0.375 and abs(t.utility[2] - 0.15) < 1e-16
     t = select_request(rows, 2, 4, kind=PROBS, lambda1=1.0, lambda2=1.0)
-    assert t.paths() == [(), (0,), (0, 0), (1,)]
-    assert t.utility[1] == 0.375 and t.utility[3] == 0.125
-    assert abs(t.utility[2] - 0.15) < 1e-16
+    assert t.paths() == [(), (0,), (1,), (0, 0)]  # breadth-first emission
+    assert t.utility[2] == 0.125
 
 
 def test_hand_worked_chain_utilities():
