@@ -277,7 +277,7 @@ __global__ __launch_bounds__(256 * WK) void attn_bf16_kernel(
       }
       // ---- mask (only tiles that reach the tree rows or the split end), online softmax
       const bool need_mask = k0 + kKT > ctx || k0 + kKT > k_end;
-      bf16x8 p[2][QB][2];
+      float nrefv[QB];
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
         if (need_mask) {
@@ -289,7 +289,8 @@ __global__ __launch_bounds__(256 * WK) void attn_bf16_kernel(
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
               const uint32_t word = kb ? mhi : mlo;
-              if (!((word >> (8 * (v >> 2) + (v & 3))) & 1u)) s[kb][qb][v] = -INFINITY;
+              const bool ok = (word >> (8 * (v >> 2) + (v & 3))) & 1u;
+              s[kb][qb][v] = ok ? s[kb][qb][v] : -INFINITY;
             }
         }
         float mx = -INFINITY;
@@ -310,39 +311,37 @@ __global__ __launch_bounds__(256 * WK) void attn_bf16_kernel(
             for (int v = 0; v < 16; ++v) o[db][qb][v] *= alpha;
           m_ref[qb] = nref;
         }
-        const float nref = m_ref[qb] == -INFINITY ? 0.f : -m_ref[qb];
-        float sum = 0.f;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int hf = 0; hf < 2; ++hf) {
-            bf16x8 pk8;
-#pragma unroll
-            for (int t = 0; t < 8; ++t) {
-              const float e = __builtin_amdgcn_exp2f(fmaf(s[kb][qb][hf * 8 + t], scale_log2, nref));
-              sum += e;
-              pk8[t] = (__bf16)e;
-            }
-            p[kb][qb][hf] = pk8;
-          }
-        l_run[qb] += sum;
+        nrefv[qb] = m_ref[qb] == -INFINITY ? 0.f : -m_ref[qb];
       }
-      // ---- O^T += V^T P^T; V^T operands by transposing reads of the row-major V tile
+      // ---- P = exp2(scale*s - ref) and O^T += V^T P^T in four groups of 8 keys per lane
+      // half: the exponentials of one group are independent of the MFMAs of the previous
+      // group, so the two overlap.  V^T operands come from transposing reads of the
+      // row-major V tile.
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const int vo = voff[db & 1] + 64 * (db & ~1);
+      for (int grp = 0; grp < 4; ++grp) {
+        const int kb = grp >> 1, hf = grp & 1;
+        bf16x8 pg[QB];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int qb = 0; qb < QB; ++qb) {
+          float sum = 0.f;
 #pragma unroll
-          for (int hf = 0; hf < 2; ++hf) {
-            const unsigned char* va = tv + (kb * 32 + 16 * hf) * ROWB + vo;
-            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)va);
-            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va + 8 * ROWB));
-            const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-#pragma unroll
-            for (int qb = 0; qb < QB; ++qb)
-              o[db][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p[kb][qb][hf], o[db][qb], 0, 0, 0);
+          for (int t = 0; t < 8; ++t) {
+            const float e = __builtin_amdgcn_exp2f(fmaf(s[kb][qb][hf * 8 + t], scale_log2, nrefv[qb]));
+            sum += e;
+            pg[qb][t] = (__bf16)e;
           }
+          l_run[qb] += sum;
+        }
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const unsigned char* va = tv + (kb * 32 + 16 * hf) * ROWB + voff[db & 1] + 64 * (db & ~1);
+          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)va);
+          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va + 8 * ROWB));
+          const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            o[db][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pg[qb], o[db][qb], 0, 0, 0);
+        }
       }
     }
     __builtin_amdgcn_s_barrier();    // the stage is free for the loads issued next iteration

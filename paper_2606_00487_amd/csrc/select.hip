@@ -336,13 +336,9 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
         const int e = j * kWave + lane;
         v[j] = e < CK ? rc[e] : 0ull;
       }
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int e = j * kWave + lane;
-        if (e < CK && e % K == 0) A.heads[wave][e / K] = v[j];
-      }
+      const uint64_t head = lane < chunks ? rc[(size_t)lane * K] : 0ull;
+      A.heads[wave][lane] = head;
       wave_fence();
-      uint64_t head = lane < chunks ? A.heads[wave][lane] : 0ull;
       int beat = 0;
       for (int j0 = 0; j0 < chunks; j0 += 8) {
         uint64_t hv[8];
@@ -452,14 +448,17 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     int mv[4], bv[4];
     bool okv[4];
     int cnt = 0;
+    const int it0 = tid * per;
+    int pp = p0 + it0 / K, rr = it0 - (it0 / K) * K;   // (parent, rank) of the first item
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const int it = tid * per + k;
+      const int it = it0 + k;
       okv[k] = false;
       qv[k] = uv[k] = 0.0;
       mv[k] = bv[k] = 0;
+      const int p = pp, r = rr;
+      if (++rr == K) { rr = 0; ++pp; }
       if (k < per && it < items) {
-        const int p = p0 + it / K, r = it - (it / K) * K;
         const uint64_t pu = L.u[p];
         if (ubin(__longlong_as_double((long long)pu)) >= bstar) {
           const double q = L.q[p] * sh.c[d][r];

@@ -35,6 +35,35 @@ __device__ inline uint64_t wave_max_u64(uint64_t v) {
   return v;
 }
 
+
+__device__ inline void wave_fence_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// after every wave wrote its sorted top-K list at s_top[w*K ...]: wave 0 merges the
+// kWaves lists (at most 64 entries, one per lane) and writes the chunk's K best keys
+__device__ inline void merge_and_store(const uint64_t* s_top, int K, int wave, int lane,
+                                       uint64_t* outp) {
+  __syncthreads();
+  if (wave != 0) return;
+  const int tot = kWaves * K;
+  const uint64_t mine = lane < tot ? s_top[lane] : 0ull;
+  int rank = 0;
+  for (int j0 = 0; j0 < tot; j0 += 8) {
+    uint64_t cv[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) cv[t] = j0 + t < tot ? s_top[j0 + t] : 0ull;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) rank += cv[t] > mine ? 1 : 0;
+  }
+  if (lane < tot && mine != 0ull && rank < K) outp[rank] = mine;
+  // ranks held by empty entries: write 0 (a chunk with fewer than K elements)
+  const int nonempty = __popcll(__ballot(lane < tot && mine != 0ull));
+  if (lane >= nonempty && lane < K) outp[lane] = 0ull;
+}
+
 template <int DT>
 __device__ inline uint32_t elem_bits(const void* row, int64_t i) {
   if (DT == TAPS_BF16) return (uint32_t)((const uint16_t*)row)[i] << 16;
@@ -86,23 +115,11 @@ __device__ inline int elem_index(bool aligned, int start, int tid, int j) {
   return aligned ? start + (tid + kThreads * (j / U)) * U + (j % U) : start + tid + kThreads * j;
 }
 
+// Any chunk, any dtype: the wave's K best keys into s_wave_top[wave*K ...].
 template <int DT, int E>
-__global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __restrict__ marg,
-                                                              int vocab, int K, int chunk_len,
-                                                              int chunks,
-                                                              uint64_t* __restrict__ cand) {
-  __shared__ uint64_t s_cand[kWaves][kWaveCap];
-  __shared__ uint64_t s_wave_top[kWaves][TAPS_MAX_K];
-
-  const int row = blockIdx.x / chunks;
-  const int chunk = blockIdx.x - row * chunks;
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  const int start = chunk * chunk_len;
-  const int end = min(vocab, start + chunk_len);
-  const size_t es = DT == TAPS_BF16 ? 2 : 4;
-  const void* rowp = (const char*)marg + (size_t)row * vocab * es;
-  const bool aligned = (((uintptr_t)rowp) & 15) == 0;
-
+__device__ inline void generic_wave_topk(const void* rowp, bool aligned, int start, int end,
+                                         int tid, int lane, int wave, int K, uint64_t* s_wc,
+                                         uint64_t* s_wave_top) {
   uint32_t key[E];
   load_chunk<DT, E>(rowp, aligned, start, end, tid, key);
   // element keys are value keys; valid elements have an index < end.  Keys of missing
@@ -115,8 +132,8 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __rest
     any |= ok;
     lmax = (ok && key[j] >= lmax) ? key[j] : lmax;
   }
-  // lanes without elements take no part in the threshold; valid keys shifted by one so
-  // that a NaN-only lane (key 0) still counts
+  // lanes without elements take no part in the threshold; a NaN-only lane takes part
+  // with key 0
   const uint32_t lkey = any ? lmax : 0u;
   const bool has = any;
   // K-th largest lane maximum by bitwise descent (over value-key bits)
@@ -140,24 +157,28 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __rest
     if (m) {
       const int pos = total + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-      if (c && pos < kWaveCap) s_cand[wave][pos] = cand_key(key[j], (uint32_t)e);
+      if (c && pos < kWaveCap) s_wc[pos] = cand_key(key[j], (uint32_t)e);
       total += __popcll(m);
     }
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  wave_fence_lds();
 
   if (total <= kWaveCap) {
     // exact rank of each compacted candidate within the wave
     for (int c0 = 0; c0 < total; c0 += kWave) {
       const int me = c0 + lane;
-      const uint64_t mine = me < total ? s_cand[wave][me] : 0ull;
+      const uint64_t mine = me < total ? s_wc[me] : 0ull;
       int rank = 0;
-      for (int j = 0; j < total; ++j) rank += s_cand[wave][j] > mine ? 1 : 0;
-      if (me < total && rank < K) s_wave_top[wave][rank] = mine;
+      for (int j0 = 0; j0 < total; j0 += 8) {
+        uint64_t cv[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) cv[t] = j0 + t < total ? s_wc[j0 + t] : 0ull;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) rank += cv[t] > mine ? 1 : 0;
+      }
+      if (me < total && rank < K) s_wave_top[wave * K + rank] = mine;
     }
-    for (int r = total + lane; r < K; r += kWave) s_wave_top[wave][r] = 0ull;
+    for (int r = total + lane; r < K; r += kWave) s_wave_top[wave * K + r] = 0ull;
   } else {
     // fallback: K rounds of exact argmax over the wave's elements
     uint64_t prev = ~0ull;
@@ -170,30 +191,95 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __rest
         best = (k < prev && k > best) ? k : best;
       }
       best = wave_max_u64(best);
-      if (lane == 0) s_wave_top[wave][r] = best;
+      if (lane == 0) s_wave_top[wave * K + r] = best;
       prev = best;
     }
   }
-  __syncthreads();
+}
 
-  // merge the wave lists: rank each of the kWaves*K entries
-  if (wave == 0) {
-    const int tot = kWaves * K;
-    uint64_t* outp = cand + ((size_t)row * chunks + chunk) * K;
-    for (int c0 = 0; c0 < tot; c0 += kWave) {
-      const int me = c0 + lane;
-      const uint64_t mine = me < tot ? s_wave_top[me / K][me % K] : 0ull;
-      int rank = 0;
-      for (int j = 0; j < tot; ++j) rank += s_wave_top[j / K][j % K] > mine ? 1 : 0;
-      if (me < tot && mine != 0ull && rank < K) outp[rank] = mine;
-    }
-    // ranks held by empty entries: write 0 (a chunk with fewer than K elements)
-    int nonempty = 0;
-    for (int j = lane; j < tot; j += kWave) nonempty += s_wave_top[j / K][j % K] != 0ull;
+template <int DT, int E>
+__global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __restrict__ marg,
+                                                              int vocab, int K, int chunk_len,
+                                                              int chunks,
+                                                              uint64_t* __restrict__ cand) {
+  __shared__ uint64_t s_cand[kWaves][kWaveCap];
+  __shared__ uint64_t s_wave_top[kWaves * TAPS_MAX_K];   // wave w's list at w*K
+
+  const int row = blockIdx.x / chunks;
+  const int chunk = blockIdx.x - row * chunks;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int start = chunk * chunk_len;
+  const int end = min(vocab, start + chunk_len);
+  const size_t es = DT == TAPS_BF16 ? 2 : 4;
+  const void* rowp = (const char*)marg + (size_t)row * vocab * es;
+  const bool aligned = (((uintptr_t)rowp) & 15) == 0;
+
+  bool done = false;
+  if (DT == TAPS_BF16 && aligned && end - start == chunk_len) {
+    // ---- fast path: a full, aligned bf16 chunk.  Filtering uses float compares (NaN
+    // fails every compare, -0 equals +0, exactly like the integer keys); exact keys are
+    // built only for the few candidates.
+    uint32_t w[E / 2];
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) nonempty += __shfl_xor(nonempty, off);
-    for (int r = nonempty + lane; r < K; r += kWave) outp[r] = 0ull;
+    for (int k = 0; k < E / 8; ++k) {
+      const uint4 u = *(const uint4*)((const char*)rowp + (int64_t)(start + (tid + kThreads * k) * 8) * 2);
+      w[4 * k] = u.x; w[4 * k + 1] = u.y; w[4 * k + 2] = u.z; w[4 * k + 3] = u.w;
+    }
+    float mx = -INFINITY;
+    bool anynum = false;
+#pragma unroll
+    for (int j = 0; j < E / 2; ++j) {
+      const float lo = __uint_as_float(w[j] << 16), hi = __uint_as_float(w[j] & 0xFFFF0000u);
+      mx = fmaxf(mx, fmaxf(lo, hi));   // ignores NaN
+      anynum |= lo == lo || hi == hi;
+    }
+    const bool lane_ok = anynum;                     // the lane holds a non-NaN value
+    if (__popcll(__ballot(lane_ok)) >= K) {          // uniform per wave
+      const uint32_t lk = lane_ok ? (value_key(__float_as_uint(mx)) >> 16) : 0u;
+      uint32_t T = 0;
+      for (int bit = 15; bit >= 0; --bit) {
+        const uint32_t c = T | (1u << bit);
+        if (__popcll(__ballot(lk >= c)) >= K) T = c;
+      }
+      const float tf = __uint_as_float((T & 0x8000u) ? ((T & 0x7FFFu) << 16) : (~(T << 16) & 0xFFFF0000u));
+      // compact the elements >= tf, in element order
+      int total = 0;
+#pragma unroll
+      for (int j = 0; j < E; ++j) {
+        const uint32_t bits = (j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16);
+        const bool c = __uint_as_float(bits) >= tf;
+        const uint64_t m = __ballot(c);
+        if (m) {
+          const int pos = total + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                            __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+          const int e = start + (tid + kThreads * (j / 8)) * 8 + (j % 8);
+          if (c && pos < kWaveCap) s_cand[wave][pos] = cand_key(value_key(bits), (uint32_t)e);
+          total += __popcll(m);
+        }
+      }
+      if (total <= kWaveCap) {
+        wave_fence_lds();
+        for (int c0 = 0; c0 < total; c0 += kWave) {
+          const int me = c0 + lane;
+          const uint64_t mine = me < total ? s_cand[wave][me] : 0ull;
+          int rank = 0;
+          for (int j0 = 0; j0 < total; j0 += 8) {
+            uint64_t cv[8];
+#pragma unroll
+            for (int t = 0; t < 8; ++t) cv[t] = j0 + t < total ? s_cand[wave][j0 + t] : 0ull;
+#pragma unroll
+            for (int t = 0; t < 8; ++t) rank += cv[t] > mine ? 1 : 0;
+          }
+          if (me < total && rank < K) s_wave_top[wave * K + rank] = mine;
+        }
+        done = true;
+      }
+    }
+    // rare: too few non-NaN lanes or too many ties for the compaction buffer
   }
+  if (!done) generic_wave_topk<DT, E>(rowp, aligned, start, end, tid, lane, wave, K,
+                                      s_cand[wave], s_wave_top);
+  merge_and_store(s_wave_top, K, wave, lane, cand + ((size_t)row * chunks + chunk) * K);
 }
 
 template <int DT>

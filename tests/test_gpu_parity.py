@@ -113,6 +113,39 @@ def test_select_fuzz(taps, seed):
     U.assert_tree_equal(gpu, trees, cfg)
 
 
+@pytest.mark.parametrize("mode", ["ties", "specials", "plain", "deep", "sparse_nan", "flat"])
+@pytest.mark.parametrize("V,K", [(32768, 8), (151936, 16), (151936, 1)])
+def test_select_full_aligned_chunks(taps, mode, V, K):
+    """bf16 rows whose chunks are all full and 16-byte aligned (vocab a multiple of 8):
+    the vocabulary scan's fast filter path, and its fall-backs (fewer than K non-NaN
+    lanes in a wave, more tied candidates than the compaction buffer holds)."""
+    rng = np.random.default_rng(7000 + V + K + len(mode))
+    cfg = _fuzz_cfg(rng, BF16, LOGITS, V, 6, K, 64)
+    say(f"[full-chunks] mode={mode} V={V} K={K}")
+    if mode in ("ties", "specials", "plain", "deep"):
+        m = _fuzz_marginals(rng, cfg, mode)
+    else:
+        x = np.full((cfg.batch, cfg.block, V), np.nan, dtype=np.float32)
+        if mode == "sparse_nan":
+            # a few finite values per row: most waves hold fewer than K of them
+            for b in range(cfg.batch):
+                for d in range(cfg.block):
+                    pos = rng.choice(V, size=int(rng.integers(1, 3 * K + 2)), replace=False)
+                    x[b, d, pos] = rng.standard_normal(pos.size)
+        else:
+            x[:] = 0.25                                   # every element ties
+            x[:, :, ::977] = -0.0
+        from workloads import f32_to_bf16_bits
+        m = f32_to_bf16_bits(x)
+    from workloads import bf16_bits_to_f32
+    xf = bf16_bits_to_f32(m).astype(np.float64)
+    trees = [oracle.select_request(xf[b], K, cfg.budget, kind=LOGITS) for b in range(cfg.batch)]
+    sel = taps.Selector(cfg.batch, cfg.block, V, K, cfg.budget, dtype=BF16, kind=LOGITS)
+    gpu = sel(U.to_dev(m, True))
+    torch.cuda.synchronize()
+    U.assert_tree_equal(gpu, trees, cfg)
+
+
 def test_select_is_deterministic(taps):
     inp = gen_round("qwen3_8b", with_attention=False)
     a, sel, m = run_select(taps, inp)
