@@ -77,7 +77,6 @@ def main():
     args = parse()
     if args.copy_calibration:
         copy_calibration()
-        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus "
               f"{args.gpus}); run with --gpus 1", file=sys.stderr)

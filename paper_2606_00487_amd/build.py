@@ -4,7 +4,8 @@
 
 Every .hip file is compiled to an object with hipcc, the selection kernel with
 -ffp-contract=off (its fp64 scores must round every product and sum separately),
-then everything is linked into paper_2606_00487_amd/libtaps.so.
+the attention kernel with MFMA results in ordinary vector registers; then
+everything is linked into paper_2606_00487_amd/libtaps.so.
 """
 from __future__ import annotations
 
@@ -25,6 +26,9 @@ COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", f"--offload-arch={ARCH}",
 PER_FILE = {
     "select.hip": ["-ffp-contract=off"],
     "api.cpp": ["-ffp-contract=off"],
+    # MFMA accumulators in ordinary VGPRs: the attention kernel fits in 256 of them, and
+    # the AGPR form would copy its accumulators back and forth around every softmax
+    "attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
 SOURCES = ["topk.hip", "select.hip", "attn.hip", "walk.hip", "api.cpp"]
 

@@ -19,6 +19,7 @@
 // fp32 path: a plain VALU kernel, one workgroup per (request, node, query head).
 #include <cstdio>
 #include <cstdlib>
+#include <type_traits>
 
 #include "common.h"
 
@@ -77,6 +78,14 @@ __device__ inline uint64_t low_bits(int j) {
   return j <= 0 ? 0ull : (j >= 64 ? ~0ull : ((1ull << j) - 1ull));
 }
 
+// the value held by lane l ^ 32 (a VALU lane swap, no LDS round trip)
+__device__ inline float other_half(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  // r[0]: lanes 0-31 keep x, lanes 32-63 get x[l-32]; r[1]: lanes 0-31 get x[l+32]
+  return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
+}
+
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 typedef __attribute__((address_space(3))) void lds_void;
@@ -86,6 +95,10 @@ typedef __attribute__((address_space(3))) void lds_void;
 #define TAPS_WAIT_VMCNT(n) \
   __builtin_amdgcn_s_waitcnt(((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (7 << 4) | (15 << 8))
 
+// workgroup barrier for the stage buffers: the explicit vmcnt waits before it cover the
+// direct loads; the memory clobber keeps the compiler from moving LDS accesses across it
+#define TAPS_STAGE_BARRIER() asm volatile("s_barrier" ::: "memory")
+
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
@@ -94,41 +107,59 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 // at once, land on distinct LDS banks
 __device__ inline int kswz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
 
-// QB: 32-row query blocks per wave; WK: key groups (each iteration stages WK tiles, wave
-// group kg = wave / 4 works on tile kg; the groups merge their results in LDS at the end).
-// K and V tiles go from global memory straight into LDS (16 bytes per lane), row-major
-// with the 16-byte chunks of key row r XOR-permuted by kswz(r); two stages alternate so
-// the next iteration's tiles load while the current ones are used.  V^T operands are
-// read with the transposing LDS read: in each 16-lane group, lane i gets element i % 4
-// of the 8 bytes read by lanes 4t + i/4 (t = 0..3), i.e. 4 consecutive keys at its d.
+// One workgroup: four waves, 32 query rows each (S^T and O^T tiles of one 32x32 MFMA
+// block per 32 keys and per 32 head dimensions), one 64-key stage of K and V per step.
+// K and V tiles go from global memory straight into LDS with buffer loads (16 bytes per
+// lane), row-major with the 16-byte chunks of key row r XOR-permuted by kswz(r).  The
+// buffer resources cover exactly this split's rows, so rows past the split's end read as
+// zeros without touching memory: the look-ahead needs no bounds logic.  V^T operands are
+// read with the transposing LDS read: in each 16-lane group, lane i gets element i % 4 of
+// the 8 bytes read by lanes 4t + i/4 (t = 0..3), i.e. 4 consecutive keys at its d.
+//
+// Software pipeline over stages i = 0, 1, ...: step i applies the softmax to S(i) and
+// accumulates P(i) V(i) while the MFMAs of S(i+1) = K(i+1) Q^T run in between; the loads
+// of V(i+3) and K(i+4) are issued at the start of step i, so every load has three steps
+// to arrive.  K and V each cycle through NBUF = 4 LDS buffers.
+//
 // The grid is one-dimensional: the query-row tiles of one (request, KV head, split) get
 // block ids that differ by multiples of 8, so they run on the same XCD and share its L2.
-template <int QB, int WK, int HD>
-__global__ __launch_bounds__(256 * WK) void attn_bf16_kernel(
+template <int HD>
+__global__ __launch_bounds__(256) void attn_bf16_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc,
     const uint16_t* __restrict__ Vc, const int64_t* __restrict__ offp,
     const int32_t* __restrict__ ctxp, const int32_t* __restrict__ parentp,
     const int32_t* __restrict__ nnp, int N, int Hq, int Hkv, int max_ctx, float scale_log2,
     int split_len, int splits, int mtiles, int pairs, int mrows_pad, float* __restrict__ wsO,
     float2* __restrict__ wsML) {
-  constexpr int NT = 256 * WK;
-  constexpr int NW = 4 * WK;
+  // the body uses the buffer-resource type, which exists only in the device pass; the
+  // host pass needs no more than the signature to emit the launch stub
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int NT = 256;
+  constexpr int NW = 4;
   constexpr int ROWB = HD * 2;        // bytes per K/V row
-  constexpr int MT = 4 * 32 * QB;     // query rows per workgroup
+  constexpr int MT = 4 * 32;          // query rows per workgroup
   constexpr int NDB = HD / 32;        // 32-row blocks of O^T
   constexpr int NKK = HD / 16;        // MFMA k-steps over head_dim
-  constexpr int TILEB = kKT * ROWB;   // bytes of one staged K (or V) tile
-  constexpr int STAGEB = 2 * WK * TILEB;  // K and V tiles of the WK key groups
+  constexpr int TILEB = kKT * ROWB;   // bytes of one K (or V) tile
   constexpr int BLK = kWave * 16;     // bytes one wave writes per direct load
-  constexpr int LPW = STAGEB / BLK / NW;  // direct loads per wave per stage
-  constexpr int XBYTES = 4 * QB * NDB * 16 * 64 * 4;  // key-group exchange of O
-  constexpr int SBYTES = (WK > 1 && XBYTES > 2 * STAGEB) ? XBYTES : 2 * STAGEB;
-  static_assert(STAGEB % (BLK * NW) == 0, "stage must split evenly over the waves");
-  static_assert(LPW <= 8, "direct loads per wave");
-  __shared__ __attribute__((aligned(16))) unsigned char s_raw[SBYTES];
+  constexpr int LPH = TILEB / BLK / NW;  // direct loads per wave per tile
+  constexpr int RB = BLK / ROWB;      // key rows per direct load
+  constexpr int STEP = kKT;           // keys per stage
+  static_assert(TILEB % (BLK * NW) == 0 && LPH >= 1 && 7 * LPH <= 63, "direct loads per wave");
+  static_assert(BLK % ROWB == 0, "a direct load covers whole rows");
+  static_assert(NT >= TAPS_MAX_BUDGET, "one parent pointer per thread");
+  // separate LDS objects, and every access names its buffer statically: the compiler can
+  // then tell that reads of one buffer do not overlap the loads in flight into another
+  __shared__ __attribute__((aligned(16))) unsigned char s_k0[TILEB];
+  __shared__ __attribute__((aligned(16))) unsigned char s_k1[TILEB];
+  __shared__ __attribute__((aligned(16))) unsigned char s_k2[TILEB];
+  __shared__ __attribute__((aligned(16))) unsigned char s_k3[TILEB];
+  __shared__ __attribute__((aligned(16))) unsigned char s_v0[TILEB];
+  __shared__ __attribute__((aligned(16))) unsigned char s_v1[TILEB];
+  __shared__ __attribute__((aligned(16))) unsigned char s_v2[TILEB];
+  __shared__ __attribute__((aligned(16))) unsigned char s_v3[TILEB];
   __shared__ uint64_t s_anc[TAPS_MAX_BUDGET][4];
   __shared__ int s_par[TAPS_MAX_BUDGET];
-  __shared__ float2 s_ml[WK > 1 ? 4 * QB * 64 : 1];
 
   // ---- which (request, KV head, split, row tile) this workgroup owns
   const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
@@ -138,7 +169,7 @@ __global__ __launch_bounds__(256 * WK) void attn_bf16_kernel(
   const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
   const int G = Hq / Hkv;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int rg = wave & 3, kg = wave >> 2;
+  const int rg = wave;
   const int l32 = lane & 31, hl = lane >> 5;
 
   const int ctx = min(max(ctxp[b], 0), max_ctx);
@@ -150,56 +181,68 @@ __global__ __launch_bounds__(256 * WK) void attn_bf16_kernel(
   if (k_begin >= k_end || row0 >= n * G) return;
   const int64_t kv0 = offp[b];
   const size_t row_stride = (size_t)Hkv * HD;  // elements between consecutive cache rows
-  const uint16_t* kbase = Kc + (size_t)kv0 * row_stride + (size_t)g * HD;
-  const uint16_t* vbase = Vc + (size_t)kv0 * row_stride + (size_t)g * HD;
+  const uint32_t rsb = (uint32_t)(row_stride * 2);   // bytes between consecutive cache rows
+  const int nst = (k_end - k_begin + STEP - 1) / STEP;   // stages of this split (>= 1)
+  // buffer resources over this split's K and V rows of head g (the host keeps
+  // (split_len + 5 * STEP) * rsb below 2^31)
+  const size_t seg = ((size_t)kv0 + k_begin) * row_stride + (size_t)g * HD;
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(Kc + seg), (short)0, (int)((uint32_t)(k_end - k_begin) * rsb), 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(Vc + seg), (short)0, (int)((uint32_t)(k_end - k_begin) * rsb), 0x00020000);
 
-  // ---- per-lane pieces of the direct loads: block j of this wave covers 4 key rows
-  int ld_row[LPW], ld_off[LPW];   // row within the stage's tile, element offset in the row
+  // ---- direct loads.  Wave w fills blocks w*LPH .. w*LPH + LPH - 1 of a tile; a block is
+  // RB whole key rows.  The wave index is made explicitly uniform so that the LDS
+  // destinations stay scalar.
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  uint32_t ld_off[LPH];    // byte offset of this lane's piece from the stage's first row
 #pragma unroll
-  for (int j = 0; j < LPW; ++j) {
-    const int byte = (wave * LPW + j) * BLK + lane * 16;
-    const int within = byte % (WK * TILEB);
-    const int t = within / TILEB;
-    const int rb = within - t * TILEB;
+  for (int j = 0; j < LPH; ++j) {
+    const int rb = (wave_u * LPH + j) * BLK + lane * 16;   // byte within the tile
     const int kr = rb / ROWB;
     const int pc = (rb - kr * ROWB) / 16;
-    ld_row[j] = t * kKT + kr;
-    ld_off[j] = (pc ^ kswz(kr)) * 8;
+    ld_off[j] = (uint32_t)kr * rsb + (uint32_t)((pc ^ kswz(kr)) * 16);
   }
-  auto issue_stage = [&](int stage, int base) {
-    unsigned char* sb = s_raw + stage * STAGEB;
-    const bool full = base + kKT * WK <= k_end;
+  // stage s of K (or V) into buffer buf; rows past the split's end arrive as zeros
+  auto issue = [&](__amdgpu_buffer_rsrc_t rs, unsigned char* buf, int s) __attribute__((always_inline)) {
+    const uint32_t soff = (uint32_t)(s * STEP) * rsb;
+    unsigned char* dst = buf + wave_u * LPH * BLK;
 #pragma unroll
-    for (int j = 0; j < LPW; ++j) {
-      const int blk = wave * LPW + j;
-      const bool isv = blk * BLK >= WK * TILEB;   // uniform per wave and j
-      int key = base + ld_row[j];
-      if (!full) key = key < k_end ? key : k_begin;   // a real row; masked out later
-      const uint16_t* src = (isv ? vbase : kbase) + (size_t)key * row_stride + ld_off[j];
-      __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(sb + blk * BLK), 16, 0, 0);
-    }
+    for (int j = 0; j < LPH; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + j * BLK), 16, ld_off[j],
+                                               soff, 0, 0);
   };
-  constexpr int STEP = kKT * WK;
-  issue_stage(0, k_begin);   // the first tiles load while the queries and masks are set up
 
   // ---- queries of this lane (B operand of S^T = K Q^T)
-  bf16x8 q[QB][NKK];
-  int qnode[QB];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    int qr = row0 + rg * 32 * QB + qb * 32 + l32;
+  bf16x8 q[NKK];
+  int qnode;
+  {
+    int qr = row0 + rg * 32 + l32;
     qr = min(qr, N * G - 1);
     const int node = qr / G, hq = g * G + (qr - node * G);
-    qnode[qb] = node;
+    qnode = node;
     const uint16_t* qp = Q + (((size_t)b * N + node) * Hq + hq) * HD;
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) q[qb][kk] = *(const bf16x8*)(qp + kk * 16 + hl * 8);
+    for (int kk = 0; kk < NKK; ++kk) q[kk] = *(const bf16x8*)(qp + kk * 16 + hl * 8);
   }
+  // parent pointers for the ancestor masks (at most one per thread: budget <= NT)
+  const bool tree_split = k_end > ctx;
+  const int my_par = tree_split && tid < n ? parentp[(size_t)b * N + tid] : -1;
+  // the first stages load while the masks are set up; the queries and parents were
+  // issued first, so waiting for them leaves these loads in flight.  The order K(0),
+  // [V(0) K(1)], [V(1) K(2)], [V(2) K(3)] matches the steps' [V(i+3) K(i+4)].
+  issue(krs, s_k0, 0);
+  issue(vrs, s_v0, 0);
+  issue(krs, s_k1, 1);
+  issue(vrs, s_v1, 1);
+  issue(krs, s_k2, 2);
+  issue(vrs, s_v2, 2);
+  issue(krs, s_k3, 3);
+  TAPS_WAIT_VMCNT(7 * LPH);
 
-  // ---- ancestor masks, only when this split reaches the tree rows
-  uint64_t anc[QB][4];
-  if (k_end > ctx) {
-    for (int i = tid; i < n; i += NT) s_par[i] = parentp[(size_t)b * N + i];
+  // ---- ancestor-or-self masks of the tree rows, in LDS (read only by masked tiles)
+  if (tree_split) {
+    if (tid < n) s_par[tid] = my_par;
     __syncthreads();
     for (int i = tid; i < n; i += NT) {
       uint64_t a[4];
@@ -208,15 +251,6 @@ __global__ __launch_bounds__(256 * WK) void attn_bf16_kernel(
       for (int w = 0; w < 4; ++w) s_anc[i][w] = a[w];
     }
     __syncthreads();
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-      for (int w = 0; w < 4; ++w) anc[qb][w] = qnode[qb] < n ? s_anc[qnode[qb]][w] : 0ull;
-  } else {
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-      for (int w = 0; w < 4; ++w) anc[qb][w] = 0ull;
   }
 
   // ---- per-lane LDS read offsets (constant over iterations)
@@ -234,171 +268,155 @@ __global__ __launch_bounds__(256 * WK) void attn_bf16_kernel(
     voff[j] = (4 * hl + tq) * ROWB + 8 * (qq & 1) + 16 * ((g16 * 2 + (qq >> 1)) ^ (fv & 3)) +
               64 * (j ^ (fv >> 2));
 
-  f32x16 o[NDB][QB];
+  // S^T of 32-key block kb of the tile in K buffer kbuf, one k-step
+  auto s_mfma = [&](const unsigned char* kbuf, int kb, int kk, f32x16 (&s)[2])
+      __attribute__((always_inline)) {
+    const bf16x8 a = *(const bf16x8*)(kbuf + kb * 32 * ROWB + 32 * (kk & ~3) + koff[kk & 3]);
+    if (kk == 0) {
+      f32x16 z;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) z[v] = 0.f;
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, q[kk], z, 0, 0, 0);
+    } else {
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, q[kk], s[kb], 0, 0, 0);
+    }
+  };
+
+  f32x16 o[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) o[db][qb][v] = 0.f;
-  float m_ref[QB], l_run[QB];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) { m_ref[qb] = -INFINITY; l_run[qb] = 0.f; }
+    for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
+  float m_ref = -INFINITY, l_run = 0.f;
 
-  int stage = 0;
-  for (int base = k_begin; base < k_end; base += STEP, stage ^= 1) {
-    const bool more = base + STEP < k_end;
-    if (more) {
-      issue_stage(stage ^ 1, base + STEP);
-      TAPS_WAIT_VMCNT(LPW);          // this stage's loads are done, the next may fly
-    } else {
-      TAPS_WAIT_VMCNT(0);
+  // Softmax of S(i) (keys base ...) and O^T += V(i)^T P(i)^T from V buffer vbuf, with
+  // the MFMAs of S(i+1) from K buffer knext interleaved
+  auto softmax_pv = [&](f32x16 (&sc)[2], const unsigned char* vbuf, const unsigned char* knext,
+                        f32x16 (&sn)[2], int base) __attribute__((always_inline)) {
+    // ---- mask (only tiles that reach the tree rows or the split end)
+    const bool need_mask = base + kKT > ctx || base + kKT > k_end;
+    if (need_mask) {
+      uint64_t anc[4] = {0ull, 0ull, 0ull, 0ull};
+      if (base + kKT > ctx && qnode < n) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) anc[w] = s_anc[qnode][w];
+      }
+      uint64_t A = (low_bits(ctx - base) | mask_window(anc, base - ctx)) & low_bits(k_end - base);
+      A >>= 4 * hl;   // this lane's keys are kb*32 + 8*(v/4) + 4*hl + v%4
+      const uint32_t mlo = (uint32_t)A, mhi = (uint32_t)(A >> 32);
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const uint32_t word = kb ? mhi : mlo;
+          const bool ok = (word >> (8 * (v >> 2) + (v & 3))) & 1u;
+          sc[kb][v] = ok ? sc[kb][v] : -INFINITY;
+        }
     }
-    __builtin_amdgcn_s_barrier();
-    const int k0 = base + kg * kKT;
-    if (k0 < k_end) {
-      const unsigned char* tk = s_raw + stage * STAGEB + kg * TILEB;
-      const unsigned char* tv = s_raw + stage * STAGEB + WK * TILEB + kg * TILEB;
-      // ---- S^T = K Q^T for the two 32-key blocks
-      f32x16 s[2][QB];
+    // ---- first key block of S(i+1) while the row maximum of S(i) is found
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+    for (int kk = 0; kk < NKK; ++kk) s_mfma(knext, 0, kk, sn);
+    float mx = -INFINITY;
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int v = 0; v < 16; ++v) s[kb][qb][v] = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) {
-          const bf16x8 a = *(const bf16x8*)(tk + kb * 32 * ROWB + 32 * (kk & ~3) + koff[kk & 3]);
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb)
-            s[kb][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, q[qb][kk], s[kb][qb], 0, 0, 0);
-        }
-      }
-      // ---- mask (only tiles that reach the tree rows or the split end), online softmax
-      const bool need_mask = k0 + kKT > ctx || k0 + kKT > k_end;
-      float nrefv[QB];
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        if (need_mask) {
-          uint64_t A = (low_bits(ctx - k0) | mask_window(anc[qb], k0 - ctx)) & low_bits(k_end - k0);
-          A >>= 4 * hl;   // this lane's keys are kb*32 + 8*(v/4) + 4*hl + v%4
-          const uint32_t mlo = (uint32_t)A, mhi = (uint32_t)(A >> 32);
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-              const uint32_t word = kb ? mhi : mlo;
-              const bool ok = (word >> (8 * (v >> 2) + (v & 3))) & 1u;
-              s[kb][qb][v] = ok ? s[kb][qb][v] : -INFINITY;
-            }
-        }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kb][qb][v]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;   // scale > 0
-        // move the reference max only when it is exceeded by more than 2^8
-        const bool upd = mx > m_ref[qb] + 8.f;
-        if (__ballot(upd)) {
-          const float nref = upd ? mx : m_ref[qb];
-          const float alpha = upd ? __builtin_amdgcn_exp2f(m_ref[qb] - nref) : 1.f;
-          l_run[qb] *= alpha;
-#pragma unroll
-          for (int db = 0; db < NDB; ++db)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) o[db][qb][v] *= alpha;
-          m_ref[qb] = nref;
-        }
-        nrefv[qb] = m_ref[qb] == -INFINITY ? 0.f : -m_ref[qb];
-      }
-      // ---- P = exp2(scale*s - ref) and O^T += V^T P^T in four groups of 8 keys per lane
-      // half: the exponentials of one group are independent of the MFMAs of the previous
-      // group, so the two overlap.  V^T operands come from transposing reads of the
-      // row-major V tile.
-#pragma unroll
-      for (int grp = 0; grp < 4; ++grp) {
-        const int kb = grp >> 1, hf = grp & 1;
-        bf16x8 pg[QB];
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-          float sum = 0.f;
-#pragma unroll
-          for (int t = 0; t < 8; ++t) {
-            const float e = __builtin_amdgcn_exp2f(fmaf(s[kb][qb][hf * 8 + t], scale_log2, nrefv[qb]));
-            sum += e;
-            pg[qb][t] = (__bf16)e;
-          }
-          l_run[qb] += sum;
-        }
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const unsigned char* va = tv + (kb * 32 + 16 * hf) * ROWB + voff[db & 1] + 64 * (db & ~1);
-          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)va);
-          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(va + 8 * ROWB));
-          const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb)
-            o[db][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pg[qb], o[db][qb], 0, 0, 0);
-        }
-      }
-    }
-    __builtin_amdgcn_s_barrier();    // the stage is free for the loads issued next iteration
-  }
-
-  float lsum[QB];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) lsum[qb] = l_run[qb] + __shfl_xor(l_run[qb], 32);
-
-  // ---- merge the key groups through LDS (the stage buffers are free now)
-  if (WK > 1) {
-    float* xo = (float*)s_raw;
-    if (kg == 1) {
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-#pragma unroll
-          for (int v = 0; v < 16; ++v)
-            xo[(((rg * QB + qb) * NDB + db) * 16 + v) * 64 + lane] = o[db][qb][v];
-        s_ml[(rg * QB + qb) * 64 + lane] = make_float2(m_ref[qb], lsum[qb]);
-      }
-    }
-    __syncthreads();
-    if (kg != 0) return;
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      const float2 ml = s_ml[(rg * QB + qb) * 64 + lane];
-      const float M = fmaxf(m_ref[qb], ml.x);
-      const float a0 = m_ref[qb] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref[qb] - M);
-      const float a1 = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - M);
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[kb][v]);
+    mx = fmaxf(mx, other_half(mx)) * scale_log2;   // scale > 0
+    // move the reference max only when it is exceeded by more than 2^8
+    const bool upd = mx > m_ref + 8.f;
+    if (__ballot(upd)) {
+      const float nref = upd ? mx : m_ref;
+      const float alpha = upd ? __builtin_amdgcn_exp2f(m_ref - nref) : 1.f;
+      l_run *= alpha;
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-          o[db][qb][v] = o[db][qb][v] * a0 + xo[(((rg * QB + qb) * NDB + db) * 16 + v) * 64 + lane] * a1;
-      lsum[qb] = lsum[qb] * a0 + ml.y * a1;
-      m_ref[qb] = M;
+        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+      m_ref = nref;
     }
+    const float nref = m_ref == -INFINITY ? 0.f : -m_ref;
+    // ---- P = exp2(scale*s - ref) and O^T += V^T P^T in four groups of 8 keys per lane
+    // half; the second key block of S(i+1) goes into groups 2 and 3, after the first key
+    // block of S(i) is dead
+#pragma unroll
+    for (int grp = 0; grp < 4; ++grp) {
+      const int kb = grp >> 1, hf = grp & 1;
+      bf16x8 pg;
+      float sum = 0.f;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const float e = __builtin_amdgcn_exp2f(fmaf(sc[kb][hf * 8 + t], scale_log2, nref));
+        sum += e;
+        pg[t] = (__bf16)e;
+      }
+      l_run += sum;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const unsigned char* va = vbuf + voff[db & 1] + ((kb * 32 + 16 * hf) * ROWB + 64 * (db & ~1));
+        const unsigned char* vb = vbuf + voff[db & 1] + ((kb * 32 + 16 * hf + 8) * ROWB + 64 * (db & ~1));
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)va);
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)vb);
+        const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pg, o[db], 0, 0, 0);
+      }
+      if (grp >= 2) {
+#pragma unroll
+        for (int kk = (grp - 2) * (NKK / 2); kk < (grp - 1) * (NKK / 2); ++kk) s_mfma(knext, 1, kk, sn);
+      }
+    }
+  };
+
+  // step i: V(i+3) and K(i+4) start loading, then the softmax and P V of stage i run
+  // together with S(i+1).  Buffers: K(i+4) replaces K(i), V(i+3) replaces V(i-1).
+  auto step = [&](f32x16 (&sc)[2], f32x16 (&sn)[2], unsigned char* k_free,
+                  const unsigned char* k_next, const unsigned char* v_cur, unsigned char* v_free,
+                  int i) __attribute__((always_inline)) {
+    issue(vrs, v_free, i + 3);
+    issue(krs, k_free, i + 4);
+    TAPS_WAIT_VMCNT(6 * LPH);         // V(i) and K(i+1) have landed (this wave's part)
+    TAPS_STAGE_BARRIER();             // ... and every other wave's part
+    softmax_pv(sc, v_cur, k_next, sn, k_begin + i * STEP);
+    TAPS_STAGE_BARRIER();             // the buffers of K(i+1) and V(i) may be refilled
+  };
+
+  // ---- S(0), then the steps, unrolled by four so that every access names its buffer
+  f32x16 sA[2], sB[2];
+  TAPS_WAIT_VMCNT(6 * LPH);           // K(0)
+  TAPS_STAGE_BARRIER();
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) s_mfma(s_k0, kb, kk, sA);
+  for (int i = 0;;) {
+    step(sA, sB, s_k0, s_k1, s_v0, s_v3, i);
+    if (++i >= nst) break;
+    step(sB, sA, s_k1, s_k2, s_v1, s_v0, i);
+    if (++i >= nst) break;
+    step(sA, sB, s_k2, s_k3, s_v2, s_v1, i);
+    if (++i >= nst) break;
+    step(sB, sA, s_k3, s_k0, s_v3, s_v2, i);
+    if (++i >= nst) break;
   }
+  // the look-ahead loads past the split's end read nothing from memory; let them land
+  // before the workgroup's LDS is released
+  TAPS_WAIT_VMCNT(0);
+
+  const float lsum = l_run + other_half(l_run);
 
   // ---- write this split's unnormalised partial output, reference max and sum
   const size_t obase = ((size_t)bg * splits + split) * mrows_pad;
+  const int qr = row0 + rg * 32 + l32;
+  float* op = wsO + (obase + qr) * HD;
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int qr = row0 + rg * 32 * QB + qb * 32 + l32;
-    float* op = wsO + (obase + qr) * HD;
+  for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int d = db * 32 + 8 * r4 + 4 * hl;
-        *(float4*)(op + d) = make_float4(o[db][qb][4 * r4], o[db][qb][4 * r4 + 1],
-                                         o[db][qb][4 * r4 + 2], o[db][qb][4 * r4 + 3]);
-      }
-    if (hl == 0) wsML[obase + qr] = make_float2(m_ref[qb], lsum[qb]);
-  }
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int d = db * 32 + 8 * r4 + 4 * hl;
+      *(float4*)(op + d) = make_float4(o[db][4 * r4], o[db][4 * r4 + 1], o[db][4 * r4 + 2],
+                                       o[db][4 * r4 + 3]);
+    }
+  if (hl == 0) wsML[obase + qr] = make_float2(m_ref, lsum);
+#endif
 }
 
 template <int HD>
@@ -420,34 +438,35 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
   const int qr = i * G + (hq - g * G);
   const int nspl = (R + split_len - 1) / split_len;
   const size_t base = (size_t)(b * Hkv + g) * splits;
-  // loads are issued eight splits at a time so their latencies overlap
-  float M = -INFINITY;
-  for (int s0 = 0; s0 < nspl; s0 += 8) {
-    float mv[8];
-#pragma unroll
-    for (int t = 0; t < 8; ++t)
-      mv[t] = s0 + t < nspl ? wsML[(base + s0 + t) * mrows_pad + qr].x : -INFINITY;
-#pragma unroll
-    for (int t = 0; t < 8; ++t) M = fmaxf(M, mv[t]);
-  }
-  float L = 0.f;
+  // one pass: the loads of up to 16 splits are issued together, then merged with a
+  // running maximum (the partial maxima are in base-2 units)
+  constexpr int CH = 16;
+  float M = -INFINITY, L = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s0 = 0; s0 < nspl; s0 += 8) {
-    float2 ml[8];
-    float4 ov[8];
+  for (int s0 = 0; s0 < nspl; s0 += CH) {
+    float2 ml[CH];
+    float4 ov[CH];
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
+    for (int t = 0; t < CH; ++t) {
       const bool ok = s0 + t < nspl;
-      ml[t] = ok ? wsML[(base + s0 + t) * mrows_pad + qr] : make_float2(-INFINITY, 0.f);
-      ov[t] = ok ? *(const float4*)(wsO + ((base + s0 + t) * mrows_pad + qr) * HD + d)
-                 : make_float4(0.f, 0.f, 0.f, 0.f);
+      const size_t r = (base + s0 + t) * mrows_pad + qr;
+      ml[t] = ok ? wsML[r] : make_float2(-INFINITY, 0.f);
+      ov[t] = ok ? *(const float4*)(wsO + r * HD + d) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
+    float Mc = M;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const float w = ml[t].x == -INFINITY ? 0.f : exp2f(ml[t].x - M);
+    for (int t = 0; t < CH; ++t) Mc = fmaxf(Mc, ml[t].x);
+    if (Mc == -INFINITY) continue;
+    const float a = M == -INFINITY ? 0.f : exp2f(M - Mc);
+    L *= a;
+    acc.x *= a; acc.y *= a; acc.z *= a; acc.w *= a;
+#pragma unroll
+    for (int t = 0; t < CH; ++t) {
+      const float w = ml[t].x == -INFINITY ? 0.f : exp2f(ml[t].x - Mc);
       L += w * ml[t].y;
       acc.x += w * ov[t].x; acc.y += w * ov[t].y; acc.z += w * ov[t].z; acc.w += w * ov[t].w;
     }
+    M = Mc;
   }
   const float inv = 1.f / L;
   __bf16 r0 = (__bf16)(acc.x * inv), r1 = (__bf16)(acc.y * inv), r2 = (__bf16)(acc.z * inv),
@@ -547,31 +566,24 @@ AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max
   AttnPlan p;
   const int G = Hq / Hkv;
   const int mrows = budget * G;
-  // two waves per SIMD (32 query rows each, two key groups) by default; TAPS_ATTN_PLAN=
-  // "qb,wk" selects another instantiation (qb in {1,2}, wk in {1,2}) for tuning
   p.qb = 1;
-  p.wk = 2;
-  if (const char* e = getenv("TAPS_ATTN_PLAN")) {
-    int qb = 0, wk = 0;
-    if (sscanf(e, "%d,%d", &qb, &wk) == 2 && (qb == 1 || qb == 2) && (wk == 1 || wk == 2) &&
-        !(qb == 2 && wk == 2)) {
-      p.qb = qb;
-      p.wk = wk;
-    }
-  }
-  p.mtile = 4 * 32 * p.qb;
+  p.wk = 1;
+  p.mtile = 4 * 32;
   p.mtiles = (mrows + p.mtile - 1) / p.mtile;
-  // split the keys so that about 256 workgroups run, each with >= 2 iterations
+  // split the keys so that about 256 workgroups run, each with >= 2 stages
   const int keys = max_ctx + budget;
-  const int step = kKT * p.wk;
+  const int step = kKT;
   const long long base = (long long)batch * Hkv * p.mtiles;
   const int splits = (int)((256 + base - 1) / base);
   int len = (keys + splits - 1) / splits;
   len = ((len + step - 1) / step) * step;
   if (len < 2 * step) len = 2 * step;
+  // the buffer ranges of a split, look-ahead included, stay below 2^31 bytes
+  const long long rsb = (long long)Hkv * head_dim * 2;
+  const long long cap = (((1ll << 31) - 1) / rsb - 5 * step) / step * step;
+  if (len > cap) len = (int)cap;
   p.split_len = len;
   p.splits = (keys + len - 1) / len;
-  (void)head_dim;
   return p;
 }
 
@@ -593,25 +605,18 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
   float2* wsML = (float2*)((char*)ws + rows * head_dim * sizeof(float));
   const int pairs = pl.splits * batch * Hkv;
   dim3 grid((unsigned)(8 * pl.mtiles * ((pairs + 7) / 8)));
-  dim3 block((unsigned)(256 * pl.wk));
+  dim3 block(256u);
   const float sl2 = scale * kLog2e;
   const uint16_t *q = (const uint16_t*)Q, *k = (const uint16_t*)K, *v = (const uint16_t*)V;
   if (ev_begin && hipEventRecord(ev_begin, s) != hipSuccess) return hipErrorInvalidValue;
-#define TAPS_ATT(QB, WK, HD)                                                                  \
-  attn_bf16_kernel<QB, WK, HD><<<grid, block, 0, s>>>(q, k, v, off, ctx, parent, n, budget,   \
-                                                      Hq, Hkv, max_ctx, sl2, pl.split_len,    \
-                                                      pl.splits, pl.mtiles, pairs, mrows_pad, \
-                                                      wsO, wsML)
-  if (head_dim == 128) {
-    if (pl.qb == 2) TAPS_ATT(2, 1, 128);
-    else if (pl.wk == 2) TAPS_ATT(1, 2, 128);
-    else TAPS_ATT(1, 1, 128);
-  } else {
-    if (pl.qb == 2) TAPS_ATT(2, 1, 64);
-    else if (pl.wk == 2) TAPS_ATT(1, 2, 64);
-    else TAPS_ATT(1, 1, 64);
-  }
-#undef TAPS_ATT
+  if (head_dim == 128)
+    attn_bf16_kernel<128><<<grid, block, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv,
+                                                 max_ctx, sl2, pl.split_len, pl.splits,
+                                                 pl.mtiles, pairs, mrows_pad, wsO, wsML);
+  else
+    attn_bf16_kernel<64><<<grid, block, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv,
+                                                max_ctx, sl2, pl.split_len, pl.splits,
+                                                pl.mtiles, pairs, mrows_pad, wsO, wsML);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (ev_end && hipEventRecord(ev_end, s) != hipSuccess) return hipErrorInvalidValue;
