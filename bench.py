@@ -4,7 +4,8 @@
 
 A step is one whole round over one batch: taps_select (vocab top-K, Eq. 1-3,
 Alg. 1), tree_verify_attn and accept_walk, launched on one stream.  Inputs are
-seeded synthetic rounds from ``workloads`` (see the design doc for the recipe), held in
+seeded synthetic rounds from ``workloads`` (Gaussian drafter logits with planted
+spikes, random bf16 Q/K/V, fixed acceptance probability per request), held in
 HBM before timing; several independent input sets rotate so that the 256 MB
 Infinity Cache cannot hold the working set.  Rounds are replayed from one HIP
 graph per input set (``--eager`` launches them directly).
@@ -32,6 +33,8 @@ METRIC = ("verification rounds/sec (select+tree-attn+accept) and achieved HBM GB
           "Qwen3-8B shape")
 HBM_PEAK_GBS = 8000.0
 MALL_BYTES = 256 << 20
+ATTN_SRC = os.path.join(ROOT, "paper_2606_00487_amd", "csrc", "attn.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_bf16_kernel_qwen3_8b_hbm.txt")
 
 
 def parse():
@@ -60,6 +63,27 @@ def copy_calibration():
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 3}), flush=True)
+
+
+def measured_traffic(cfg_name):
+    """HBM bytes per launch of the main attention kernel from the committed counter
+    summary (FETCH_SIZE and WRITE_SIZE per dispatch, each scaled by what the counter reads
+    for a plain copy of known size), or None when the summary does not cover this
+    workload or the kernel source has changed since the counters were taken."""
+    import hashlib
+    if cfg_name != "qwen3_8b" or not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        line = line.strip()
+        if "=" in line and not line.startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()
+    if kv.get("attn_source_sha256") != sha:
+        return None
+    return int(float(kv["fetch_kib_per_launch"]) * 1024 * float(kv["fetch_scale"]) +
+               float(kv["write_kib_per_launch"]) * 1024 * float(kv["write_scale"]))
 
 
 def algorithmic_bytes(cfg, ctx_len, n_nodes):
@@ -241,7 +265,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(cfg.name),
             "bytes_per_launch": int(attn_bytes),
             "avg_launch_us": round(t_attn, 3),
         },

@@ -70,8 +70,9 @@ typedef struct {
   double lambda1, lambda2, tau, beta;
 } taps_select_params;
 
-/* Selected subtree S per request, in selection order (a parent always precedes its
- * children).  Arrays are [batch][budget] unless noted; slots n..budget-1 hold
+/* Selected subtree S per request, breadth first: nodes ordered by depth, then by rank
+ * path (the ranks of the tokens from the root down), so a parent always precedes its
+ * children.  Arrays are [batch][budget] unless noted; slots n..budget-1 hold
  * parent = token = depth = rank = -1 and q_reach = 0.
  *   parent    index of the parent node within the request; -1 at the root (index 0)
  *   token     vocabulary id; -1 at the root
@@ -148,9 +149,11 @@ taps_status tree_verify_attn(const void *Q_tree, const void *K_cache, const void
                              int32_t head_dim, int32_t max_ctx, int32_t dtype, float scale,
                              void *O, void *ws, size_t ws_bytes, hipStream_t stream);
 
-/* tree_verify_attn that also records `ev_begin` on `stream` right before its main attention
- * kernel and `ev_end` right after it (before the split combine), so a caller can time that
- * kernel alone with hipEventElapsedTime.  Either event may be NULL.  For profiling callers. */
+/* tree_verify_attn that also times its main attention kernel: `ev_begin` and `ev_end` are
+ * set to the start and the end of that kernel's execution (hipExtLaunchKernel events; the
+ * split combine that follows is not included), so hipEventElapsedTime gives the kernel's
+ * own duration.  Either event may be NULL; both must have been created.  For profiling
+ * callers. */
 taps_status tree_verify_attn_timed(const void *Q_tree, const void *K_cache, const void *V_cache,
                                    const int64_t *kv_offset, const int32_t *ctx_len,
                                    const int32_t *tree_parent, const int32_t *n_nodes,

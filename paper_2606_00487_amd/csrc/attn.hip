@@ -21,6 +21,8 @@
 #include <cstdlib>
 #include <type_traits>
 
+#include <hip/hip_ext.h>
+
 #include "common.h"
 
 namespace taps {
@@ -608,18 +610,28 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
   dim3 block(256u);
   const float sl2 = scale * kLog2e;
   const uint16_t *q = (const uint16_t*)Q, *k = (const uint16_t*)K, *v = (const uint16_t*)V;
-  if (ev_begin && hipEventRecord(ev_begin, s) != hipSuccess) return hipErrorInvalidValue;
-  if (head_dim == 128)
-    attn_bf16_kernel<128><<<grid, block, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv,
-                                                 max_ctx, sl2, pl.split_len, pl.splits,
-                                                 pl.mtiles, pairs, mrows_pad, wsO, wsML);
-  else
-    attn_bf16_kernel<64><<<grid, block, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv,
-                                                max_ctx, sl2, pl.split_len, pl.splits,
-                                                pl.mtiles, pairs, mrows_pad, wsO, wsML);
+  // with events, the launch records the kernel's own start and end (hipExtLaunchKernel)
+  if (head_dim == 128) {
+    if (ev_begin || ev_end)
+      hipExtLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, s, ev_begin, ev_end, 0, q, k,
+                            v, off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2, pl.split_len,
+                            pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML);
+    else
+      attn_bf16_kernel<128><<<grid, block, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv,
+                                                   max_ctx, sl2, pl.split_len, pl.splits,
+                                                   pl.mtiles, pairs, mrows_pad, wsO, wsML);
+  } else {
+    if (ev_begin || ev_end)
+      hipExtLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, s, ev_begin, ev_end, 0, q, k,
+                            v, off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2, pl.split_len,
+                            pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML);
+    else
+      attn_bf16_kernel<64><<<grid, block, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv,
+                                                  max_ctx, sl2, pl.split_len, pl.splits,
+                                                  pl.mtiles, pairs, mrows_pad, wsO, wsML);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (ev_end && hipEventRecord(ev_end, s) != hipSuccess) return hipErrorInvalidValue;
   const int rows_out = batch * budget * Hq;
   if (head_dim == 128) {
     const int rpb = kThreads / 32;
@@ -642,15 +654,13 @@ hipError_t launch_attn_f32(const float* Q, const float* K, const float* V, const
                            hipEvent_t ev_end) {
   if (batch <= 0) return hipSuccess;
   dim3 grid((unsigned)budget, (unsigned)Hq, (unsigned)batch), block(kThreads);
-  if (ev_begin && hipEventRecord(ev_begin, s) != hipSuccess) return hipErrorInvalidValue;
   if (head_dim == 128)
-    attn_f32_kernel<128><<<grid, block, 0, s>>>(Q, K, V, off, ctx, parent, n, budget, Hq, Hkv, max_ctx, scale, O);
+    hipExtLaunchKernelGGL(attn_f32_kernel<128>, grid, block, 0, s, ev_begin, ev_end, 0, Q, K, V,
+                          off, ctx, parent, n, budget, Hq, Hkv, max_ctx, scale, O);
   else
-    attn_f32_kernel<64><<<grid, block, 0, s>>>(Q, K, V, off, ctx, parent, n, budget, Hq, Hkv, max_ctx, scale, O);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if (ev_end && hipEventRecord(ev_end, s) != hipSuccess) return hipErrorInvalidValue;
-  return hipSuccess;
+    hipExtLaunchKernelGGL(attn_f32_kernel<64>, grid, block, 0, s, ev_begin, ev_end, 0, Q, K, V,
+                          off, ctx, parent, n, budget, Hq, Hkv, max_ctx, scale, O);
+  return hipGetLastError();
 }
 
 }  // namespace taps
