@@ -29,7 +29,9 @@ namespace taps {
 
 namespace {
 
-constexpr int kThreads = 1024;
+constexpr int kThreadsA = 1024;                   // Phase A: one wave per marginal row
+constexpr int kWavesA = kThreadsA / kWave;
+constexpr int kThreads = 256;                     // Phases B-D: four waves
 constexpr int kWaves = kThreads / kWave;
 constexpr int kRowCap = TAPS_MAX_K * TAPS_MAX_K;  // entries >= the threshold, at most K*K
 constexpr int kCap = 3072;                        // expanded nodes held in LDS
@@ -65,10 +67,12 @@ __device__ inline int lanes_below(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
+// LDS exchange between the lanes of one wave: a wave's LDS accesses execute in order,
+// so wavefront-scope ordering suffices (no wait for outstanding global loads)
 __device__ inline void wave_fence() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 // exclusive prefix of a small non-negative count (< 2^bits) over the lanes of a wave
@@ -83,6 +87,17 @@ __device__ inline int wave_prefix_small(int v, int& total) {
   }
   total = tot;
   return pre;
+}
+
+// inclusive prefix sum over the lanes of a wave (DPP row shifts, then row broadcasts)
+__device__ inline int wave_inclusive_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return v;
 }
 
 // exclusive prefix over the whole workgroup (values < 2^BITS); s_w holds kWaves ints
@@ -137,8 +152,8 @@ __device__ inline uint32_t wave_min_u32(uint32_t v) {
 
 // ------------------------------------------------------------------ shared memory layout
 struct PhaseA {
-  uint64_t heads[kWaves][64];
-  uint64_t rowc[kWaves][kRowCap];
+  uint64_t heads[kWavesA][64];
+  uint64_t rowc[kWavesA][kRowCap];
 };
 struct Level {                 // expanded trie nodes, stored depth by depth
   double q[kCap];
@@ -314,7 +329,7 @@ __device__ int select_sequential(Shared& sh, int D, int K, int N, double tau) {
 }
 
 template <int SLOTS>
-__global__ __launch_bounds__(kThreads) void select_kernel(
+__global__ __launch_bounds__(kThreadsA) void select_kernel(
     int D, int K, int N, int kind, double lambda1, double lambda2, double tau, double beta,
     int chunks, const uint64_t* __restrict__ cand, int32_t* __restrict__ o_parent,
     int32_t* __restrict__ o_token, int32_t* __restrict__ o_depth, int32_t* __restrict__ o_rank,
@@ -328,15 +343,23 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
   {
     PhaseA& A = sh.x.a;
     const int CK = chunks * K;
-    for (int i = wave; i < D; i += kWaves) {
+    for (int i = wave; i < D; i += kWavesA) {
       const uint64_t* rc = cand + ((size_t)b * D + i) * CK;
+      // loads of clamped (in-bounds) addresses under a wave-uniform count, zeroed
+      // afterwards: the loads issue back to back without per-lane branches
+      const int jmax = (CK + kWave - 1) / kWave;
       uint64_t v[16];
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const int e = j * kWave + lane;
-        v[j] = e < CK ? rc[e] : 0ull;
+        v[j] = 0ull;
+        if (j < jmax) {
+          const uint64_t x = rc[min(e, CK - 1)];
+          v[j] = e < CK ? x : 0ull;
+        }
       }
-      const uint64_t head = lane < chunks ? rc[(size_t)lane * K] : 0ull;
+      const uint64_t hx = rc[(size_t)min(lane, chunks - 1) * K];
+      const uint64_t head = lane < chunks ? hx : 0ull;
       A.heads[wave][lane] = head;
       wave_fence();
       int beat = 0;
@@ -389,10 +412,14 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     }
   }
   __syncthreads();
+  // The selection proper runs on the first four waves.  The other waves end here; a
+  // workgroup barrier waits only for the waves that have not ended, so the barriers
+  // below synchronize the remaining four.
+  if (wave >= kWaves) return;
 
   // ---------------- Phase B: Eq. 1 edge probabilities, Eq. 3 denominators
-  if (tid < D * K) {
-    const int i = tid / K, r = tid - (tid / K) * K;
+  for (int it = tid; it < D * K; it += kThreads) {
+    const int i = it / K, r = it - (it / K) * K;
     const uint64_t k = sh.top[i][r];
     const double x = k ? (double)value_from_key((uint32_t)(k >> 32)) : (double)__uint_as_float(0x7FC00000u);
     double e;
@@ -408,8 +435,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
   if (tid <= D) sh.den[tid] = lambda1 + lambda2 * (double)tid;
   if (tid < kWaves) sh.wsum[tid] = 0;
   __syncthreads();
-  if (tid < D * K) {
-    const int i = tid / K, r = tid - (tid / K) * K;
+  for (int it = tid; it < D * K; it += kThreads) {
+    const int i = it / K, r = it - (it / K) * K;
     double Z = 0.0;
     for (int j = 0; j < K; ++j) Z = Z + sh.e[i][j];
     const bool ok = Z > 0.0 && Z <= 1.7976931348623157e308;
@@ -437,68 +464,78 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     const int items = (p1 - p0) * K;
     if (items == 0) break;
     const int bstar = sh.bstar;
-    const int per = (items + kThreads - 1) / kThreads;  // contiguous items per thread
-    if (per > 4) {                                       // too wide a level: sequential path
-      if (tid == 0) sh.flag = 1;
-      __syncthreads();
-      break;
-    }
-    // evaluate this thread's candidates once: child r of stored node p at depth d
-    double qv[4], uv[4];
-    int mv[4], bv[4];
-    bool okv[4];
-    int cnt = 0;
-    const int it0 = tid * per;
-    int pp = p0 + it0 / K, rr = it0 - (it0 / K) * K;   // (parent, rank) of the first item
+    const double den1 = sh.den[d + 1];
+    // the level's items in chunks of up to 4 per thread, each thread taking contiguous
+    // items so that the stored order stays (parent, rank)
+    int base = sh.total;
+    bool overflow = false;
+    for (int c0 = 0; c0 < items; c0 += 4 * kThreads) {
+      const int citems = min(items - c0, 4 * kThreads);
+      const int per = (citems + kThreads - 1) / kThreads;
+      // evaluate this thread's candidates once: child r of stored node p at depth d
+      double qv[4], uv[4];
+      int mv[4], bv[4];
+      bool okv[4];
+      int cnt = 0;
+      const int it0 = c0 + tid * per;
+      int pp = p0 + it0 / K, rr = it0 - (it0 / K) * K;   // (parent, rank) of the first item
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int it = it0 + k;
-      okv[k] = false;
-      qv[k] = uv[k] = 0.0;
-      mv[k] = bv[k] = 0;
-      const int p = pp, r = rr;
-      if (++rr == K) { rr = 0; ++pp; }
-      if (k < per && it < items) {
-        const uint64_t pu = L.u[p];
-        if (ubin(__longlong_as_double((long long)pu)) >= bstar) {
-          const double q = L.q[p] * sh.c[d][r];
-          const double u = q / sh.den[d + 1];
-          const int bn = ubin(u);
-          okv[k] = u > tau && bn >= bstar;
-          qv[k] = q;
-          uv[k] = u;
-          bv[k] = bn;
-          mv[k] = (p << 16) | ((d + 1) << 8) | r;
+      for (int k = 0; k < 4; ++k) {
+        const int it = it0 + k;
+        okv[k] = false;
+        qv[k] = uv[k] = 0.0;
+        mv[k] = bv[k] = 0;
+        const int p = pp, r = rr;
+        if (++rr == K) { rr = 0; ++pp; }
+        // items beyond this chunk's per-thread count are skipped (a wave-uniform test);
+        // the others are evaluated without branches (clamped parent index), so their loads
+        // and fp64 arithmetic overlap; invalid ones are masked
+        if (k >= per) continue;
+        const int pc = min(p, p1 - 1);
+        const uint64_t pu = L.u[pc];
+        const double qp = L.q[pc], cr = sh.c[d][r];
+        const double q = qp * cr;
+        const double u = q / den1;
+        const int bn = ubin(u);
+        okv[k] = k < per && it < c0 + citems &&
+                 ubin(__longlong_as_double((long long)pu)) >= bstar && u > tau && bn >= bstar;
+        qv[k] = q;
+        uv[k] = u;
+        bv[k] = bn;
+        mv[k] = (p << 16) | ((d + 1) << 8) | r;
+        cnt += okv[k] ? 1 : 0;
+      }
+      int total;
+      const int pre = block_prefix<3>(cnt, sh.wsum, total);
+      if (base + total > kCap) {       // uniform: the expansion outgrows LDS
+        overflow = true;
+        break;
+      }
+      int pos = base + pre;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (okv[k]) {
+          L.q[pos] = qv[k];
+          L.u[pos] = ubits(uv[k]);
+          L.meta[pos] = mv[k];
+          atomicAdd(&L.hist[bv[k]], 1);
+          ++pos;
         }
       }
-      cnt += okv[k] ? 1 : 0;
+      base += total;
     }
-    int total;
-    const int pre = block_prefix<3>(cnt, sh.wsum, total);
-    const int base = sh.total;
-    if (base + total > kCap) {
+    if (overflow) {
       if (tid == 0) sh.flag = 1;
       __syncthreads();
       break;
-    }
-    int pos = base + pre;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      if (okv[k]) {
-        L.q[pos] = qv[k];
-        L.u[pos] = ubits(uv[k]);
-        L.meta[pos] = mv[k];
-        atomicAdd(&L.hist[bv[k]], 1);
-        ++pos;
-      }
     }
     __syncthreads();
     if (tid == 0) {
-      sh.total = base + total;
-      L.lvl_start[d + 2] = base + total;
+      sh.total = base;
+      L.lvl_start[d + 2] = base;
     }
     // new b*: the highest bin whose suffix count reaches N-1 (0 while fewer nodes exist)
-    if (wave == 0) {
+    if (wave == 0 && base >= N - 1) {
       constexpr int BPL = kBins / kWave;  // bins per lane
       int hv[BPL];
 #pragma unroll
@@ -509,9 +546,9 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
       int sl = 0;
 #pragma unroll
       for (int j = 0; j < BPL; ++j) sl += hv[j];
-      int tot_all;
-      const int below = wave_prefix_small<12>(sl, tot_all);
-      const int suffix = tot_all - below;            // nodes in this lane's bins and above
+      const int incl = wave_inclusive_sum(sl);
+      const int tot_all = __shfl(incl, kWave - 1);
+      const int suffix = tot_all - (incl - sl);      // nodes in this lane's bins and above
       const uint64_t ok = __ballot(N > 1 && suffix >= N - 1);
       if (ok != 0ull) {
         const int Ls = 63 - __clzll((long long)ok);
@@ -538,7 +575,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
   if (!fallback) {
     // ---- final cut: keep bins > b*, rank the members of bin b* exactly
     const int tot = sh.total, bstar = sh.bstar;
-    const int per = (tot + kThreads - 1) / kThreads;   // <= 3
+    const int per = (tot + kThreads - 1) / kThreads;   // <= kCap / kThreads = 12
     int above = 0, inb = 0;
     for (int k = 0; k < per; ++k) {
       const int j = tid * per + k;
@@ -549,8 +586,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
       }
     }
     int c_hi, c_b;
-    block_prefix<2>(above, sh.wsum, c_hi);
-    int mpos = block_prefix<2>(inb, sh.wsum, c_b);
+    block_prefix<4>(above, sh.wsum, c_hi);   // per <= kCap / kThreads = 12
+    int mpos = block_prefix<4>(inb, sh.wsum, c_b);
     for (int k = 0; k < per; ++k) {
       const int j = tid * per + k;
       if (j >= 1 && j < tot && ubin(__longlong_as_double((long long)L.u[j])) == bstar)
@@ -649,7 +686,7 @@ double spec_exp_host(double t) { return spec_exp(t); }
 
 hipError_t launch_select(const void* /*marg*/, const taps_select_params& p, const TopkPlan& plan,
                          const uint64_t* cand, const taps_tree& out, hipStream_t s) {
-  dim3 grid((unsigned)p.batch), block(kThreads);
+  dim3 grid((unsigned)p.batch), block(kThreadsA);
   const int slots = (p.budget + kWave - 1) / kWave;
 #define TAPS_SEL(SL)                                                                          \
   select_kernel<SL><<<grid, block, 0, s>>>(p.block, p.K, p.budget, p.kind, p.lambda1,         \
