@@ -80,6 +80,15 @@ __device__ inline uint64_t low_bits(int j) {
   return j <= 0 ? 0ull : (j >= 64 ? ~0ull : ((1ull << j) - 1ull));
 }
 
+// four floats rounded to bf16 (nearest even), packed little-endian
+__device__ inline uint2 pack_bf16x4(float a, float b, float c, float d) {
+  const __bf16 r0 = (__bf16)a, r1 = (__bf16)b, r2 = (__bf16)c, r3 = (__bf16)d;
+  uint2 pk;
+  pk.x = (uint32_t)__builtin_bit_cast(uint16_t, r0) | ((uint32_t)__builtin_bit_cast(uint16_t, r1) << 16);
+  pk.y = (uint32_t)__builtin_bit_cast(uint16_t, r2) | ((uint32_t)__builtin_bit_cast(uint16_t, r3) << 16);
+  return pk;
+}
+
 // the value held by lane l ^ 32 (a VALU lane swap, no LDS round trip)
 __device__ inline float other_half(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
@@ -126,12 +135,12 @@ __device__ inline int kswz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
 // The grid is one-dimensional: the query-row tiles of one (request, KV head, split) get
 // block ids that differ by multiples of 8, so they run on the same XCD and share its L2.
 template <int HD>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(
+__global__ __launch_bounds__(256) void attn_bf16_w4_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc,
     const uint16_t* __restrict__ Vc, const int64_t* __restrict__ offp,
     const int32_t* __restrict__ ctxp, const int32_t* __restrict__ parentp,
     const int32_t* __restrict__ nnp, int N, int Hq, int Hkv, int max_ctx, float scale_log2,
-    int split_len, int splits, int mtiles, int pairs, int mrows_pad, float* __restrict__ wsO,
+    int split_len, int splits, int mtiles, int pairs, int mrows_pad, uint16_t* __restrict__ wsO,
     float2* __restrict__ wsML) {
   // the body uses the buffer-resource type, which exists only in the device pass; the
   // host pass needs no more than the signature to emit the launch stub
@@ -404,26 +413,344 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(
   TAPS_WAIT_VMCNT(0);
 
   const float lsum = l_run + other_half(l_run);
+  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
 
-  // ---- write this split's unnormalised partial output, reference max and sum
+  // ---- write this split's partial: O / sum in bf16, reference max and sum
   const size_t obase = ((size_t)bg * splits + split) * mrows_pad;
   const int qr = row0 + rg * 32 + l32;
-  float* op = wsO + (obase + qr) * HD;
+  uint16_t* op = wsO + (obase + qr) * HD;
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int r4 = 0; r4 < 4; ++r4) {
       const int d = db * 32 + 8 * r4 + 4 * hl;
-      *(float4*)(op + d) = make_float4(o[db][4 * r4], o[db][4 * r4 + 1], o[db][4 * r4 + 2],
-                                       o[db][4 * r4 + 3]);
+      *(uint2*)(op + d) = pack_bf16x4(o[db][4 * r4] * inv, o[db][4 * r4 + 1] * inv,
+                                      o[db][4 * r4 + 2] * inv, o[db][4 * r4 + 3] * inv);
     }
   if (hl == 0) wsML[obase + qr] = make_float2(m_ref, lsum);
 #endif
 }
 
+// Eight waves per workgroup (two per SIMD), in two key groups of four: group g works on
+// the 32-key stages g, g + 2, g + 4, ... of the split, each wave on 32 query rows, and
+// the groups merge their results through LDS at the end.  K and V cycle through rings of
+// eight 32-key slots (sixteen separate LDS objects): step t processes stages 2t and
+// 2t + 1 and issues the loads of V(2t + 6), V(2t + 7), K(2t + 8) and K(2t + 9), so every
+// load has three steps to arrive.  Within a group the pipeline is the same as in the
+// four-wave kernel: the softmax and P V of a stage run together with the MFMAs of S for
+// the group's next stage.  The step loop is written once per group (template) and
+// unrolled by four, so that every LDS access names its slot statically.
+template <int KG>
+struct GroupTag {
+  static constexpr int value = KG;
+};
+
+__global__ __launch_bounds__(512) void attn_bf16_kernel(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc,
+    const uint16_t* __restrict__ Vc, const int64_t* __restrict__ offp,
+    const int32_t* __restrict__ ctxp, const int32_t* __restrict__ parentp,
+    const int32_t* __restrict__ nnp, int N, int Hq, int Hkv, int max_ctx, float scale_log2,
+    int split_len, int splits, int mtiles, int pairs, int mrows_pad, uint16_t* __restrict__ wsO,
+    float2* __restrict__ wsML) {
+  // the body uses the buffer-resource type, which exists only in the device pass; the
+  // host pass needs no more than the signature to emit the launch stub
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int HD = 128;
+  constexpr int NT = 512;
+  constexpr int ROWB = HD * 2;        // bytes per K/V row
+  constexpr int MT = 4 * 32;          // query rows per workgroup
+  constexpr int NDB = HD / 32;        // 32-row blocks of O^T
+  constexpr int NKK = HD / 16;        // MFMA k-steps over head_dim
+  constexpr int KT = 32;              // keys per stage
+  constexpr int TILEB = KT * ROWB;    // 8 KB: one K (or V) slot
+  constexpr int BLK = kWave * 16;     // bytes one wave writes per direct load
+  static_assert(TILEB == 8 * BLK, "one direct load per wave and slot");
+  static_assert(NT >= TAPS_MAX_BUDGET, "one parent pointer per thread");
+  __shared__ __attribute__((aligned(16))) unsigned char s_k0[TILEB], s_k1[TILEB], s_k2[TILEB],
+      s_k3[TILEB], s_k4[TILEB], s_k5[TILEB], s_k6[TILEB], s_k7[TILEB];
+  __shared__ __attribute__((aligned(16))) unsigned char s_v0[TILEB], s_v1[TILEB], s_v2[TILEB],
+      s_v3[TILEB], s_v4[TILEB], s_v5[TILEB], s_v6[TILEB], s_v7[TILEB];
+  __shared__ uint64_t s_anc[TAPS_MAX_BUDGET][4];
+  __shared__ int s_par[TAPS_MAX_BUDGET];
+  __shared__ float2 s_ml[8 * 64];
+
+  // ---- which (request, KV head, split, row tile) this workgroup owns
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int mt = slot % mtiles, pair = (slot / mtiles) * 8 + xcd;
+  if (pair >= pairs) return;
+  const int split = pair % splits, bg = pair / splits;
+  const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
+  const int G = Hq / Hkv;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rg = wave & 3, kg = wave >> 2;
+  const int l32 = lane & 31, hl = lane >> 5;
+
+  const int ctx = min(max(ctxp[b], 0), max_ctx);
+  const int n = min(max(nnp[b], 0), N);
+  const int R = ctx + n;
+  const int k_begin = split * split_len;
+  const int k_end = min(R, k_begin + split_len);
+  const int row0 = mt * MT;
+  if (k_begin >= k_end || row0 >= n * G) return;
+  const int64_t kv0 = offp[b];
+  const size_t row_stride = (size_t)Hkv * HD;
+  const uint32_t rsb = (uint32_t)(row_stride * 2);
+  const int nst = (k_end - k_begin + KT - 1) / KT;   // 32-key stages of this split
+  const int steps = (nst + 1) / 2;                    // each step: one stage per group
+  // buffer resources over this split's K and V rows of head g: rows past the split's end
+  // read as zeros without touching memory (the host keeps the range below 2^31 bytes)
+  const size_t seg = ((size_t)kv0 + k_begin) * row_stride + (size_t)g * HD;
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(Kc + seg), (short)0, (int)((uint32_t)(k_end - k_begin) * rsb), 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(Vc + seg), (short)0, (int)((uint32_t)(k_end - k_begin) * rsb), 0x00020000);
+
+  // ---- direct loads: wave w fills block w (rows 4w .. 4w + 3) of every slot
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  uint32_t ld_off;
+  {
+    const int rb = wave_u * BLK + lane * 16;
+    const int kr = rb / ROWB;
+    const int pc = (rb - kr * ROWB) / 16;
+    ld_off = (uint32_t)kr * rsb + (uint32_t)((pc ^ kswz(kr)) * 16);
+  }
+  auto issue = [&](__amdgpu_buffer_rsrc_t rs, unsigned char* buf, int s) __attribute__((always_inline)) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(buf + wave_u * BLK), 16, ld_off,
+                                             (uint32_t)(s * KT) * rsb, 0, 0);
+  };
+
+  // ---- queries of this lane (B operand of S^T = K Q^T)
+  bf16x8 q[NKK];
+  int qnode;
+  {
+    int qr = row0 + rg * 32 + l32;
+    qr = min(qr, N * G - 1);
+    const int node = qr / G, hq = g * G + (qr - node * G);
+    qnode = node;
+    const uint16_t* qp = Q + (((size_t)b * N + node) * Hq + hq) * HD;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) q[kk] = *(const bf16x8*)(qp + kk * 16 + hl * 8);
+  }
+  const bool tree_split = k_end > ctx;
+  const int my_par = tree_split && tid < n ? parentp[(size_t)b * N + tid] : -1;
+  // K(0) K(1) and the loads of step -3 [V(2t+6) V(2t+7) K(2t+8) K(2t+9)] now; those of
+  // steps -2 and -1 after the first S (so its reads of K(0), K(1) wait for nothing else)
+  issue(krs, s_k0, 0);
+  issue(krs, s_k1, 1);
+  issue(vrs, s_v0, 0); issue(vrs, s_v1, 1); issue(krs, s_k2, 2); issue(krs, s_k3, 3);
+  TAPS_WAIT_VMCNT(6);   // queries and parents
+
+  // ---- ancestor-or-self masks of the tree rows, in LDS (read only by masked tiles)
+  if (tree_split) {
+    if (tid < n) s_par[tid] = my_par;
+    __syncthreads();
+    for (int i = tid; i < n; i += NT) {
+      uint64_t a[4];
+      ancestor_mask(i, [&](int j) { return s_par[j]; }, a);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) s_anc[i][w] = a[w];
+    }
+    __syncthreads();
+  }
+
+  // ---- per-lane LDS read offsets
+  const int fk = kswz(l32);
+  int koff[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) koff[j] = l32 * ROWB + 32 * (j ^ (fk >> 1)) + 16 * (hl ^ (fk & 1));
+  const int g16 = (lane >> 4) & 1, tq = (lane & 15) >> 2, qq = lane & 3;
+  const int fv = kswz(4 * hl + tq);
+  int voff[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+    voff[j] = (4 * hl + tq) * ROWB + 8 * (qq & 1) + 16 * ((g16 * 2 + (qq >> 1)) ^ (fv & 3)) +
+              64 * (j ^ (fv >> 2));
+
+  // S^T of the 32 keys in K slot kbuf, one k-step
+  auto s_mfma = [&](const unsigned char* kbuf, int kk, f32x16& s) __attribute__((always_inline)) {
+    const bf16x8 a = *(const bf16x8*)(kbuf + 32 * (kk & ~3) + koff[kk & 3]);
+    if (kk == 0) {
+      f32x16 z;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) z[v] = 0.f;
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, q[kk], z, 0, 0, 0);
+    } else {
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, q[kk], s, 0, 0, 0);
+    }
+  };
+
+  f32x16 o[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
+  float m_ref = -INFINITY, l_run = 0.f;
+
+  // Softmax of S (keys base .. base + 31) and O^T += V^T P^T from V slot vbuf, with the
+  // MFMAs of the group's next S from K slot knext interleaved
+  auto softmax_pv = [&](f32x16& sc, const unsigned char* vbuf, const unsigned char* knext,
+                        f32x16& sn, int base) __attribute__((always_inline)) {
+    const bool need_mask = base + KT > ctx || base + KT > k_end;
+    if (need_mask) {
+      uint64_t anc[4] = {0ull, 0ull, 0ull, 0ull};
+      if (base + KT > ctx && qnode < n) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) anc[w] = s_anc[qnode][w];
+      }
+      uint64_t A = (low_bits(ctx - base) | mask_window(anc, base - ctx)) & low_bits(k_end - base);
+      const uint32_t word = (uint32_t)(A >> (4 * hl));   // keys 8*(v/4) + 4*hl + v%4
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const bool ok = (word >> (8 * (v >> 2) + (v & 3))) & 1u;
+        sc[v] = ok ? sc[v] : -INFINITY;
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < NKK / 2; ++kk) s_mfma(knext, kk, sn);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[v]);
+    mx = fmaxf(mx, other_half(mx)) * scale_log2;   // scale > 0
+    const bool upd = mx > m_ref + 8.f;                // move the reference by > 2^8 only
+    if (__ballot(upd)) {
+      const float nref = upd ? mx : m_ref;
+      const float alpha = upd ? __builtin_amdgcn_exp2f(m_ref - nref) : 1.f;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+      m_ref = nref;
+    }
+    const float nref = m_ref == -INFINITY ? 0.f : -m_ref;
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      bf16x8 pg;
+      float sum = 0.f;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const float e = __builtin_amdgcn_exp2f(fmaf(sc[hf * 8 + t], scale_log2, nref));
+        sum += e;
+        pg[t] = (__bf16)e;
+      }
+      l_run += sum;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const unsigned char* va = vbuf + voff[db & 1] + ((16 * hf) * ROWB + 64 * (db & ~1));
+        const unsigned char* vb = vbuf + voff[db & 1] + ((16 * hf + 8) * ROWB + 64 * (db & ~1));
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)va);
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)vb);
+        const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pg, o[db], 0, 0, 0);
+      }
+#pragma unroll
+      for (int kk = NKK / 2 + hf * (NKK / 4); kk < NKK / 2 + (hf + 1) * (NKK / 4); ++kk)
+        s_mfma(knext, kk, sn);
+    }
+  };
+
+  // one step for group KG: slots of stage 2t + KG (V) and 2t + 2 + KG (K look-ahead)
+  f32x16 sA, sB;
+  auto run = [&](auto tag) __attribute__((always_inline)) {
+    constexpr int KGc = decltype(tag)::value;
+    unsigned char* const ks[8] = {s_k0, s_k1, s_k2, s_k3, s_k4, s_k5, s_k6, s_k7};
+    unsigned char* const vs[8] = {s_v0, s_v1, s_v2, s_v3, s_v4, s_v5, s_v6, s_v7};
+    auto step = [&](auto pt, f32x16& sc, f32x16& sn, int t) __attribute__((always_inline)) {
+      constexpr int P = decltype(pt)::value;   // t % 4
+      issue(vrs, vs[(2 * P + 6) & 7], 2 * t + 6);
+      issue(vrs, vs[(2 * P + 7) & 7], 2 * t + 7);
+      issue(krs, ks[(2 * P + 8) & 7], 2 * t + 8);
+      issue(krs, ks[(2 * P + 9) & 7], 2 * t + 9);
+      TAPS_WAIT_VMCNT(12);            // V(2t), V(2t+1), K(2t+2), K(2t+3): this wave's part
+      TAPS_STAGE_BARRIER();           // ... and every other wave's part
+      softmax_pv(sc, vs[(2 * P + KGc) & 7], ks[(2 * P + 2 + KGc) & 7], sn,
+                 k_begin + (2 * t + KGc) * KT);
+      TAPS_STAGE_BARRIER();           // these slots may be refilled
+    };
+    TAPS_WAIT_VMCNT(4);               // K(0), K(1)
+    TAPS_STAGE_BARRIER();
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) s_mfma(ks[KGc], kk, sA);
+    issue(vrs, s_v2, 2); issue(vrs, s_v3, 3); issue(krs, s_k4, 4); issue(krs, s_k5, 5);
+    issue(vrs, s_v4, 4); issue(vrs, s_v5, 5); issue(krs, s_k6, 6); issue(krs, s_k7, 7);
+    for (int t = 0;;) {
+      step(GroupTag<0>(), sA, sB, t);
+      if (++t >= steps) break;
+      step(GroupTag<1>(), sB, sA, t);
+      if (++t >= steps) break;
+      step(GroupTag<2>(), sA, sB, t);
+      if (++t >= steps) break;
+      step(GroupTag<3>(), sB, sA, t);
+      if (++t >= steps) break;
+    }
+  };
+  if (kg == 0) run(GroupTag<0>());
+  else run(GroupTag<1>());
+  // the look-ahead loads past the split's end read nothing from memory; let them land
+  // before the slots are reused and the workgroup's LDS is released
+  TAPS_WAIT_VMCNT(0);
+  __syncthreads();
+
+  const float lsum = l_run + other_half(l_run);
+  // ---- merge the key groups through LDS.  Group 0 finishes head dims 0..63 and group 1
+  // dims 64..127: each wave leaves the two O^T blocks the other group finishes, and its
+  // (max, sum), in the K slot of its own index.
+  auto xslot = [&](int w) -> float* {
+    switch (w) {
+      case 0: return (float*)s_k0;
+      case 1: return (float*)s_k1;
+      case 2: return (float*)s_k2;
+      case 3: return (float*)s_k3;
+      case 4: return (float*)s_k4;
+      case 5: return (float*)s_k5;
+      case 6: return (float*)s_k6;
+      default: return (float*)s_k7;
+    }
+  };
+  {
+    float* mine = xslot(wave);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int db = kg == 0 ? 2 + j : j;     // the blocks the other group finishes
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mine[(j * 16 + v) * 64 + lane] = o[db][v];
+    }
+    s_ml[wave * 64 + lane] = make_float2(m_ref, lsum);
+  }
+  __syncthreads();
+  const int other = wave ^ 4;
+  const float* theirs = xslot(other);
+  const float2 ml = s_ml[other * 64 + lane];
+  const float M = fmaxf(m_ref, ml.x);
+  const float a0 = m_ref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref - M);
+  const float a1 = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - M);
+  const float Ls = lsum * a0 + ml.y * a1;
+  const float inv = Ls > 0.f ? 1.f / Ls : 0.f;
+
+  // ---- write this split's partial: O / sum in bf16 (dims of this group), max and sum
+  const size_t obase = ((size_t)bg * splits + split) * mrows_pad;
+  const int qr = row0 + rg * 32 + l32;
+  uint16_t* op = wsO + (obase + qr) * HD;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int db = kg == 0 ? j : 2 + j;       // the blocks this group finishes
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      float x[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        x[t] = (o[db][4 * r4 + t] * a0 + theirs[(j * 16 + 4 * r4 + t) * 64 + lane] * a1) * inv;
+      const int d = db * 32 + 8 * r4 + 4 * hl;
+      *(uint2*)(op + d) = pack_bf16x4(x[0], x[1], x[2], x[3]);
+    }
+  }
+  if (kg == 0 && hl == 0) wsML[obase + qr] = make_float2(M, Ls);
+#endif
+}
+
 template <int HD>
 __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
-    const float* __restrict__ wsO, const float2* __restrict__ wsML,
+    const uint16_t* __restrict__ wsO, const float2* __restrict__ wsML,
     const int32_t* __restrict__ ctxp, const int32_t* __restrict__ nnp, int B, int N, int Hq,
     int Hkv, int max_ctx, int split_len, int splits, int mrows_pad, uint16_t* __restrict__ O) {
   constexpr int TPR = HD / 4;  // threads per output row, 4 values each
@@ -440,20 +767,21 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
   const int qr = i * G + (hq - g * G);
   const int nspl = (R + split_len - 1) / split_len;
   const size_t base = (size_t)(b * Hkv + g) * splits;
-  // one pass: the loads of up to 16 splits are issued together, then merged with a
-  // running maximum (the partial maxima are in base-2 units)
+  // each split holds O_s / l_s (bf16) and (m_s, l_s) with m_s in base 2:
+  // O = sum_s 2^(m_s - M) l_s (O_s / l_s) / sum_s 2^(m_s - M) l_s.  The loads of up to 16
+  // splits are issued together, then merged with a running maximum.
   constexpr int CH = 16;
   float M = -INFINITY, L = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int s0 = 0; s0 < nspl; s0 += CH) {
     float2 ml[CH];
-    float4 ov[CH];
+    uint2 ov[CH];
 #pragma unroll
     for (int t = 0; t < CH; ++t) {
       const bool ok = s0 + t < nspl;
       const size_t r = (base + s0 + t) * mrows_pad + qr;
       ml[t] = ok ? wsML[r] : make_float2(-INFINITY, 0.f);
-      ov[t] = ok ? *(const float4*)(wsO + r * HD + d) : make_float4(0.f, 0.f, 0.f, 0.f);
+      ov[t] = ok ? *(const uint2*)(wsO + r * HD + d) : make_uint2(0u, 0u);
     }
     float Mc = M;
 #pragma unroll
@@ -464,19 +792,18 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
     acc.x *= a; acc.y *= a; acc.z *= a; acc.w *= a;
 #pragma unroll
     for (int t = 0; t < CH; ++t) {
-      const float w = ml[t].x == -INFINITY ? 0.f : exp2f(ml[t].x - Mc);
-      L += w * ml[t].y;
-      acc.x += w * ov[t].x; acc.y += w * ov[t].y; acc.z += w * ov[t].z; acc.w += w * ov[t].w;
+      const float w = ml[t].x == -INFINITY ? 0.f : exp2f(ml[t].x - Mc) * ml[t].y;
+      L += w;
+      acc.x += w * __uint_as_float(ov[t].x << 16);
+      acc.y += w * __uint_as_float(ov[t].x & 0xFFFF0000u);
+      acc.z += w * __uint_as_float(ov[t].y << 16);
+      acc.w += w * __uint_as_float(ov[t].y & 0xFFFF0000u);
     }
     M = Mc;
   }
   const float inv = 1.f / L;
-  __bf16 r0 = (__bf16)(acc.x * inv), r1 = (__bf16)(acc.y * inv), r2 = (__bf16)(acc.z * inv),
-         r3 = (__bf16)(acc.w * inv);
-  uint2 pk;
-  pk.x = (uint32_t)__builtin_bit_cast(uint16_t, r0) | ((uint32_t)__builtin_bit_cast(uint16_t, r1) << 16);
-  pk.y = (uint32_t)__builtin_bit_cast(uint16_t, r2) | ((uint32_t)__builtin_bit_cast(uint16_t, r3) << 16);
-  *(uint2*)(O + (((size_t)b * N + i) * Hq + hq) * HD + d) = pk;
+  *(uint2*)(O + (((size_t)b * N + i) * Hq + hq) * HD + d) =
+      pack_bf16x4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
 }
 
 // ---------------------------------------------------------------- fp32 VALU path
@@ -592,7 +919,7 @@ AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max
 size_t attn_ws_bytes(const AttnPlan& pl, int batch, int /*budget*/, int /*Hq*/, int Hkv,
                      int head_dim) {
   const size_t rows = (size_t)batch * Hkv * pl.splits * (size_t)pl.mtiles * pl.mtile;
-  return rows * head_dim * sizeof(float) + rows * sizeof(float2) + 256;
+  return rows * head_dim * sizeof(uint16_t) + rows * sizeof(float2) + 256;
 }
 
 hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const int64_t* off,
@@ -603,8 +930,8 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
   if (batch <= 0) return hipSuccess;
   const int mrows_pad = pl.mtiles * pl.mtile;
   const size_t rows = (size_t)batch * Hkv * pl.splits * mrows_pad;
-  float* wsO = (float*)ws;
-  float2* wsML = (float2*)((char*)ws + rows * head_dim * sizeof(float));
+  uint16_t* wsO = (uint16_t*)ws;
+  float2* wsML = (float2*)((char*)ws + rows * head_dim * sizeof(uint16_t));
   const int pairs = pl.splits * batch * Hkv;
   dim3 grid((unsigned)(8 * pl.mtiles * ((pairs + 7) / 8)));
   dim3 block(256u);
@@ -612,23 +939,25 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
   const uint16_t *q = (const uint16_t*)Q, *k = (const uint16_t*)K, *v = (const uint16_t*)V;
   // with events, the launch records the kernel's own start and end (hipExtLaunchKernel)
   if (head_dim == 128) {
+    const dim3 block8(512u);
     if (ev_begin || ev_end)
-      hipExtLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, s, ev_begin, ev_end, 0, q, k,
-                            v, off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2, pl.split_len,
+      hipExtLaunchKernelGGL(attn_bf16_kernel, grid, block8, 0, s, ev_begin, ev_end, 0, q, k, v,
+                            off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2, pl.split_len,
                             pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML);
     else
-      attn_bf16_kernel<128><<<grid, block, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv,
-                                                   max_ctx, sl2, pl.split_len, pl.splits,
-                                                   pl.mtiles, pairs, mrows_pad, wsO, wsML);
+      attn_bf16_kernel<<<grid, block8, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv,
+                                               max_ctx, sl2, pl.split_len, pl.splits,
+                                               pl.mtiles, pairs, mrows_pad, wsO, wsML);
   } else {
     if (ev_begin || ev_end)
-      hipExtLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, s, ev_begin, ev_end, 0, q, k,
-                            v, off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2, pl.split_len,
-                            pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML);
+      hipExtLaunchKernelGGL(attn_bf16_w4_kernel<64>, grid, block, 0, s, ev_begin, ev_end, 0, q,
+                            k, v, off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2,
+                            pl.split_len, pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML);
     else
-      attn_bf16_kernel<64><<<grid, block, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv,
-                                                  max_ctx, sl2, pl.split_len, pl.splits,
-                                                  pl.mtiles, pairs, mrows_pad, wsO, wsML);
+      attn_bf16_w4_kernel<64><<<grid, block, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq,
+                                                     Hkv, max_ctx, sl2, pl.split_len,
+                                                     pl.splits, pl.mtiles, pairs, mrows_pad,
+                                                     wsO, wsML);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
