@@ -727,10 +727,21 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
   const float Ls = lsum * a0 + ml.y * a1;
   const float inv = Ls > 0.f ? 1.f / Ls : 0.f;
 
-  // ---- write this split's partial: O / sum in bf16 (dims of this group), max and sum
-  const size_t obase = ((size_t)bg * splits + split) * mrows_pad;
-  const int qr = row0 + rg * 32 + l32;
-  uint16_t* op = wsO + (obase + qr) * HD;
+  // ---- write this split's partial: O / sum in bf16 for this group's 64 head dims of the
+  // wave's 32 rows, max and sum.  The tile goes through LDS (this wave's V slot, free
+  // now) so that each store instruction writes whole 128-byte row segments.
+  constexpr int TROW = 144;            // bytes per staged row (128 + 16: fewer bank conflicts)
+  unsigned char* stage;
+  switch (wave) {
+    case 0: stage = s_v0; break;
+    case 1: stage = s_v1; break;
+    case 2: stage = s_v2; break;
+    case 3: stage = s_v3; break;
+    case 4: stage = s_v4; break;
+    case 5: stage = s_v5; break;
+    case 6: stage = s_v6; break;
+    default: stage = s_v7; break;
+  }
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int db = kg == 0 ? j : 2 + j;       // the blocks this group finishes
@@ -740,10 +751,21 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
 #pragma unroll
       for (int t = 0; t < 4; ++t)
         x[t] = (o[db][4 * r4 + t] * a0 + theirs[(j * 16 + 4 * r4 + t) * 64 + lane] * a1) * inv;
-      const int d = db * 32 + 8 * r4 + 4 * hl;
-      *(uint2*)(op + d) = pack_bf16x4(x[0], x[1], x[2], x[3]);
+      *(uint2*)(stage + l32 * TROW + 2 * (j * 32 + 8 * r4 + 4 * hl)) = pack_bf16x4(x[0], x[1], x[2], x[3]);
     }
   }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const size_t obase = ((size_t)bg * splits + split) * mrows_pad;
+  const int qbase = row0 + rg * 32;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 8 * i + (lane >> 3), c = (lane & 7) * 16;   // row in the tile, byte in the half
+    const uint4 v = *(const uint4*)(stage + r * TROW + c);
+    *(uint4*)((unsigned char*)(wsO + (obase + qbase + r) * HD) + kg * 128 + c) = v;
+  }
+  const int qr = qbase + l32;
   if (kg == 0 && hl == 0) wsML[obase + qr] = make_float2(M, Ls);
 #endif
 }
