@@ -36,6 +36,7 @@ constexpr int kWaves = kThreads / kWave;
 constexpr int kRowCap = TAPS_MAX_K * TAPS_MAX_K;  // entries >= the threshold, at most K*K
 constexpr int kCap = 3072;                        // expanded nodes held in LDS
 constexpr int kBins = 1024;
+constexpr int kCoarse = kBins / 16;
 constexpr int kBinBase = (1023 - 110) * 8;        // bin 0 holds u < 2^-110
 
 // ------------------------------------------------------------------ shared exponential
@@ -60,6 +61,11 @@ __host__ __device__ inline double spec_exp(double t) {
   for (int n = 12; n >= 0; --n) p = p * r + C[n];
   return ldexp(p, (int)kf);
 }
+
+template <int V>
+struct IntC {
+  static constexpr int value = V;
+};
 
 // ------------------------------------------------------------------ wave helpers
 __device__ inline int lanes_below(uint64_t mask) {
@@ -100,24 +106,34 @@ __device__ inline int wave_inclusive_sum(int v) {
   return v;
 }
 
-// exclusive prefix over the whole workgroup (values < 2^BITS); s_w holds kWaves ints
-template <int BITS>
-__device__ inline int block_prefix(int v, int* s_w, int& total) {
+// inclusive prefix sum within each row of 16 lanes
+__device__ inline int row_inclusive_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  return v;
+}
+
+// Exclusive prefix sum over the workgroup (every thread calls it, in uniform control
+// flow).  The wave totals pass through one of two LDS slots, alternating per call: a slot
+// is written again only two calls later, after every wave has passed the barrier of the
+// call in between, so one barrier per call suffices.
+__device__ inline int block_prefix(int v, int (*s_w)[kWaves], int& parity, int& total) {
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  int wt;
-  const int pre = wave_prefix_small<BITS>(v, wt);
-  if (lane == 0) s_w[wave] = wt;
+  const int incl = wave_inclusive_sum(v);
+  if (lane == kWave - 1) s_w[parity][wave] = incl;
   __syncthreads();
   int base = 0, tot = 0;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) {
-    const int x = s_w[w];
+    const int x = s_w[parity][w];
     base += w < wave ? x : 0;
     tot += x;
   }
-  __syncthreads();
+  parity ^= 1;
   total = tot;
-  return base + pre;
+  return base + incl - v;
 }
 
 // utility key: order-preserving bits of a non-negative double
@@ -161,9 +177,8 @@ struct Level {                 // expanded trie nodes, stored depth by depth
   int meta[kCap];              // parent index << 16 | depth << 8 | rank
   int newidx[kCap];
   int mlist[kCap];             // members of the boundary bin, in stored order
-  alignas(16) int hist[kBins];
-  int lvl_start[TAPS_MAX_BLOCK + 2];
-  int bsum[64];
+  int hist[kBins];             // nodes per utility bin
+  int chist[kCoarse];          // nodes per group of 16 bins
 };
 struct Seq {                   // sequential fallback: candidate children per selected node
   uint64_t U[TAPS_MAX_BUDGET][TAPS_MAX_K];
@@ -183,10 +198,27 @@ struct Shared {
   double e[TAPS_MAX_BLOCK][TAPS_MAX_K];
   double c[TAPS_MAX_BLOCK][TAPS_MAX_K];
   double den[TAPS_MAX_BLOCK + 1];
-  int wsum[kWaves];
-  int flag, bstar, n, total;
+  int wsum[2][kWaves];
+  int n;
   Scratch x;
 };
+
+// The pruning bin b*: the highest bin j such that at least N-1 expanded nodes lie in
+// bins >= j (0 if there is none).  Every wave computes it from the two histograms: the
+// coarse one picks the group of 16 bins, the fine one the bin within it.
+__device__ inline int find_bstar(const Level& L, int N) {
+  const int lane = threadIdx.x & (kWave - 1);
+  static_assert(kCoarse == kWave, "one coarse bin per lane");
+  const int incl = wave_inclusive_sum(L.chist[kCoarse - 1 - lane]);  // bins >= 16 (63 - lane)
+  const uint64_t ok = __ballot(incl >= N - 1);
+  if (ok == 0ull) return 0;
+  const int l0 = __ffsll((long long)ok) - 1;
+  const int C = kCoarse - 1 - l0;
+  const int above = l0 > 0 ? __builtin_amdgcn_readlane(incl, l0 - 1) : 0;
+  const int f = row_inclusive_sum(lane < 16 ? L.hist[C * 16 + 15 - lane] : 0);
+  const uint64_t ok2 = __ballot(lane < 16 && above + f >= N - 1);
+  return C * 16 + 15 - (__ffsll((long long)ok2) - 1);
+}
 
 // ------------------------------------------------------------------ Phase C fallback
 // Sequential best-first selection (one wave) for expansions larger than kCap; emits
@@ -340,46 +372,44 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
 
   // ---------------- Phase A: row merge (one wave per row)
+  // Loads below take clamped (in-bounds) addresses and are issued unconditionally, the
+  // values past the end being masked afterwards, so that each batch costs one round trip.
   {
     PhaseA& A = sh.x.a;
     const int CK = chunks * K;
-    for (int i = wave; i < D; i += kWavesA) {
+    auto merge_row = [&](auto jm_tag, int i) __attribute__((always_inline)) {
+      constexpr int JM = decltype(jm_tag)::value;   // 64-entry slices of the row's lists
       const uint64_t* rc = cand + ((size_t)b * D + i) * CK;
-      // loads of clamped (in-bounds) addresses under a wave-uniform count, zeroed
-      // afterwards: the loads issue back to back without per-lane branches
-      const int jmax = (CK + kWave - 1) / kWave;
-      uint64_t v[16];
+      uint64_t v[JM];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
+      for (int j = 0; j < JM; ++j) {
         const int e = j * kWave + lane;
-        v[j] = 0ull;
-        if (j < jmax) {
-          const uint64_t x = rc[min(e, CK - 1)];
-          v[j] = e < CK ? x : 0ull;
-        }
+        const uint64_t x = rc[min(e, CK - 1)];
+        v[j] = e < CK ? x : 0ull;
       }
       const uint64_t hx = rc[(size_t)min(lane, chunks - 1) * K];
       const uint64_t head = lane < chunks ? hx : 0ull;
-      A.heads[wave][lane] = head;
+      A.heads[wave][lane] = head;   // all 64 slots: zero past the last chunk
       wave_fence();
       int beat = 0;
-      for (int j0 = 0; j0 < chunks; j0 += 8) {
-        uint64_t hv[8];
+      for (int j0 = 0; j0 < chunks; j0 += 16) {
+        uint64_t hv[16];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) hv[t] = j0 + t < chunks ? A.heads[wave][j0 + t] : 0ull;
+        for (int t = 0; t < 16; ++t) hv[t] = A.heads[wave][j0 + t];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) beat += hv[t] > head ? 1 : 0;
+        for (int t = 0; t < 16; ++t) beat += hv[t] > head ? 1 : 0;
       }
       const int nheads = __popcll(__ballot(head != 0ull));
       uint64_t T = 1ull;  // fewer non-empty chunks than K: every entry is a candidate
       if (nheads >= K) {
-        const uint64_t sel = __ballot(head != 0ull && beat == K - 1);
-        T = A.heads[wave][__ffsll((long long)sel) - 1];
+        const int tl = __ffsll((long long)__ballot(head != 0ull && beat == K - 1)) - 1;
+        T = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(head >> 32), tl) << 32) |
+            (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)head, tl);
       }
       // compact the entries >= T (at most K*K of them) in order
       int total = 0;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
+      for (int j = 0; j < JM; ++j) {
         const uint64_t m = __ballot(v[j] >= T);
         const int pos = total + lanes_below(m);
         if (v[j] >= T && pos < kRowCap) A.rowc[wave][pos] = v[j];
@@ -387,28 +417,39 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
       }
       total = total < kRowCap ? total : kRowCap;
       wave_fence();
+      // exact ranks; the entry of rank r < K is the row's r-th candidate
+      const size_t orow = ((size_t)b * D + i) * K;
       for (int c0 = 0; c0 < total; c0 += kWave) {
         const int me = c0 + lane;
-        const uint64_t mine = me < total ? A.rowc[wave][me] : 0ull;
+        const uint64_t mx = A.rowc[wave][min(me, kRowCap - 1)];
+        const uint64_t mine = me < total ? mx : 0ull;
         int rank = 0;
-        for (int j0 = 0; j0 < total; j0 += 8) {
-          uint64_t rv[8];
+        for (int j0 = 0; j0 < total; j0 += 16) {
+          uint64_t rv[16];
 #pragma unroll
-          for (int t = 0; t < 8; ++t) rv[t] = j0 + t < total ? A.rowc[wave][j0 + t] : 0ull;
+          for (int t = 0; t < 16; ++t) {
+            const uint64_t x = A.rowc[wave][min(j0 + t, kRowCap - 1)];
+            rv[t] = j0 + t < total ? x : 0ull;
+          }
 #pragma unroll
-          for (int t = 0; t < 8; ++t) rank += rv[t] > mine ? 1 : 0;
+          for (int t = 0; t < 16; ++t) rank += rv[t] > mine ? 1 : 0;
         }
-        if (me < total && rank < K) sh.top[i][rank] = mine;
+        if (me < total && rank < K) {
+          sh.top[i][rank] = mine;
+          o_tidx[orow + rank] = (int32_t)cand_index(mine);
+          if (o_tval) o_tval[orow + rank] = value_from_key((uint32_t)(mine >> 32));
+        }
       }
-      for (int r = total + lane; r < K; r += kWave) sh.top[i][r] = 0ull;
-      wave_fence();
-      if (lane < K) {
-        const uint64_t k = sh.top[i][lane];
-        const size_t o = ((size_t)b * D + i) * K + lane;
-        o_tidx[o] = k ? (int32_t)cand_index(k) : -1;
-        if (o_tval) o_tval[o] = value_from_key((uint32_t)(k >> 32));
+      for (int r = total + lane; r < K; r += kWave) {   // a row with fewer than K entries
+        sh.top[i][r] = 0ull;
+        o_tidx[orow + r] = -1;
+        if (o_tval) o_tval[orow + r] = value_from_key(0u);
       }
       wave_fence();
+    };
+    for (int i = wave; i < D; i += kWavesA) {
+      if (CK <= 4 * kWave) merge_row(IntC<4>(), i);
+      else merge_row(IntC<16>(), i);
     }
   }
   __syncthreads();
@@ -433,7 +474,6 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
     sh.e[i][r] = e;
   }
   if (tid <= D) sh.den[tid] = lambda1 + lambda2 * (double)tid;
-  if (tid < kWaves) sh.wsum[tid] = 0;
   __syncthreads();
   for (int it = tid; it < D * K; it += kThreads) {
     const int i = it / K, r = it - (it / K) * K;
@@ -445,30 +485,29 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
   __syncthreads();
 
   // ---------------- Phase C: depth-by-depth expansion with a safe pruning bin
+  // floor(n / K) for 0 <= n < 2^20 as a high multiply by ceil(2^32 / K): the error term
+  // n (ceil(2^32/K) - 2^32/K) / 2^32 < 2^-12 never reaches the next integer
+  const uint32_t kmul = K > 1 ? (uint32_t)((0x100000000ull + (uint64_t)K - 1) / (uint64_t)K) : 0u;
+  auto divK = [&](int v) { return K > 1 ? (int)__umulhi((uint32_t)v, kmul) : v; };
   Level& L = sh.x.l;
   for (int j = tid; j < kBins; j += kThreads) L.hist[j] = 0;
+  if (tid < kCoarse) L.chist[tid] = 0;
   if (tid == 0) {
     L.q[0] = 1.0;
     L.u[0] = ubits(1.0 / sh.den[0]);
     L.meta[0] = (0xFFFF << 16) | 0;
-    L.lvl_start[0] = 0;
-    L.lvl_start[1] = 1;
-    sh.total = 1;
-    sh.bstar = 0;
-    sh.flag = 0;
   }
   __syncthreads();
-  int d = 0;
-  for (; d < D && N > 1; ++d) {
-    const int p0 = L.lvl_start[d], p1 = L.lvl_start[d + 1];
+  // uniform state: stored nodes [p0, p1) form the current depth, base nodes are stored
+  int parity = 0;
+  int p0 = 0, p1 = 1, base = 1, bstar = 0;
+  bool fallback = false;
+  for (int d = 0; d < D && N > 1; ++d) {
     const int items = (p1 - p0) * K;
     if (items == 0) break;
-    const int bstar = sh.bstar;
     const double den1 = sh.den[d + 1];
     // the level's items in chunks of up to 4 per thread, each thread taking contiguous
     // items so that the stored order stays (parent, rank)
-    int base = sh.total;
-    bool overflow = false;
     for (int c0 = 0; c0 < items; c0 += 4 * kThreads) {
       const int citems = min(items - c0, 4 * kThreads);
       const int per = (citems + kThreads - 1) / kThreads;
@@ -478,37 +517,42 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
       bool okv[4];
       int cnt = 0;
       const int it0 = c0 + tid * per;
-      int pp = p0 + it0 / K, rr = it0 - (it0 / K) * K;   // (parent, rank) of the first item
+      const int q0 = divK(it0);
+      // items past this thread's count are evaluated too (clamped parent index, so every
+      // load is in bounds and the loads and fp64 arithmetic of all items overlap) and
+      // masked; a chunk of at most one item per thread evaluates one
+      auto eval = [&](auto ni_tag) __attribute__((always_inline)) {
+        constexpr int NI = decltype(ni_tag)::value;
+        int pp = p0 + q0, rr = it0 - q0 * K;   // (parent, rank) of the first item
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int it = it0 + k;
-        okv[k] = false;
-        qv[k] = uv[k] = 0.0;
-        mv[k] = bv[k] = 0;
-        const int p = pp, r = rr;
-        if (++rr == K) { rr = 0; ++pp; }
-        // items beyond this chunk's per-thread count are skipped (a wave-uniform test);
-        // the others are evaluated without branches (clamped parent index), so their loads
-        // and fp64 arithmetic overlap; invalid ones are masked
-        if (k >= per) continue;
-        const int pc = min(p, p1 - 1);
-        const uint64_t pu = L.u[pc];
-        const double qp = L.q[pc], cr = sh.c[d][r];
-        const double q = qp * cr;
-        const double u = q / den1;
-        const int bn = ubin(u);
-        okv[k] = k < per && it < c0 + citems &&
-                 ubin(__longlong_as_double((long long)pu)) >= bstar && u > tau && bn >= bstar;
-        qv[k] = q;
-        uv[k] = u;
-        bv[k] = bn;
-        mv[k] = (p << 16) | ((d + 1) << 8) | r;
-        cnt += okv[k] ? 1 : 0;
-      }
+        for (int k = 0; k < NI; ++k) {
+          const int it = it0 + k;
+          const int p = pp, r = rr;
+          if (++rr == K) { rr = 0; ++pp; }
+          const int pc = min(p, p1 - 1);
+          const uint64_t pu = L.u[pc];
+          const double qp = L.q[pc], cr = sh.c[d][r];
+          const double q = qp * cr;
+          const double u = q / den1;
+          const int bn = ubin(u);
+          // non-short-circuit: no branch may separate a load from the others
+          okv[k] = (k < per) & (it < c0 + citems) &
+                   (ubin(__longlong_as_double((long long)pu)) >= bstar) & (u > tau) & (bn >= bstar);
+          qv[k] = q;
+          uv[k] = u;
+          bv[k] = bn;
+          mv[k] = (p << 16) | ((d + 1) << 8) | r;
+          cnt += okv[k] ? 1 : 0;
+        }
+#pragma unroll
+        for (int k = NI; k < 4; ++k) okv[k] = false;
+      };
+      if (per == 1) eval(IntC<1>());
+      else eval(IntC<4>());
       int total;
-      const int pre = block_prefix<3>(cnt, sh.wsum, total);
+      const int pre = block_prefix(cnt, sh.wsum, parity, total);
       if (base + total > kCap) {       // uniform: the expansion outgrows LDS
-        overflow = true;
+        fallback = true;
         break;
       }
       int pos = base + pre;
@@ -519,137 +563,83 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
           L.u[pos] = ubits(uv[k]);
           L.meta[pos] = mv[k];
           atomicAdd(&L.hist[bv[k]], 1);
+          atomicAdd(&L.chist[bv[k] >> 4], 1);
           ++pos;
         }
       }
       base += total;
     }
-    if (overflow) {
-      if (tid == 0) sh.flag = 1;
-      __syncthreads();
-      break;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      sh.total = base;
-      L.lvl_start[d + 2] = base;
-    }
-    // new b*: the highest bin whose suffix count reaches N-1 (0 while fewer nodes exist)
-    if (wave == 0 && base >= N - 1) {
-      constexpr int BPL = kBins / kWave;  // bins per lane
-      int hv[BPL];
-#pragma unroll
-      for (int j = 0; j < BPL / 4; ++j) {
-        const int4 h4 = *(const int4*)&L.hist[lane * BPL + 4 * j];
-        hv[4 * j] = h4.x; hv[4 * j + 1] = h4.y; hv[4 * j + 2] = h4.z; hv[4 * j + 3] = h4.w;
-      }
-      int sl = 0;
-#pragma unroll
-      for (int j = 0; j < BPL; ++j) sl += hv[j];
-      const int incl = wave_inclusive_sum(sl);
-      const int tot_all = __shfl(incl, kWave - 1);
-      const int suffix = tot_all - (incl - sl);      // nodes in this lane's bins and above
-      const uint64_t ok = __ballot(N > 1 && suffix >= N - 1);
-      if (ok != 0ull) {
-        const int Ls = 63 - __clzll((long long)ok);
-        if (lane == Ls) {
-          // the highest bin j of this lane whose suffix count reaches N-1
-          int run = suffix - sl;
-          int bsel = Ls * BPL;
-          bool found = false;
-#pragma unroll
-          for (int j = BPL - 1; j >= 0; --j) {
-            run += hv[j];
-            if (!found && run >= N - 1) { bsel = Ls * BPL + j; found = true; }
-          }
-          sh.bstar = bsel;
-        }
-      } else if (lane == 0) {
-        sh.bstar = 0;
-      }
-    }
-    __syncthreads();
+    if (fallback) break;
+    __syncthreads();   // the level's nodes and histogram counts are complete
+    p0 = p1;
+    p1 = base;
+    if (base >= N - 1) bstar = find_bstar(L, N);
   }
   int n;
-  const bool fallback = sh.flag != 0;
   if (!fallback) {
-    // ---- final cut: keep bins > b*, rank the members of bin b* exactly
-    const int tot = sh.total, bstar = sh.bstar;
-    const int per = (tot + kThreads - 1) / kThreads;   // <= kCap / kThreads = 12
-    int above = 0, inb = 0;
-    for (int k = 0; k < per; ++k) {
-      const int j = tid * per + k;
-      if (j >= 1 && j < tot) {
-        const int bn = ubin(__longlong_as_double((long long)L.u[j]));
-        above += bn > bstar ? 1 : 0;
-        inb += bn == bstar ? 1 : 0;
-      }
+    // ---- final cut: keep bins > b*; members of bin b* compete for the places left.
+    // Thread t owns the stored nodes t*per .. t*per + per - 1 (per <= kCap / kThreads);
+    // bit k of a mask below stands for its node t*per + k.
+    const int tot = base;
+    const int per = (tot + kThreads - 1) / kThreads;
+    const int j0 = tid * per;
+    const int jn = min(per, tot - j0);   // nodes this thread owns (may be <= 0)
+    uint32_t amask = 0u, bmask = 0u;     // bins > b* (the root counts here), bin b*
+    for (int k = 0; k < jn; ++k) {
+      const int j = j0 + k;
+      const int bn = ubin(__longlong_as_double((long long)L.u[j]));
+      if (j == 0 || bn > bstar) amask |= 1u << k;
+      else if (bn == bstar) bmask |= 1u << k;
     }
-    int c_hi, c_b;
-    block_prefix<4>(above, sh.wsum, c_hi);   // per <= kCap / kThreads = 12
-    int mpos = block_prefix<4>(inb, sh.wsum, c_b);
-    for (int k = 0; k < per; ++k) {
-      const int j = tid * per + k;
-      if (j >= 1 && j < tot && ubin(__longlong_as_double((long long)L.u[j])) == bstar)
-        L.mlist[mpos++] = j;
-    }
+    const int above = __popc(amask) - (j0 == 0 && jn > 0 ? 1 : 0), inb = __popc(bmask);
+    // both counts in one prefix: each total stays below 2^16
+    int tot2;
+    const int pre2 = block_prefix(above | (inb << 16), sh.wsum, parity, tot2);
+    const int c_hi = tot2 & 0xFFFF, c_b = tot2 >> 16;
     const int room = N - 1 - c_hi;   // places left for members of bin b*
-    __syncthreads();
-    for (int j = tid; j < tot; j += kThreads) {
-      int keep = 0;
-      if (j == 0) {
-        keep = 1;
-      } else {
-        const int bn = ubin(__longlong_as_double((long long)L.u[j]));
-        keep = bn > bstar || (bn == bstar && c_b <= room);
-      }
-      L.newidx[j] = keep;
-    }
-    if (c_b > room) {
-      // members ranked by (u desc, stored index asc); the stored index orders equal
-      // utilities exactly like (depth, rank path)
-      for (int i = tid; i < c_b; i += kThreads) {
-        const int j = L.mlist[i];
+    uint32_t kmask = amask | bmask;
+    if (c_b > room) {                // uniform: the members of bin b* are ranked
+      int mpos = pre2 >> 16;
+      for (uint32_t m = bmask; m; m &= m - 1) L.mlist[mpos++] = j0 + __ffs(m) - 1;
+      __syncthreads();
+      // a member is kept if fewer than `room` members beat it under (u desc, stored index
+      // asc): the stored index orders equal utilities exactly like (depth, rank path)
+      for (uint32_t m = bmask; m; m &= m - 1) {
+        const int k = __ffs(m) - 1, j = j0 + k;
         const uint64_t uj = L.u[j];
         int rank = 0;
         for (int k0 = 0; k0 < c_b; k0 += 8) {
           uint64_t ukv[8];
           int jk[8];
 #pragma unroll
-          for (int t = 0; t < 8; ++t) {
-            jk[t] = k0 + t < c_b ? L.mlist[k0 + t] : 0x7FFFFFFF;
-            ukv[t] = k0 + t < c_b ? L.u[jk[t]] : 0ull;
-          }
+          for (int t = 0; t < 8; ++t) jk[t] = L.mlist[min(k0 + t, c_b - 1)];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) ukv[t] = L.u[jk[t]];
 #pragma unroll
           for (int t = 0; t < 8; ++t)
             rank += (k0 + t < c_b && (ukv[t] > uj || (ukv[t] == uj && jk[t] < j))) ? 1 : 0;
         }
-        L.newidx[j] = rank < room ? 1 : 0;
+        if (rank >= room) kmask &= ~(1u << k);
       }
     }
-    __syncthreads();
     // breadth-first compaction: stored order is already (depth, rank path)
-    int cnt = 0;
-    for (int k = 0; k < per; ++k) {
-      const int j = tid * per + k;
-      cnt += j < tot ? L.newidx[j] : 0;
-    }
     int total;
-    int pre = block_prefix<4>(cnt, sh.wsum, total);
-    for (int k = 0; k < per; ++k) {
-      const int j = tid * per + k;
-      if (j < tot) {
-        const int keep = L.newidx[j];
-        L.newidx[j] = keep ? pre : -1;
-        pre += keep;
+    const int pos0 = block_prefix(__popc(kmask), sh.wsum, parity, total);
+    {
+      int pos = pos0;
+      for (int k = 0; k < jn; ++k) {
+        const bool kp = (kmask >> k) & 1u;
+        L.newidx[j0 + k] = kp ? pos : -1;
+        pos += kp ? 1 : 0;
       }
     }
     __syncthreads();
     n = total;
-    for (int j = tid; j < tot; j += kThreads) {
-      const int o = L.newidx[j];
-      if (o >= 0) {
-        const size_t g = (size_t)b * N + o;
+    {
+      int pos = pos0;
+      for (uint32_t m = kmask; m; m &= m - 1) {
+        const int j = j0 + __ffs(m) - 1;
+        const size_t g = (size_t)b * N + pos++;
         const int meta = L.meta[j];
         const int dj = (meta >> 8) & 0xFF, rj = meta & 0xFF, pj = meta >> 16;
         o_parent[g] = j == 0 ? -1 : L.newidx[pj];
