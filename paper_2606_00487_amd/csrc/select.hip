@@ -148,6 +148,12 @@ __device__ inline float value_from_key(uint32_t vk) {
   return __uint_as_float((vk & 0x80000000u) ? (vk & 0x7FFFFFFFu) : ~vk);
 }
 
+// the value of lane l (wave-uniform l) in every lane
+__device__ inline uint64_t read_lane_u64(uint64_t v, int l) {
+  return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(v >> 32), l) << 32) |
+         (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+}
+
 __device__ inline uint64_t wave_max_u64(uint64_t v) {
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) {
@@ -168,7 +174,6 @@ __device__ inline uint32_t wave_min_u32(uint32_t v) {
 
 // ------------------------------------------------------------------ shared memory layout
 struct PhaseA {
-  uint64_t heads[kWavesA][64];
   uint64_t rowc[kWavesA][kRowCap];
 };
 struct Level {                 // expanded trie nodes, stored depth by depth
@@ -389,22 +394,15 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
       }
       const uint64_t hx = rc[(size_t)min(lane, chunks - 1) * K];
       const uint64_t head = lane < chunks ? hx : 0ull;
-      A.heads[wave][lane] = head;   // all 64 slots: zero past the last chunk
-      wave_fence();
+      // heads that beat this lane's head, read across lanes (no LDS traffic: sixteen
+      // waves share the LDS pipe here)
       int beat = 0;
-      for (int j0 = 0; j0 < chunks; j0 += 16) {
-        uint64_t hv[16];
-#pragma unroll
-        for (int t = 0; t < 16; ++t) hv[t] = A.heads[wave][j0 + t];
-#pragma unroll
-        for (int t = 0; t < 16; ++t) beat += hv[t] > head ? 1 : 0;
-      }
+      for (int t = 0; t < chunks; ++t) beat += read_lane_u64(head, t) > head ? 1 : 0;
       const int nheads = __popcll(__ballot(head != 0ull));
       uint64_t T = 1ull;  // fewer non-empty chunks than K: every entry is a candidate
       if (nheads >= K) {
         const int tl = __ffsll((long long)__ballot(head != 0ull && beat == K - 1)) - 1;
-        T = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(head >> 32), tl) << 32) |
-            (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)head, tl);
+        T = read_lane_u64(head, tl);
       }
       // compact the entries >= T (at most K*K of them) in order
       int total = 0;
@@ -424,15 +422,19 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
         const uint64_t mx = A.rowc[wave][min(me, kRowCap - 1)];
         const uint64_t mine = me < total ? mx : 0ull;
         int rank = 0;
-        for (int j0 = 0; j0 < total; j0 += 16) {
-          uint64_t rv[16];
+        if (total <= kWave) {   // every candidate sits in a lane: compare across lanes
+          for (int t = 0; t < total; ++t) rank += read_lane_u64(mine, t) > mine ? 1 : 0;
+        } else {
+          for (int j0 = 0; j0 < total; j0 += 16) {
+            uint64_t rv[16];
 #pragma unroll
-          for (int t = 0; t < 16; ++t) {
-            const uint64_t x = A.rowc[wave][min(j0 + t, kRowCap - 1)];
-            rv[t] = j0 + t < total ? x : 0ull;
+            for (int t = 0; t < 16; ++t) {
+              const uint64_t x = A.rowc[wave][min(j0 + t, kRowCap - 1)];
+              rv[t] = j0 + t < total ? x : 0ull;
+            }
+#pragma unroll
+            for (int t = 0; t < 16; ++t) rank += rv[t] > mine ? 1 : 0;
           }
-#pragma unroll
-          for (int t = 0; t < 16; ++t) rank += rv[t] > mine ? 1 : 0;
         }
         if (me < total && rank < K) {
           sh.top[i][rank] = mine;

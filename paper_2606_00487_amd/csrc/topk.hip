@@ -5,8 +5,8 @@
 // descending, to the workspace.  The selection kernel merges the chunks of a row.
 //
 // Per wave: every lane holds E values in registers (16-byte coalesced loads).  The
-// K-th largest lane maximum T is found by a bitwise descent with ballots; only values
-// with key >= T can be in the wave's top-K, and there are few of them, so they are
+// K-th largest lane maximum T is found by a descent over its key bits with ballots; only
+// values >= T can be in the wave's top-K, and there are few of them, so they are
 // compacted into LDS and ranked exactly by counting.  A wave whose compacted set
 // overflows falls back to K rounds of exact wave-wide argmax.  The four wave lists are
 // merged by ranking again.
@@ -36,28 +36,31 @@ __device__ inline uint64_t wave_max_u64(uint64_t v) {
 }
 
 
+// LDS exchange between the lanes of one wave (its LDS accesses execute in order)
 __device__ inline void wave_fence_lds() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// the value of lane l (wave-uniform l) in every lane
+__device__ inline uint64_t read_lane_u64(uint64_t v, int l) {
+  return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(v >> 32), l) << 32) |
+         (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
 }
 
 // after every wave wrote its sorted top-K list at s_top[w*K ...]: wave 0 merges the
 // kWaves lists (at most 64 entries, one per lane) and writes the chunk's K best keys
 __device__ inline void merge_and_store(const uint64_t* s_top, int K, int wave, int lane,
                                        uint64_t* outp) {
+  static_assert(kWaves * TAPS_MAX_K <= kWave, "one list entry per lane");
   __syncthreads();
   if (wave != 0) return;
   const int tot = kWaves * K;
-  const uint64_t mine = lane < tot ? s_top[lane] : 0ull;
+  const uint64_t mx = s_top[min(lane, tot - 1)];
+  const uint64_t mine = lane < tot ? mx : 0ull;
   int rank = 0;
-  for (int j0 = 0; j0 < tot; j0 += 8) {
-    uint64_t cv[8];
-#pragma unroll
-    for (int t = 0; t < 8; ++t) cv[t] = j0 + t < tot ? s_top[j0 + t] : 0ull;
-#pragma unroll
-    for (int t = 0; t < 8; ++t) rank += cv[t] > mine ? 1 : 0;
-  }
+  for (int t = 0; t < tot; ++t) rank += read_lane_u64(mine, t) > mine ? 1 : 0;
   if (lane < tot && mine != 0ull && rank < K) outp[rank] = mine;
   // ranks held by empty entries: write 0 (a chunk with fewer than K elements)
   const int nonempty = __popcll(__ballot(lane < tot && mine != 0ull));
@@ -197,6 +200,107 @@ __device__ inline void generic_wave_topk(const void* rowp, bool aligned, int sta
   }
 }
 
+// bf16 chunks whose length is a multiple of 8 and whose row is 16-byte aligned: the
+// wave's K best keys into s_wave_top[wave*K ...].  Filtering uses float compares (NaN
+// fails every compare, -0 equals +0, exactly like the integer keys); exact keys are built
+// only for the few candidates.  Returns false (nothing written) when the wave has fewer
+// than K non-NaN lanes or too many candidates; the generic path then takes the wave.
+template <int E>
+__device__ inline bool fast_wave_topk_bf16(const void* rowp, int start, int end, int tid,
+                                           int lane, int wave, int K, uint64_t* s_wc,
+                                           uint64_t* s_wave_top) {
+  static_assert(E % 8 == 0, "whole 16-byte units");
+  // units past the chunk's end load an in-bounds unit and are replaced by NaN
+  uint32_t w[E / 2];
+#pragma unroll
+  for (int k = 0; k < E / 8; ++k) {
+    const int u = start + (tid + kThreads * k) * 8;
+    const uint4 v = *(const uint4*)((const char*)rowp + (int64_t)min(u, end - 8) * 2);
+    const bool in = u < end;
+    w[4 * k] = in ? v.x : 0x7FC07FC0u;
+    w[4 * k + 1] = in ? v.y : 0x7FC07FC0u;
+    w[4 * k + 2] = in ? v.z : 0x7FC07FC0u;
+    w[4 * k + 3] = in ? v.w : 0x7FC07FC0u;
+  }
+  float mx = -INFINITY;
+  bool anynum = false;
+#pragma unroll
+  for (int j = 0; j < E / 2; ++j) {
+    const float lo = __uint_as_float(w[j] << 16), hi = __uint_as_float(w[j] & 0xFFFF0000u);
+    mx = fmaxf(mx, fmaxf(lo, hi));   // ignores NaN
+    anynum |= lo == lo || hi == hi;
+  }
+  if (__popcll(__ballot(anynum)) < K) return false;   // uniform
+  // T: the largest 16-bit key with at least K lane maxima >= it, two bits per step
+  const uint32_t lk = anynum ? (value_key(__float_as_uint(mx)) >> 16) : 0u;
+  uint32_t T = 0;
+#pragma unroll
+  for (int b = 14; b >= 0; b -= 2) {
+    const uint32_t c1 = T | (1u << b), c2 = T | (2u << b), c3 = T | (3u << b);
+    const int n1 = __popcll(__ballot(lk >= c1));
+    const int n2 = __popcll(__ballot(lk >= c2));
+    const int n3 = __popcll(__ballot(lk >= c3));
+    T = n3 >= K ? c3 : (n2 >= K ? c2 : (n1 >= K ? c1 : T));
+  }
+  const float tf = __uint_as_float((T & 0x8000u) ? ((T & 0x7FFFu) << 16) : (~(T << 16) & 0xFFFF0000u));
+  // compact the elements >= tf in element order; the ballots of a 16-byte unit are taken
+  // together and the unit is skipped when none of its lanes holds a candidate
+  int total = 0;
+#pragma unroll
+  for (int k = 0; k < E / 8; ++k) {
+    uint64_t m[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const int j = 8 * k + t;
+      const uint32_t bits = (j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16);
+      m[t] = __ballot(__uint_as_float(bits) >= tf);
+    }
+    if ((m[0] | m[1] | m[2] | m[3] | m[4] | m[5] | m[6] | m[7]) == 0ull) continue;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      if (m[t]) {
+        const int j = 8 * k + t;
+        const uint32_t bits = (j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16);
+        const int pos = total + __builtin_amdgcn_mbcnt_hi((uint32_t)(m[t] >> 32),
+                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)m[t], 0u));
+        const int e = start + (tid + kThreads * k) * 8 + t;
+        if (((m[t] >> lane) & 1ull) && pos < kWaveCap) s_wc[pos] = cand_key(value_key(bits), (uint32_t)e);
+        total += __popcll(m[t]);
+      }
+    }
+  }
+  if (total > kWaveCap) return false;   // uniform; rare (many ties)
+  wave_fence_lds();
+  // exact ranks among the candidates
+  if (total <= kWave) {
+    const uint64_t cx = s_wc[min(lane, total - 1)];
+    const uint64_t mine = lane < total ? cx : 0ull;
+    int rank = 0;
+    for (int t = 0; t < total; ++t) rank += read_lane_u64(mine, t) > mine ? 1 : 0;
+    if (lane < total && rank < K) s_wave_top[wave * K + rank] = mine;
+  } else {
+    for (int c0 = 0; c0 < total; c0 += kWave) {
+      const int me = c0 + lane;
+      const uint64_t cx = s_wc[min(me, total - 1)];
+      const uint64_t mine = me < total ? cx : 0ull;
+      int rank = 0;
+      for (int j0 = 0; j0 < total; j0 += 8) {
+        uint64_t cv[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const uint64_t x = s_wc[min(j0 + t, total - 1)];
+          cv[t] = j0 + t < total ? x : 0ull;
+        }
+#pragma unroll
+        for (int t = 0; t < 8; ++t) rank += cv[t] > mine ? 1 : 0;
+      }
+      if (me < total && rank < K) s_wave_top[wave * K + rank] = mine;
+    }
+  }
+  for (int r = total + lane; r < K; r += kWave) s_wave_top[wave * K + r] = 0ull;
+  return true;
+}
+
 template <int DT, int E>
 __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __restrict__ marg,
                                                               int vocab, int K, int chunk_len,
@@ -215,68 +319,8 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __rest
   const bool aligned = (((uintptr_t)rowp) & 15) == 0;
 
   bool done = false;
-  if (DT == TAPS_BF16 && aligned && end - start == chunk_len) {
-    // ---- fast path: a full, aligned bf16 chunk.  Filtering uses float compares (NaN
-    // fails every compare, -0 equals +0, exactly like the integer keys); exact keys are
-    // built only for the few candidates.
-    uint32_t w[E / 2];
-#pragma unroll
-    for (int k = 0; k < E / 8; ++k) {
-      const uint4 u = *(const uint4*)((const char*)rowp + (int64_t)(start + (tid + kThreads * k) * 8) * 2);
-      w[4 * k] = u.x; w[4 * k + 1] = u.y; w[4 * k + 2] = u.z; w[4 * k + 3] = u.w;
-    }
-    float mx = -INFINITY;
-    bool anynum = false;
-#pragma unroll
-    for (int j = 0; j < E / 2; ++j) {
-      const float lo = __uint_as_float(w[j] << 16), hi = __uint_as_float(w[j] & 0xFFFF0000u);
-      mx = fmaxf(mx, fmaxf(lo, hi));   // ignores NaN
-      anynum |= lo == lo || hi == hi;
-    }
-    const bool lane_ok = anynum;                     // the lane holds a non-NaN value
-    if (__popcll(__ballot(lane_ok)) >= K) {          // uniform per wave
-      const uint32_t lk = lane_ok ? (value_key(__float_as_uint(mx)) >> 16) : 0u;
-      uint32_t T = 0;
-      for (int bit = 15; bit >= 0; --bit) {
-        const uint32_t c = T | (1u << bit);
-        if (__popcll(__ballot(lk >= c)) >= K) T = c;
-      }
-      const float tf = __uint_as_float((T & 0x8000u) ? ((T & 0x7FFFu) << 16) : (~(T << 16) & 0xFFFF0000u));
-      // compact the elements >= tf, in element order
-      int total = 0;
-#pragma unroll
-      for (int j = 0; j < E; ++j) {
-        const uint32_t bits = (j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16);
-        const bool c = __uint_as_float(bits) >= tf;
-        const uint64_t m = __ballot(c);
-        if (m) {
-          const int pos = total + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                            __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-          const int e = start + (tid + kThreads * (j / 8)) * 8 + (j % 8);
-          if (c && pos < kWaveCap) s_cand[wave][pos] = cand_key(value_key(bits), (uint32_t)e);
-          total += __popcll(m);
-        }
-      }
-      if (total <= kWaveCap) {
-        wave_fence_lds();
-        for (int c0 = 0; c0 < total; c0 += kWave) {
-          const int me = c0 + lane;
-          const uint64_t mine = me < total ? s_cand[wave][me] : 0ull;
-          int rank = 0;
-          for (int j0 = 0; j0 < total; j0 += 8) {
-            uint64_t cv[8];
-#pragma unroll
-            for (int t = 0; t < 8; ++t) cv[t] = j0 + t < total ? s_cand[wave][j0 + t] : 0ull;
-#pragma unroll
-            for (int t = 0; t < 8; ++t) rank += cv[t] > mine ? 1 : 0;
-          }
-          if (me < total && rank < K) s_wave_top[wave * K + rank] = mine;
-        }
-        done = true;
-      }
-    }
-    // rare: too few non-NaN lanes or too many ties for the compaction buffer
-  }
+  if (DT == TAPS_BF16 && aligned && ((end - start) & 7) == 0 && end - start >= 8)
+    done = fast_wave_topk_bf16<E>(rowp, start, end, tid, lane, wave, K, s_cand[wave], s_wave_top);
   if (!done) generic_wave_topk<DT, E>(rowp, aligned, start, end, tid, lane, wave, K,
                                       s_cand[wave], s_wave_top);
   merge_and_store(s_wave_top, K, wave, lane, cand + ((size_t)row * chunks + chunk) * K);
