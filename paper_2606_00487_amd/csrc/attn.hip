@@ -440,6 +440,33 @@ __global__ __launch_bounds__(256) void attn_bf16_w4_kernel(
 // four-wave kernel: the softmax and P V of a stage run together with the MFMAs of S for
 // the group's next stage.  The step loop is written once per group (template) and
 // unrolled by four, so that every LDS access names its slot statically.
+// Division of small non-negative ints by the launch's tile, split, head and group
+// counts: floor(n / d) = high half of n * ceil(2^32 / d), exact for n < 2^32 / d (the
+// rounding term of the multiplier adds less than n / 2^32 < 1/d to n / d)
+struct DivMagic {
+  uint32_t mt, sp, hk, g;
+  __device__ int div(int n, int d, uint32_t m) const {
+    return d == 1 ? n : (int)__umulhi((uint32_t)n, m);
+  }
+  static uint32_t make(int d) {
+    return d > 1 ? (uint32_t)((0x100000000ull + (uint64_t)d - 1) / (uint64_t)d) : 0u;
+  }
+};
+
+// The request's context length, node count and KV offset in one scalar-memory round
+// trip (issued together, then one wait)
+__device__ inline void load_request_scalars(const int32_t* c, const int32_t* nn,
+                                            const int64_t* o, int& cv, int& nv, int64_t& ov) {
+  asm volatile(
+      "s_load_dword %0, %3, 0x0\n\t"
+      "s_load_dword %1, %4, 0x0\n\t"
+      "s_load_dwordx2 %2, %5, 0x0\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&s"(cv), "=&s"(nv), "=&s"(ov)
+      : "s"(c), "s"(nn), "s"(o)
+      : "memory");
+}
+
 template <int KG>
 struct GroupTag {
   static constexpr int value = KG;
@@ -451,7 +478,7 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     const int32_t* __restrict__ ctxp, const int32_t* __restrict__ parentp,
     const int32_t* __restrict__ nnp, int N, int Hq, int Hkv, int max_ctx, float scale_log2,
     int split_len, int splits, int mtiles, int pairs, int mrows_pad, uint16_t* __restrict__ wsO,
-    float2* __restrict__ wsML) {
+    float2* __restrict__ wsML, DivMagic dm) {
   // the body uses the buffer-resource type, which exists only in the device pass; the
   // host pass needs no more than the signature to emit the launch stub
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -474,25 +501,50 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
   __shared__ int s_par[TAPS_MAX_BUDGET];
   __shared__ float2 s_ml[8 * 64];
 
+  // every kernel argument into scalar registers at once: one round trip for all of them
+  // instead of one per first use
+  asm volatile("" ::"s"(Q), "s"(Kc), "s"(Vc), "s"(offp), "s"(ctxp), "s"(parentp), "s"(nnp),
+               "s"(N), "s"(Hq), "s"(Hkv), "s"(max_ctx), "s"(scale_log2), "s"(split_len),
+               "s"(splits), "s"(mtiles), "s"(pairs), "s"(mrows_pad), "s"(wsO), "s"(wsML),
+               "s"(dm.mt), "s"(dm.sp), "s"(dm.hk), "s"(dm.g));
   // ---- which (request, KV head, split, row tile) this workgroup owns
   const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-  const int mt = slot % mtiles, pair = (slot / mtiles) * 8 + xcd;
+  const int sq = dm.div(slot, mtiles, dm.mt);
+  const int mt = slot - sq * mtiles, pair = sq * 8 + xcd;
   if (pair >= pairs) return;
-  const int split = pair % splits, bg = pair / splits;
-  const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
-  const int G = Hq / Hkv;
+  const int bg = dm.div(pair, splits, dm.sp);
+  const int split = pair - bg * splits;
+  const int b = dm.div(bg, Hkv, dm.hk), g = bg - b * Hkv;
+  const int G = dm.div(Hq, Hkv, dm.hk);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rg = wave & 3, kg = wave >> 2;
   const int l32 = lane & 31, hl = lane >> 5;
+  const int row0 = mt * MT;
 
-  const int ctx = min(max(ctxp[b], 0), max_ctx);
-  const int n = min(max(nnp[b], 0), N);
+  // ---- queries of this lane (B operand of S^T = K Q^T) and the parent pointer of node
+  // tid: their addresses do not depend on the request's sizes, so they go out first
+  bf16x8 q[NKK];
+  int qnode;
+  {
+    int qr = row0 + rg * 32 + l32;
+    qr = min(qr, N * G - 1);
+    const int node = dm.div(qr, G, dm.g), hq = g * G + (qr - node * G);
+    qnode = node;
+    const uint16_t* qp = Q + (((size_t)b * N + node) * Hq + hq) * HD;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) q[kk] = *(const bf16x8*)(qp + kk * 16 + hl * 8);
+  }
+  const int par_raw = parentp[(size_t)b * N + min(tid, N - 1)];
+
+  int ctx_raw, n_raw;
+  int64_t kv0;
+  load_request_scalars(ctxp + b, nnp + b, offp + b, ctx_raw, n_raw, kv0);
+  const int ctx = min(max(ctx_raw, 0), max_ctx);
+  const int n = min(max(n_raw, 0), N);
   const int R = ctx + n;
   const int k_begin = split * split_len;
   const int k_end = min(R, k_begin + split_len);
-  const int row0 = mt * MT;
   if (k_begin >= k_end || row0 >= n * G) return;
-  const int64_t kv0 = offp[b];
   const size_t row_stride = (size_t)Hkv * HD;
   const uint32_t rsb = (uint32_t)(row_stride * 2);
   const int nst = (k_end - k_begin + KT - 1) / KT;   // 32-key stages of this split
@@ -519,20 +571,8 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
                                              (uint32_t)(s * KT) * rsb, 0, 0);
   };
 
-  // ---- queries of this lane (B operand of S^T = K Q^T)
-  bf16x8 q[NKK];
-  int qnode;
-  {
-    int qr = row0 + rg * 32 + l32;
-    qr = min(qr, N * G - 1);
-    const int node = qr / G, hq = g * G + (qr - node * G);
-    qnode = node;
-    const uint16_t* qp = Q + (((size_t)b * N + node) * Hq + hq) * HD;
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) q[kk] = *(const bf16x8*)(qp + kk * 16 + hl * 8);
-  }
   const bool tree_split = k_end > ctx;
-  const int my_par = tree_split && tid < n ? parentp[(size_t)b * N + tid] : -1;
+  const int my_par = tree_split && tid < n ? par_raw : -1;
   // K(0) K(1) and the loads of step -3 [V(2t+6) V(2t+7) K(2t+8) K(2t+9)] now; those of
   // steps -2 and -1 after the first S (so its reads of K(0), K(1) wait for nothing else)
   issue(krs, s_k0, 0);
@@ -657,15 +697,15 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     unsigned char* const vs[8] = {s_v0, s_v1, s_v2, s_v3, s_v4, s_v5, s_v6, s_v7};
     auto step = [&](auto pt, f32x16& sc, f32x16& sn, int t) __attribute__((always_inline)) {
       constexpr int P = decltype(pt)::value;   // t % 4
+      TAPS_WAIT_VMCNT(8);             // V(2t), V(2t+1), K(2t+2), K(2t+3): this wave's part
+      TAPS_STAGE_BARRIER();           // ... and every other wave's part; and every wave is
+                                      // done with the slots of step t - 1, refilled here
       issue(vrs, vs[(2 * P + 6) & 7], 2 * t + 6);
       issue(vrs, vs[(2 * P + 7) & 7], 2 * t + 7);
       issue(krs, ks[(2 * P + 8) & 7], 2 * t + 8);
       issue(krs, ks[(2 * P + 9) & 7], 2 * t + 9);
-      TAPS_WAIT_VMCNT(12);            // V(2t), V(2t+1), K(2t+2), K(2t+3): this wave's part
-      TAPS_STAGE_BARRIER();           // ... and every other wave's part
       softmax_pv(sc, vs[(2 * P + KGc) & 7], ks[(2 * P + 2 + KGc) & 7], sn,
                  k_begin + (2 * t + KGc) * KT);
-      TAPS_STAGE_BARRIER();           // these slots may be refilled
     };
     TAPS_WAIT_VMCNT(4);               // K(0), K(1)
     TAPS_STAGE_BARRIER();
@@ -962,14 +1002,16 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
   // with events, the launch records the kernel's own start and end (hipExtLaunchKernel)
   if (head_dim == 128) {
     const dim3 block8(512u);
+    const DivMagic dm{DivMagic::make(pl.mtiles), DivMagic::make(pl.splits), DivMagic::make(Hkv),
+                      DivMagic::make(Hq / Hkv)};
     if (ev_begin || ev_end)
       hipExtLaunchKernelGGL(attn_bf16_kernel, grid, block8, 0, s, ev_begin, ev_end, 0, q, k, v,
                             off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2, pl.split_len,
-                            pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML);
+                            pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML, dm);
     else
       attn_bf16_kernel<<<grid, block8, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv,
                                                max_ctx, sl2, pl.split_len, pl.splits,
-                                               pl.mtiles, pairs, mrows_pad, wsO, wsML);
+                                               pl.mtiles, pairs, mrows_pad, wsO, wsML, dm);
   } else {
     if (ev_begin || ev_end)
       hipExtLaunchKernelGGL(attn_bf16_w4_kernel<64>, grid, block, 0, s, ev_begin, ev_end, 0, q,
