@@ -467,6 +467,17 @@ __device__ inline void load_request_scalars(const int32_t* c, const int32_t* nn,
       : "memory");
 }
 
+// two per-request ints in one scalar-memory round trip
+__device__ inline void load_two_scalars(const int32_t* x, const int32_t* y, int& xv, int& yv) {
+  asm volatile(
+      "s_load_dword %0, %2, 0x0\n\t"
+      "s_load_dword %1, %3, 0x0\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&s"(xv), "=&s"(yv)
+      : "s"(x), "s"(y)
+      : "memory");
+}
+
 template <int KG>
 struct GroupTag {
   static constexpr int value = KG;
@@ -748,18 +759,21 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     }
   };
   {
-    float* mine = xslot(wave);
+    // 16-byte LDS accesses: value v of block j at float4 (4 j + v / 4) of this lane
+    float4* mine = (float4*)xslot(wave);
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int db = kg == 0 ? 2 + j : j;     // the blocks the other group finishes
 #pragma unroll
-      for (int v = 0; v < 16; ++v) mine[(j * 16 + v) * 64 + lane] = o[db][v];
+      for (int v4 = 0; v4 < 4; ++v4)
+        mine[(4 * j + v4) * 64 + lane] =
+            make_float4(o[db][4 * v4], o[db][4 * v4 + 1], o[db][4 * v4 + 2], o[db][4 * v4 + 3]);
     }
     s_ml[wave * 64 + lane] = make_float2(m_ref, lsum);
   }
   __syncthreads();
   const int other = wave ^ 4;
-  const float* theirs = xslot(other);
+  const float4* theirs = (const float4*)xslot(other);
   const float2 ml = s_ml[other * 64 + lane];
   const float M = fmaxf(m_ref, ml.x);
   const float a0 = m_ref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref - M);
@@ -787,10 +801,11 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     const int db = kg == 0 ? j : 2 + j;       // the blocks this group finishes
 #pragma unroll
     for (int r4 = 0; r4 < 4; ++r4) {
+      const float4 th = theirs[(4 * j + r4) * 64 + lane];
+      const float tv[4] = {th.x, th.y, th.z, th.w};
       float x[4];
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
-        x[t] = (o[db][4 * r4 + t] * a0 + theirs[(j * 16 + 4 * r4 + t) * 64 + lane] * a1) * inv;
+      for (int t = 0; t < 4; ++t) x[t] = (o[db][4 * r4 + t] * a0 + tv[t] * a1) * inv;
       *(uint2*)(stage + l32 * TROW + 2 * (j * 32 + 8 * r4 + 4 * hl)) = pack_bf16x4(x[0], x[1], x[2], x[3]);
     }
   }
@@ -810,28 +825,37 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
 #endif
 }
 
+// Split combine: grid (row blocks, batch); one thread per 4 head dims of one output row.
 template <int HD>
 __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
     const uint16_t* __restrict__ wsO, const float2* __restrict__ wsML,
-    const int32_t* __restrict__ ctxp, const int32_t* __restrict__ nnp, int B, int N, int Hq,
-    int Hkv, int max_ctx, int split_len, int splits, int mrows_pad, uint16_t* __restrict__ O) {
+    const int32_t* __restrict__ ctxp, const int32_t* __restrict__ nnp, int N, int Hq, int Hkv,
+    int max_ctx, int split_len, int splits, int mrows_pad, DivMagic dm,
+    uint16_t* __restrict__ O) {
   constexpr int TPR = HD / 4;  // threads per output row, 4 values each
   constexpr int RPB = kThreads / TPR;
-  const int row = blockIdx.x * RPB + threadIdx.x / TPR;
+  asm volatile("" ::"s"(wsO), "s"(wsML), "s"(ctxp), "s"(nnp), "s"(N), "s"(Hq), "s"(Hkv),
+               "s"(max_ctx), "s"(split_len), "s"(splits), "s"(mrows_pad), "s"(dm.hk),
+               "s"(dm.g), "s"(O));
+  const int b = blockIdx.y;
+  const int rr = blockIdx.x * RPB + threadIdx.x / TPR;   // (node, query head) of request b
   const int d = (threadIdx.x % TPR) * 4;
-  if (row >= B * N * Hq) return;
-  const int hq = row % Hq, i = (row / Hq) % N, b = row / (Hq * N);
-  const int n = min(max(nnp[b], 0), N);
+  if (rr >= N * Hq) return;
+  const int i = dm.div(rr, Hq, dm.hk), hq = rr - i * Hq;   // dm.hk holds the Hq multiplier
+  int ctx_raw, n_raw;
+  load_two_scalars(ctxp + b, nnp + b, ctx_raw, n_raw);
+  const int n = min(max(n_raw, 0), N);
   if (i >= n) return;
-  const int ctx = min(max(ctxp[b], 0), max_ctx);
+  const int ctx = min(max(ctx_raw, 0), max_ctx);
   const int R = ctx + n;
-  const int G = Hq / Hkv, g = hq / G;
+  const int G = Hq / Hkv, g = dm.div(hq, G, dm.g);
   const int qr = i * G + (hq - g * G);
   const int nspl = (R + split_len - 1) / split_len;
   const size_t base = (size_t)(b * Hkv + g) * splits;
   // each split holds O_s / l_s (bf16) and (m_s, l_s) with m_s in base 2:
   // O = sum_s 2^(m_s - M) l_s (O_s / l_s) / sum_s 2^(m_s - M) l_s.  The loads of up to 16
-  // splits are issued together, then merged with a running maximum.
+  // splits are issued together (clamped split index, masked after), then merged with a
+  // running maximum.
   constexpr int CH = 16;
   float M = -INFINITY, L = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -840,11 +864,13 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
     uint2 ov[CH];
 #pragma unroll
     for (int t = 0; t < CH; ++t) {
-      const bool ok = s0 + t < nspl;
-      const size_t r = (base + s0 + t) * mrows_pad + qr;
-      ml[t] = ok ? wsML[r] : make_float2(-INFINITY, 0.f);
-      ov[t] = ok ? *(const uint2*)(wsO + r * HD + d) : make_uint2(0u, 0u);
+      const size_t r = (base + min(s0 + t, nspl - 1)) * mrows_pad + qr;
+      ml[t] = wsML[r];
+      ov[t] = *(const uint2*)(wsO + r * HD + d);
     }
+#pragma unroll
+    for (int t = 0; t < CH; ++t)
+      if (s0 + t >= nspl) ml[t] = make_float2(-INFINITY, 0.f);
     float Mc = M;
 #pragma unroll
     for (int t = 0; t < CH; ++t) Mc = fmaxf(Mc, ml[t].x);
@@ -1025,17 +1051,20 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int rows_out = batch * budget * Hq;
+  const int rows_req = budget * Hq;   // output rows of one request
+  const DivMagic cm{0u, 0u, DivMagic::make(Hq), DivMagic::make(Hq / Hkv)};
   if (head_dim == 128) {
     const int rpb = kThreads / 32;
-    attn_combine_kernel<128><<<dim3((unsigned)((rows_out + rpb - 1) / rpb)), dim3(kThreads), 0, s>>>(
-        wsO, wsML, ctx, n, batch, budget, Hq, Hkv, max_ctx, pl.split_len, pl.splits, mrows_pad,
-        (uint16_t*)O);
+    attn_combine_kernel<128><<<dim3((unsigned)((rows_req + rpb - 1) / rpb), (unsigned)batch),
+                               dim3(kThreads), 0, s>>>(wsO, wsML, ctx, n, budget, Hq, Hkv, max_ctx,
+                                                       pl.split_len, pl.splits, mrows_pad, cm,
+                                                       (uint16_t*)O);
   } else {
     const int rpb = kThreads / 16;
-    attn_combine_kernel<64><<<dim3((unsigned)((rows_out + rpb - 1) / rpb)), dim3(kThreads), 0, s>>>(
-        wsO, wsML, ctx, n, batch, budget, Hq, Hkv, max_ctx, pl.split_len, pl.splits, mrows_pad,
-        (uint16_t*)O);
+    attn_combine_kernel<64><<<dim3((unsigned)((rows_req + rpb - 1) / rpb), (unsigned)batch),
+                              dim3(kThreads), 0, s>>>(wsO, wsML, ctx, n, budget, Hq, Hkv, max_ctx,
+                                                      pl.split_len, pl.splits, mrows_pad, cm,
+                                                      (uint16_t*)O);
   }
   return hipGetLastError();
 }
