@@ -43,6 +43,17 @@ __device__ inline void wave_fence_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// inclusive prefix sum over the lanes of a wave (DPP row shifts, then row broadcasts)
+__device__ inline int wave_inclusive_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return v;
+}
+
 // the value of lane l (wave-uniform l) in every lane
 __device__ inline uint64_t read_lane_u64(uint64_t v, int l) {
   return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(v >> 32), l) << 32) |
@@ -223,12 +234,20 @@ __device__ inline bool fast_wave_topk_bf16(const void* rowp, int start, int end,
     w[4 * k + 3] = in ? v.w : 0x7FC07FC0u;
   }
   float mx = -INFINITY;
-  bool anynum = false;
 #pragma unroll
   for (int j = 0; j < E / 2; ++j) {
     const float lo = __uint_as_float(w[j] << 16), hi = __uint_as_float(w[j] & 0xFFFF0000u);
     mx = fmaxf(mx, fmaxf(lo, hi));   // ignores NaN
-    anynum |= lo == lo || hi == hi;
+  }
+  // a lane takes part if it holds a non-NaN value; only a lane whose maximum is -inf
+  // (all NaN, or -inf values) needs the element-wise test
+  bool anynum = mx > -INFINITY;
+  if (__ballot(!anynum)) {
+#pragma unroll
+    for (int j = 0; j < E / 2; ++j) {
+      const float lo = __uint_as_float(w[j] << 16), hi = __uint_as_float(w[j] & 0xFFFF0000u);
+      anynum |= lo == lo || hi == hi;
+    }
   }
   if (__popcll(__ballot(anynum)) < K) return false;   // uniform
   // T: the largest 16-bit key with at least K lane maxima >= it, two bits per step
@@ -243,33 +262,45 @@ __device__ inline bool fast_wave_topk_bf16(const void* rowp, int start, int end,
     T = n3 >= K ? c3 : (n2 >= K ? c2 : (n1 >= K ? c1 : T));
   }
   const float tf = __uint_as_float((T & 0x8000u) ? ((T & 0x7FFFu) << 16) : (~(T << 16) & 0xFFFF0000u));
-  // compact the elements >= tf in element order; the ballots of a 16-byte unit are taken
-  // together and the unit is skipped when none of its lanes holds a candidate
-  int total = 0;
+  // candidates (elements >= tf) of this lane as a bit mask over its elements, built with
+  // vector operations only
+  uint32_t mlo = 0u, mhi = 0u;
 #pragma unroll
-  for (int k = 0; k < E / 8; ++k) {
-    uint64_t m[8];
+  for (int j = 0; j < E; ++j) {
+    const uint32_t bits = (j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16);
+    const uint32_t bit = __uint_as_float(bits) >= tf ? 1u : 0u;
+    if (j < 32) mlo |= bit << (j & 31);
+    else mhi |= bit << (j & 31);
+  }
+  const int c = __popc(mlo) + __popc(mhi);
+  const int incl = wave_inclusive_sum(c);
+  const int total = __builtin_amdgcn_readlane(incl, kWave - 1);
+  if (total > kWaveCap) return false;   // uniform; rare (many ties)
+  // compact: lane candidates go to positions incl - c ...; each round stores one
+  // candidate per lane (the lane's lowest remaining element), reading its bits through a
+  // select tree over the lane's words
+  int pos = incl - c;
+  while (__ballot((mlo | mhi) != 0u)) {
+    if ((mlo | mhi) != 0u) {
+      const int j = mlo ? __builtin_ctz(mlo) : 32 + __builtin_ctz(mhi);
+      const int wi = j >> 1;
+      uint32_t sel[E / 2];
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const int j = 8 * k + t;
-      const uint32_t bits = (j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16);
-      m[t] = __ballot(__uint_as_float(bits) >= tf);
-    }
-    if ((m[0] | m[1] | m[2] | m[3] | m[4] | m[5] | m[6] | m[7]) == 0ull) continue;
+      for (int i = 0; i < E / 2; ++i) sel[i] = w[i];
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      if (m[t]) {
-        const int j = 8 * k + t;
-        const uint32_t bits = (j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16);
-        const int pos = total + __builtin_amdgcn_mbcnt_hi((uint32_t)(m[t] >> 32),
-                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)m[t], 0u));
-        const int e = start + (tid + kThreads * k) * 8 + t;
-        if (((m[t] >> lane) & 1ull) && pos < kWaveCap) s_wc[pos] = cand_key(value_key(bits), (uint32_t)e);
-        total += __popcll(m[t]);
+      for (int st = E / 4; st >= 1; st >>= 1) {
+        const bool up = (wi & st) != 0;
+#pragma unroll
+        for (int i = 0; i < st; ++i) sel[i] = up ? sel[i + st] : sel[i];
       }
+      const uint32_t bits = (j & 1) ? (sel[0] & 0xFFFF0000u) : (sel[0] << 16);
+      const int e = start + (tid + kThreads * (j >> 3)) * 8 + (j & 7);
+      s_wc[pos] = cand_key(value_key(bits), (uint32_t)e);
+      ++pos;
+      if (mlo) mlo &= mlo - 1u;
+      else mhi &= mhi - 1u;
     }
   }
-  if (total > kWaveCap) return false;   // uniform; rare (many ties)
   wave_fence_lds();
   // exact ranks among the candidates
   if (total <= kWave) {
