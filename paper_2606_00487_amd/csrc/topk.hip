@@ -60,24 +60,6 @@ __device__ inline uint64_t read_lane_u64(uint64_t v, int l) {
          (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
 }
 
-// after every wave wrote its sorted top-K list at s_top[w*K ...]: wave 0 merges the
-// kWaves lists (at most 64 entries, one per lane) and writes the chunk's K best keys
-__device__ inline void merge_and_store(const uint64_t* s_top, int K, int wave, int lane,
-                                       uint64_t* outp) {
-  static_assert(kWaves * TAPS_MAX_K <= kWave, "one list entry per lane");
-  __syncthreads();
-  if (wave != 0) return;
-  const int tot = kWaves * K;
-  const uint64_t mx = s_top[min(lane, tot - 1)];
-  const uint64_t mine = lane < tot ? mx : 0ull;
-  int rank = 0;
-  for (int t = 0; t < tot; ++t) rank += read_lane_u64(mine, t) > mine ? 1 : 0;
-  if (lane < tot && mine != 0ull && rank < K) outp[rank] = mine;
-  // ranks held by empty entries: write 0 (a chunk with fewer than K elements)
-  const int nonempty = __popcll(__ballot(lane < tot && mine != 0ull));
-  if (lane >= nonempty && lane < K) outp[lane] = 0ull;
-}
-
 template <int DT>
 __device__ inline uint32_t elem_bits(const void* row, int64_t i) {
   if (DT == TAPS_BF16) return (uint32_t)((const uint16_t*)row)[i] << 16;
@@ -212,14 +194,13 @@ __device__ inline void generic_wave_topk(const void* rowp, bool aligned, int sta
 }
 
 // bf16 chunks whose length is a multiple of 8 and whose row is 16-byte aligned: the
-// wave's K best keys into s_wave_top[wave*K ...].  Filtering uses float compares (NaN
+// wave's candidates (every element that can be among its K best) into s_wc[0 .. *n_out).  Filtering uses float compares (NaN
 // fails every compare, -0 equals +0, exactly like the integer keys); exact keys are built
 // only for the few candidates.  Returns false (nothing written) when the wave has fewer
 // than K non-NaN lanes or too many candidates; the generic path then takes the wave.
 template <int E>
 __device__ inline bool fast_wave_topk_bf16(const void* rowp, int start, int end, int tid,
-                                           int lane, int wave, int K, uint64_t* s_wc,
-                                           uint64_t* s_wave_top) {
+                                           int K, uint64_t* s_wc, int* n_out) {
   static_assert(E % 8 == 0, "whole 16-byte units");
   // units past the chunk's end load an in-bounds unit and are replaced by NaN
   uint32_t w[E / 2];
@@ -301,35 +282,32 @@ __device__ inline bool fast_wave_topk_bf16(const void* rowp, int start, int end,
       else mhi &= mhi - 1u;
     }
   }
-  wave_fence_lds();
-  // exact ranks among the candidates
-  if (total <= kWave) {
-    const uint64_t cx = s_wc[min(lane, total - 1)];
-    const uint64_t mine = lane < total ? cx : 0ull;
-    int rank = 0;
-    for (int t = 0; t < total; ++t) rank += read_lane_u64(mine, t) > mine ? 1 : 0;
-    if (lane < total && rank < K) s_wave_top[wave * K + rank] = mine;
-  } else {
-    for (int c0 = 0; c0 < total; c0 += kWave) {
-      const int me = c0 + lane;
-      const uint64_t cx = s_wc[min(me, total - 1)];
-      const uint64_t mine = me < total ? cx : 0ull;
-      int rank = 0;
-      for (int j0 = 0; j0 < total; j0 += 8) {
-        uint64_t cv[8];
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-          const uint64_t x = s_wc[min(j0 + t, total - 1)];
-          cv[t] = j0 + t < total ? x : 0ull;
-        }
-#pragma unroll
-        for (int t = 0; t < 8; ++t) rank += cv[t] > mine ? 1 : 0;
-      }
-      if (me < total && rank < K) s_wave_top[wave * K + rank] = mine;
-    }
-  }
-  for (int r = total + lane; r < K; r += kWave) s_wave_top[wave * K + r] = 0ull;
+  *n_out = total;
   return true;
+}
+
+// The K best of a wave's `total` compacted candidates into s_top[0 .. K), in rank order
+// (zero-padded): the rare path for workgroups with more than 64 candidates in all.
+__device__ inline void rank_wave_candidates(const uint64_t* s_wc, int total, int K, int lane,
+                                            uint64_t* s_top) {
+  for (int c0 = 0; c0 < total; c0 += kWave) {
+    const int me = c0 + lane;
+    const uint64_t cx = s_wc[min(me, total - 1)];
+    const uint64_t mine = me < total ? cx : 0ull;
+    int rank = 0;
+    for (int j0 = 0; j0 < total; j0 += 8) {
+      uint64_t cv[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const uint64_t x = s_wc[min(j0 + t, total - 1)];
+        cv[t] = j0 + t < total ? x : 0ull;
+      }
+#pragma unroll
+      for (int t = 0; t < 8; ++t) rank += cv[t] > mine ? 1 : 0;
+    }
+    if (me < total && rank < K) s_top[rank] = mine;
+  }
+  for (int r = total + lane; r < K; r += kWave) s_top[r] = 0ull;
 }
 
 template <int DT, int E>
@@ -337,8 +315,10 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __rest
                                                               int vocab, int K, int chunk_len,
                                                               int chunks,
                                                               uint64_t* __restrict__ cand) {
-  __shared__ uint64_t s_cand[kWaves][kWaveCap];
-  __shared__ uint64_t s_wave_top[kWaves * TAPS_MAX_K];   // wave w's list at w*K
+  __shared__ uint64_t s_cand[kWaves][kWaveCap];          // fast path: unranked candidates
+  __shared__ uint64_t s_top[kWaves * TAPS_MAX_K];        // ranked lists: wave w's at w*K
+  __shared__ int s_cnt[kWaves];                          // candidates of a fast-path wave, -1
+                                                         // for a ranked list in s_top
 
   const int row = blockIdx.x / chunks;
   const int chunk = blockIdx.x - row * chunks;
@@ -349,12 +329,48 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __rest
   const void* rowp = (const char*)marg + (size_t)row * vocab * es;
   const bool aligned = (((uintptr_t)rowp) & 15) == 0;
 
-  bool done = false;
-  if (DT == TAPS_BF16 && aligned && ((end - start) & 7) == 0 && end - start >= 8)
-    done = fast_wave_topk_bf16<E>(rowp, start, end, tid, lane, wave, K, s_cand[wave], s_wave_top);
-  if (!done) generic_wave_topk<DT, E>(rowp, aligned, start, end, tid, lane, wave, K,
-                                      s_cand[wave], s_wave_top);
-  merge_and_store(s_wave_top, K, wave, lane, cand + ((size_t)row * chunks + chunk) * K);
+  int n = -1;
+  if (DT == TAPS_BF16 && aligned && ((end - start) & 7) == 0 && end - start >= 8) {
+    if (!fast_wave_topk_bf16<E>(rowp, start, end, tid, K, s_cand[wave], &n)) n = -1;
+  }
+  if (n < 0) generic_wave_topk<DT, E>(rowp, aligned, start, end, tid, lane, wave, K, s_cand[wave], s_top);
+  if (lane == 0) s_cnt[wave] = n;
+  __syncthreads();
+  // list sizes: an unranked candidate list, or a ranked list of K in s_top
+  int cnt[kWaves], tot = 0;
+  bool all_ranked = false;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const int c = s_cnt[w];
+    cnt[w] = c < 0 ? K : c;
+    tot += cnt[w];
+  }
+  if (tot > kWave) {   // uniform, rare: every wave first cuts its candidates to its K best
+    if (n >= 0) rank_wave_candidates(s_cand[wave], n, K, lane, s_top + wave * K);
+    __syncthreads();
+    all_ranked = true;
+    tot = kWaves * K;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) cnt[w] = K;
+  }
+  if (wave != 0) return;
+  // wave 0 ranks the (at most 64) entries of the four lists, one per lane
+  int w = 0, off = 0;
+#pragma unroll
+  for (int v = 0; v < kWaves - 1; ++v)
+    if (lane >= off + cnt[w]) { off += cnt[w]; ++w; }
+  const bool in = lane < tot;
+  const int wl = in ? w : 0, il = in ? lane - off : 0;
+  const bool from_top = all_ranked || s_cnt[wl] < 0;
+  const uint64_t cx = from_top ? s_top[wl * K + min(il, K - 1)] : s_cand[wl][il];
+  const uint64_t mine = in ? cx : 0ull;
+  int rank = 0;
+  for (int t = 0; t < tot; ++t) rank += read_lane_u64(mine, t) > mine ? 1 : 0;
+  uint64_t* outp = cand + ((size_t)row * chunks + chunk) * K;
+  if (in && mine != 0ull && rank < K) outp[rank] = mine;
+  // ranks held by empty entries: write 0 (a chunk with fewer than K elements)
+  const int nonempty = __popcll(__ballot(in && mine != 0ull));
+  if (lane >= nonempty && lane < K) outp[lane] = 0ull;
 }
 
 template <int DT>
