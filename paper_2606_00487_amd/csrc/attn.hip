@@ -214,14 +214,15 @@ __global__ __launch_bounds__(256) void attn_bf16_w4_kernel(
     const int pc = (rb - kr * ROWB) / 16;
     ld_off[j] = (uint32_t)kr * rsb + (uint32_t)((pc ^ kswz(kr)) * 16);
   }
-  // stage s of K (or V) into buffer buf; rows past the split's end arrive as zeros
+  // stage s of K (or V) into buffer buf; rows past the split's end arrive as zeros (the
+  // whole offset goes into the per-lane offset, which the buffer range check covers)
   auto issue = [&](__amdgpu_buffer_rsrc_t rs, unsigned char* buf, int s) __attribute__((always_inline)) {
     const uint32_t soff = (uint32_t)(s * STEP) * rsb;
     unsigned char* dst = buf + wave_u * LPH * BLK;
 #pragma unroll
     for (int j = 0; j < LPH; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + j * BLK), 16, ld_off[j],
-                                               soff, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + j * BLK), 16,
+                                               ld_off[j] + soff, 0, 0, 0);
   };
 
   // ---- queries of this lane (B operand of S^T = K Q^T)
@@ -577,9 +578,10 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     const int pc = (rb - kr * ROWB) / 16;
     ld_off = (uint32_t)kr * rsb + (uint32_t)((pc ^ kswz(kr)) * 16);
   }
+  // the stage's offset goes into the per-lane offset, which the buffer range check covers
   auto issue = [&](__amdgpu_buffer_rsrc_t rs, unsigned char* buf, int s) __attribute__((always_inline)) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(buf + wave_u * BLK), 16, ld_off,
-                                             (uint32_t)(s * KT) * rsb, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(buf + wave_u * BLK), 16,
+                                             ld_off + (uint32_t)(s * KT) * rsb, 0, 0, 0);
   };
 
   const bool tree_split = k_end > ctx;
@@ -842,32 +844,37 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
   const int d = (threadIdx.x % TPR) * 4;
   if (rr >= N * Hq) return;
   const int i = dm.div(rr, Hq, dm.hk), hq = rr - i * Hq;   // dm.hk holds the Hq multiplier
+  const int G = Hq / Hkv, g = dm.div(hq, G, dm.g);
+  const int qr = i * G + (hq - g * G);
+  const size_t base = (size_t)(b * Hkv + g) * splits;
+  // each split holds O_s / l_s (bf16) and (m_s, l_s) with m_s in base 2:
+  // O = sum_s 2^(m_s - M) l_s (O_s / l_s) / sum_s 2^(m_s - M) l_s.  The loads of the first
+  // CH splits go out before the request's sizes are known (their addresses do not depend on
+  // them; splits past the request's keys are masked once the sizes have arrived), then
+  // groups of up to CH splits are merged with a running maximum.
+  constexpr int CH = 16;
+  float2 ml[CH];
+  uint2 ov[CH];
+  auto load_group = [&](int s0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int t = 0; t < CH; ++t) {
+      const size_t r = (base + min(s0 + t, splits - 1)) * mrows_pad + qr;
+      ml[t] = wsML[r];
+      ov[t] = *(const uint2*)(wsO + r * HD + d);
+    }
+  };
+  load_group(0);
   int ctx_raw, n_raw;
   load_two_scalars(ctxp + b, nnp + b, ctx_raw, n_raw);
   const int n = min(max(n_raw, 0), N);
   if (i >= n) return;
   const int ctx = min(max(ctx_raw, 0), max_ctx);
   const int R = ctx + n;
-  const int G = Hq / Hkv, g = dm.div(hq, G, dm.g);
-  const int qr = i * G + (hq - g * G);
-  const int nspl = (R + split_len - 1) / split_len;
-  const size_t base = (size_t)(b * Hkv + g) * splits;
-  // each split holds O_s / l_s (bf16) and (m_s, l_s) with m_s in base 2:
-  // O = sum_s 2^(m_s - M) l_s (O_s / l_s) / sum_s 2^(m_s - M) l_s.  The loads of up to 16
-  // splits are issued together (clamped split index, masked after), then merged with a
-  // running maximum.
-  constexpr int CH = 16;
+  const int nspl = min((R + split_len - 1) / split_len, splits);
   float M = -INFINITY, L = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int s0 = 0; s0 < nspl; s0 += CH) {
-    float2 ml[CH];
-    uint2 ov[CH];
-#pragma unroll
-    for (int t = 0; t < CH; ++t) {
-      const size_t r = (base + min(s0 + t, nspl - 1)) * mrows_pad + qr;
-      ml[t] = wsML[r];
-      ov[t] = *(const uint2*)(wsO + r * HD + d);
-    }
+    if (s0 > 0) load_group(s0);
 #pragma unroll
     for (int t = 0; t < CH; ++t)
       if (s0 + t >= nspl) ml[t] = make_float2(-INFINITY, 0.f);
