@@ -45,6 +45,8 @@ taps_status attn_check(int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv, i
   if ((int64_t)max_ctx + budget > (int64_t)1 << 30) return TAPS_ERR_UNSUPPORTED;
   if ((int64_t)batch * Hkv > 65535 || (int64_t)budget * Hq / Hkv > (int64_t)1 << 20)
     return TAPS_ERR_UNSUPPORTED;
+  // one request's queries must span < 2^31 bytes
+  if ((int64_t)budget * Hq * hd * 2 >= ((int64_t)1 << 31)) return TAPS_ERR_UNSUPPORTED;
   // one split's K or V rows, with the kernel's look-ahead, must span < 2^31 bytes
   if ((int64_t)Hkv * hd * 2 * 6 * 64 >= ((int64_t)1 << 31)) return TAPS_ERR_UNSUPPORTED;
   return TAPS_OK;

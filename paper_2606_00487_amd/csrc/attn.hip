@@ -110,6 +110,54 @@ typedef __attribute__((address_space(3))) void lds_void;
 // direct loads; the memory clobber keeps the compiler from moving LDS accesses across it
 #define TAPS_STAGE_BARRIER() asm volatile("s_barrier" ::: "memory")
 
+// workgroup barrier after LDS writes: waits for this wave's LDS operations only, so the
+// direct loads in flight stay in flight (__syncthreads would also wait for them)
+#define TAPS_LDS_BARRIER()                                                   \
+  do {                                                                       \
+    __builtin_amdgcn_s_waitcnt(0xF | (7 << 4) | (0 << 8) | (3 << 14));       \
+    asm volatile("s_barrier" ::: "memory");                                  \
+  } while (0)
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer resource over `bytes` bytes from p (raw buffer, no stride): accesses at offsets
+// >= bytes read as zeros without touching memory.
+__device__ inline i32x4 buffer_rsrc(const void* p, uint32_t bytes) {
+  const uint64_t a = (uint64_t)p;
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+  r[3] = 0x00020000;
+  return r;
+}
+
+// 16 bytes per lane from buffer offset `off` straight into LDS at dst + 16 * lane, issued
+// as inline assembly so that the compiler does not track it.  Its own bookkeeping of
+// direct-to-LDS loads cannot tell the sixteen ring slots apart and would make every LDS
+// read wait for all but the newest loads in flight, which cuts the look-ahead of the ring
+// to one step.  Callers order every global read of the kernel with explicit vmcnt waits.
+// m0 carries the LDS address; nothing else in the kernels that call this uses m0.  A
+// direct-to-LDS load must not follow the scalar write of m0 immediately (one wait state).
+__device__ inline void load_lds16(const i32x4& rs, unsigned char* dst, uint32_t off) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)dst);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(m0v), "v"(off), "s"(rs) : "memory");
+}
+
+// 4 bytes per lane into LDS at dst + 4 * lane (same conventions as load_lds16)
+__device__ inline void load_lds4(const i32x4& rs, unsigned char* dst, uint32_t off) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)dst);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               :: "s"(m0v), "v"(off), "s"(rs) : "memory");
+}
+
+// permutation of all four bits of a row's 16-byte chunk index (the 16 rows a 16-byte
+// per-lane read touches at once land on distinct chunk positions, i.e. on all 64 banks)
+__device__ inline int kswz16(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
@@ -533,20 +581,36 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
   const int l32 = lane & 31, hl = lane >> 5;
   const int row0 = mt * MT;
 
-  // ---- queries of this lane (B operand of S^T = K Q^T) and the parent pointer of node
-  // tid: their addresses do not depend on the request's sizes, so they go out first
-  bf16x8 q[NKK];
+  // ---- the query tile and the parent pointers go straight into LDS first (their
+  // addresses do not depend on the request's sizes): V slots 4-7 are free until after
+  // the first S.  Every global read of this kernel is such a direct load, issued as inline
+  // assembly and ordered by explicit vmcnt waits.  Tile row r (query row row0 + r: node
+  // (row0 + r) / G, query head g * G + (row0 + r) % G) is in V slot 4 + r / 32, its 16-byte
+  // chunks XOR-permuted by kswz16(r % 32); wave (rg, kg) loads rows rg * 32 + kg * 16 ..
+  // + 15, four rows (1 KB) per load.
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int rg_u = wave_u & 3, kg_u = wave_u >> 2;
+  unsigned char* const qslot = rg_u == 0 ? s_v4 : rg_u == 1 ? s_v5 : rg_u == 2 ? s_v6 : s_v7;
+  {
+    const i32x4 qrs = buffer_rsrc(Q + (size_t)b * N * Hq * HD, (uint32_t)((size_t)N * Hq * HD * 2));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = kg_u * 16 + 4 * j + (lane >> 4);   // row within the slot
+      const int qr = min(row0 + rg_u * 32 + r, N * G - 1);
+      const int node = dm.div(qr, G, dm.g);
+      const uint32_t off = (uint32_t)(node * Hq + g * G + (qr - node * G)) * (HD * 2) +
+                           16u * (uint32_t)((lane & 15) ^ kswz16(r));
+      load_lds16(qrs, qslot + (kg_u * 16 + 4 * j) * ROWB, off);
+    }
+    if (wave_u < TAPS_MAX_BUDGET / 64)
+      load_lds4(buffer_rsrc(parentp + (size_t)b * N, (uint32_t)N * 4),
+                (unsigned char*)s_par + 256 * wave_u, (uint32_t)(64 * wave_u + lane) * 4);
+  }
   int qnode;
   {
-    int qr = row0 + rg * 32 + l32;
-    qr = min(qr, N * G - 1);
-    const int node = dm.div(qr, G, dm.g), hq = g * G + (qr - node * G);
-    qnode = node;
-    const uint16_t* qp = Q + (((size_t)b * N + node) * Hq + hq) * HD;
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) q[kk] = *(const bf16x8*)(qp + kk * 16 + hl * 8);
+    const int qr = min(row0 + rg * 32 + l32, N * G - 1);
+    qnode = dm.div(qr, G, dm.g);
   }
-  const int par_raw = parentp[(size_t)b * N + min(tid, N - 1)];
 
   int ctx_raw, n_raw;
   int64_t kv0;
@@ -556,7 +620,10 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
   const int R = ctx + n;
   const int k_begin = split * split_len;
   const int k_end = min(R, k_begin + split_len);
-  if (k_begin >= k_end || row0 >= n * G) return;
+  if (k_begin >= k_end || row0 >= n * G) {
+    TAPS_WAIT_VMCNT(0);   // the direct loads into LDS land before the LDS is released
+    return;
+  }
   const size_t row_stride = (size_t)Hkv * HD;
   const uint32_t rsb = (uint32_t)(row_stride * 2);
   const int nst = (k_end - k_begin + KT - 1) / KT;   // 32-key stages of this split
@@ -564,13 +631,10 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
   // buffer resources over this split's K and V rows of head g: rows past the split's end
   // read as zeros without touching memory (the host keeps the range below 2^31 bytes)
   const size_t seg = ((size_t)kv0 + k_begin) * row_stride + (size_t)g * HD;
-  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(Kc + seg), (short)0, (int)((uint32_t)(k_end - k_begin) * rsb), 0x00020000);
-  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(Vc + seg), (short)0, (int)((uint32_t)(k_end - k_begin) * rsb), 0x00020000);
+  const i32x4 krs = buffer_rsrc(Kc + seg, (uint32_t)(k_end - k_begin) * rsb);
+  const i32x4 vrs = buffer_rsrc(Vc + seg, (uint32_t)(k_end - k_begin) * rsb);
 
   // ---- direct loads: wave w fills block w (rows 4w .. 4w + 3) of every slot
-  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   uint32_t ld_off;
   {
     const int rb = wave_u * BLK + lane * 16;
@@ -579,31 +643,32 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     ld_off = (uint32_t)kr * rsb + (uint32_t)((pc ^ kswz(kr)) * 16);
   }
   // the stage's offset goes into the per-lane offset, which the buffer range check covers
-  auto issue = [&](__amdgpu_buffer_rsrc_t rs, unsigned char* buf, int s) __attribute__((always_inline)) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(buf + wave_u * BLK), 16,
-                                             ld_off + (uint32_t)(s * KT) * rsb, 0, 0, 0);
+  auto issue = [&](const i32x4& rs, unsigned char* buf, int s) __attribute__((always_inline)) {
+    load_lds16(rs, buf + wave_u * BLK, ld_off + (uint32_t)(s * KT) * rsb);
   };
 
   const bool tree_split = k_end > ctx;
-  const int my_par = tree_split && tid < n ? par_raw : -1;
   // K(0) K(1) and the loads of step -3 [V(2t+6) V(2t+7) K(2t+8) K(2t+9)] now; those of
   // steps -2 and -1 after the first S (so its reads of K(0), K(1) wait for nothing else)
   issue(krs, s_k0, 0);
   issue(krs, s_k1, 1);
   issue(vrs, s_v0, 0); issue(vrs, s_v1, 1); issue(krs, s_k2, 2); issue(krs, s_k3, 3);
-  TAPS_WAIT_VMCNT(6);   // queries and parents
+  TAPS_WAIT_VMCNT(6);   // queries and parents: this wave's part
+  TAPS_LDS_BARRIER();   // ... and every other wave's part (the K/V loads stay in flight)
+  bf16x8 q[NKK];        // queries of this lane: B operand of S^T = K Q^T
+#pragma unroll
+  for (int kk = 0; kk < NKK; ++kk)
+    q[kk] = *(const bf16x8*)(qslot + l32 * ROWB + 16 * ((2 * kk + hl) ^ kswz16(l32)));
 
   // ---- ancestor-or-self masks of the tree rows, in LDS (read only by masked tiles)
   if (tree_split) {
-    if (tid < n) s_par[tid] = my_par;
-    __syncthreads();
     for (int i = tid; i < n; i += NT) {
       uint64_t a[4];
       ancestor_mask(i, [&](int j) { return s_par[j]; }, a);
 #pragma unroll
       for (int w = 0; w < 4; ++w) s_anc[i][w] = a[w];
     }
-    __syncthreads();
+    TAPS_LDS_BARRIER();
   }
 
   // ---- per-lane LDS read offsets
@@ -721,7 +786,7 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
                  k_begin + (2 * t + KGc) * KT);
     };
     TAPS_WAIT_VMCNT(4);               // K(0), K(1)
-    TAPS_STAGE_BARRIER();
+    TAPS_LDS_BARRIER();               // every wave has its queries: V slots 4-7 refill below
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) s_mfma(ks[KGc], kk, sA);
     issue(vrs, s_v2, 2); issue(vrs, s_v3, 3); issue(krs, s_k4, 4); issue(krs, s_k5, 5);
