@@ -2,9 +2,11 @@
 //
 // Phase A  merge the per-chunk top-K lists of each row into the row's top-K (one wave
 //          per row): a threshold at the K-th largest chunk head keeps only the few
-//          entries that can still be in the top-K; those are ranked exactly.
-// Phase B  sibling-softmax edge probabilities c[i][r] (Eq. 1) in IEEE fp64 and the
-//          utility denominators lambda1 + lambda2*d (Eq. 3).
+//          entries that can still be in the top-K (more than 64 of them are first cut
+//          to the K largest by a descent over the key bits); those are ranked exactly.
+//          The same wave then computes the row's sibling-softmax edge probabilities
+//          c[i][r] (Eq. 1) in IEEE fp64.  The utility denominators lambda1 + lambda2*d
+//          (Eq. 3) are set alongside.
 // Phase C  the selected set of Alg. 1.  Because q_cond <= 1 and the denominators do not
 //          decrease with depth, a child never beats its parent (ties go to the shallower
 //          node), so Alg. 1 adds exactly one node per iteration and its result is the
@@ -175,6 +177,7 @@ __device__ inline uint32_t wave_min_u32(uint32_t v) {
 // ------------------------------------------------------------------ shared memory layout
 struct PhaseA {
   uint64_t rowc[kWavesA][kRowCap];
+  uint64_t heads[kWavesA][kWave];
 };
 struct Level {                 // expanded trie nodes, stored depth by depth
   double q[kCap];
@@ -394,10 +397,18 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
       }
       const uint64_t hx = rc[(size_t)min(lane, chunks - 1) * K];
       const uint64_t head = lane < chunks ? hx : 0ull;
-      // heads that beat this lane's head, read across lanes (no LDS traffic: sixteen
-      // waves share the LDS pipe here)
+      // heads that beat this lane's head, read back from LDS eight at a time (every lane
+      // reads the same address; the heads of lanes >= chunks are 0 and beat nothing)
+      A.heads[wave][lane] = head;
+      wave_fence();
       int beat = 0;
-      for (int t = 0; t < chunks; ++t) beat += read_lane_u64(head, t) > head ? 1 : 0;
+      for (int t0 = 0; t0 < chunks; t0 += 8) {
+        uint64_t hv[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) hv[t] = A.heads[wave][t0 + t];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) beat += hv[t] > head ? 1 : 0;
+      }
       const int nheads = __popcll(__ballot(head != 0ull));
       uint64_t T = 1ull;  // fewer non-empty chunks than K: every entry is a candidate
       if (nheads >= K) {
@@ -415,28 +426,60 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
       }
       total = total < kRowCap ? total : kRowCap;
       wave_fence();
-      // exact ranks; the entry of rank r < K is the row's r-th candidate
       const size_t orow = ((size_t)b * D + i) * K;
-      for (int c0 = 0; c0 < total; c0 += kWave) {
-        const int me = c0 + lane;
-        const uint64_t mx = A.rowc[wave][min(me, kRowCap - 1)];
-        const uint64_t mine = me < total ? mx : 0ull;
-        int rank = 0;
-        if (total <= kWave) {   // every candidate sits in a lane: compare across lanes
-          for (int t = 0; t < total; ++t) rank += read_lane_u64(mine, t) > mine ? 1 : 0;
-        } else {
-          for (int j0 = 0; j0 < total; j0 += 16) {
-            uint64_t rv[16];
+      // More than a wave's worth of candidates (flat rows): the K-th largest of them, T2,
+      // by a descent over the key bits, two bits per step; the K entries >= T2 (keys are
+      // unique) replace the candidate list.
+      if (total > kWave) {   // uniform
+        constexpr int JC = kRowCap / kWave;
+        uint64_t cv[JC];
 #pragma unroll
-            for (int t = 0; t < 16; ++t) {
-              const uint64_t x = A.rowc[wave][min(j0 + t, kRowCap - 1)];
-              rv[t] = j0 + t < total ? x : 0ull;
-            }
-#pragma unroll
-            for (int t = 0; t < 16; ++t) rank += rv[t] > mine ? 1 : 0;
-          }
+        for (int j = 0; j < JC; ++j) {
+          const int e = j * kWave + lane;
+          const uint64_t x = A.rowc[wave][e];
+          cv[j] = e < total ? x : 0ull;
         }
-        if (me < total && rank < K) {
+        uint64_t T2 = 0ull;
+        for (int bit = 62; bit >= 0; bit -= 2) {
+          const uint64_t c1 = T2 | (1ull << bit), c2 = T2 | (2ull << bit), c3 = T2 | (3ull << bit);
+          int n1 = 0, n2 = 0, n3 = 0;
+#pragma unroll
+          for (int j = 0; j < JC; ++j) {
+            n1 += __popcll(__ballot(cv[j] >= c1));
+            n2 += __popcll(__ballot(cv[j] >= c2));
+            n3 += __popcll(__ballot(cv[j] >= c3));
+          }
+          T2 = n3 >= K ? c3 : (n2 >= K ? c2 : (n1 >= K ? c1 : T2));
+        }
+        wave_fence();   // every lane has read the list before it is overwritten
+        int kept = 0;
+#pragma unroll
+        for (int j = 0; j < JC; ++j) {
+          const uint64_t m = __ballot(cv[j] >= T2);
+          const int pos = kept + lanes_below(m);
+          if (cv[j] >= T2) A.rowc[wave][pos] = cv[j];
+          kept += __popcll(m);
+        }
+        total = kept;   // == K
+        wave_fence();
+      }
+      // exact ranks of the (at most 64) candidates, one per lane, read back from LDS
+      // eight at a time; the entry of rank r < K is the row's r-th candidate
+      {
+        const uint64_t mx = A.rowc[wave][lane];
+        const uint64_t mine = lane < total ? mx : 0ull;
+        int rank = 0;
+        for (int t0 = 0; t0 < total; t0 += 8) {
+          uint64_t rv[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) {
+            const uint64_t x = A.rowc[wave][t0 + t];
+            rv[t] = t0 + t < total ? x : 0ull;
+          }
+#pragma unroll
+          for (int t = 0; t < 8; ++t) rank += rv[t] > mine ? 1 : 0;
+        }
+        if (lane < total && rank < K) {
           sh.top[i][rank] = mine;
           o_tidx[orow + rank] = (int32_t)cand_index(mine);
           if (o_tval) o_tval[orow + rank] = value_from_key((uint32_t)(mine >> 32));
@@ -448,43 +491,40 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
         if (o_tval) o_tval[orow + r] = value_from_key(0u);
       }
       wave_fence();
+      // Eq. 1 for this row (lane r < K): e_r, then c_r = e_r / Z with Z summed in rank order
+      if (lane < K) {
+        const uint64_t k = sh.top[i][lane];
+        const double x = k ? (double)value_from_key((uint32_t)(k >> 32)) : (double)__uint_as_float(0x7FC00000u);
+        double e;
+        if (kind == TAPS_LOGITS) {
+          const uint64_t k0 = sh.top[i][0];
+          const double x0 = k0 ? (double)value_from_key((uint32_t)(k0 >> 32)) : x;
+          e = spec_exp(beta * (x - x0));
+        } else {
+          e = x > 0.0 ? x : 0.0;
+        }
+        sh.e[i][lane] = e;
+      }
+      wave_fence();
+      if (lane < K) {
+        double Z = 0.0;
+        for (int j = 0; j < K; ++j) Z = Z + sh.e[i][j];
+        const bool ok = Z > 0.0 && Z <= 1.7976931348623157e308;
+        sh.c[i][lane] = ok ? sh.e[i][lane] / Z : 0.0;
+      }
     };
     for (int i = wave; i < D; i += kWavesA) {
       if (CK <= 4 * kWave) merge_row(IntC<4>(), i);
       else merge_row(IntC<16>(), i);
     }
   }
+  // Eq. 3 denominators lambda1 + lambda2 * depth
+  if (tid <= D) sh.den[tid] = lambda1 + lambda2 * (double)tid;
   __syncthreads();
   // The selection proper runs on the first four waves.  The other waves end here; a
   // workgroup barrier waits only for the waves that have not ended, so the barriers
   // below synchronize the remaining four.
   if (wave >= kWaves) return;
-
-  // ---------------- Phase B: Eq. 1 edge probabilities, Eq. 3 denominators
-  for (int it = tid; it < D * K; it += kThreads) {
-    const int i = it / K, r = it - (it / K) * K;
-    const uint64_t k = sh.top[i][r];
-    const double x = k ? (double)value_from_key((uint32_t)(k >> 32)) : (double)__uint_as_float(0x7FC00000u);
-    double e;
-    if (kind == TAPS_LOGITS) {
-      const uint64_t k0 = sh.top[i][0];
-      const double x0 = k0 ? (double)value_from_key((uint32_t)(k0 >> 32)) : x;
-      e = spec_exp(beta * (x - x0));
-    } else {
-      e = x > 0.0 ? x : 0.0;
-    }
-    sh.e[i][r] = e;
-  }
-  if (tid <= D) sh.den[tid] = lambda1 + lambda2 * (double)tid;
-  __syncthreads();
-  for (int it = tid; it < D * K; it += kThreads) {
-    const int i = it / K, r = it - (it / K) * K;
-    double Z = 0.0;
-    for (int j = 0; j < K; ++j) Z = Z + sh.e[i][j];
-    const bool ok = Z > 0.0 && Z <= 1.7976931348623157e308;
-    sh.c[i][r] = ok ? sh.e[i][r] / Z : 0.0;
-  }
-  __syncthreads();
 
   // ---------------- Phase C: depth-by-depth expansion with a safe pruning bin
   // floor(n / K) for 0 <= n < 2^20 as a high multiply by ceil(2^32 / K): the error term

@@ -54,12 +54,6 @@ __device__ inline int wave_inclusive_sum(int v) {
   return v;
 }
 
-// the value of lane l (wave-uniform l) in every lane
-__device__ inline uint64_t read_lane_u64(uint64_t v, int l) {
-  return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(v >> 32), l) << 32) |
-         (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
-}
-
 template <int DT>
 __device__ inline uint32_t elem_bits(const void* row, int64_t i) {
   if (DT == TAPS_BF16) return (uint32_t)((const uint16_t*)row)[i] << 16;
@@ -319,6 +313,8 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __rest
   __shared__ uint64_t s_top[kWaves * TAPS_MAX_K];        // ranked lists: wave w's at w*K
   __shared__ int s_cnt[kWaves];                          // candidates of a fast-path wave, -1
                                                          // for a ranked list in s_top
+  __shared__ uint64_t s_all[kWave];                      // the workgroup's candidates, one per
+                                                         // lane of wave 0
 
   const int row = blockIdx.x / chunks;
   const int chunk = blockIdx.x - row * chunks;
@@ -364,8 +360,18 @@ __global__ __launch_bounds__(kThreads) void topk_chunk_kernel(const void* __rest
   const bool from_top = all_ranked || s_cnt[wl] < 0;
   const uint64_t cx = from_top ? s_top[wl * K + min(il, K - 1)] : s_cand[wl][il];
   const uint64_t mine = in ? cx : 0ull;
+  // rank = candidates that beat this one, read back from LDS eight at a time (every lane
+  // reads the same address; entries past tot are 0 and beat nothing)
+  s_all[lane] = mine;
+  wave_fence_lds();
   int rank = 0;
-  for (int t = 0; t < tot; ++t) rank += read_lane_u64(mine, t) > mine ? 1 : 0;
+  for (int t0 = 0; t0 < tot; t0 += 8) {
+    uint64_t v[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) v[t] = s_all[t0 + t];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) rank += v[t] > mine ? 1 : 0;
+  }
   uint64_t* outp = cand + ((size_t)row * chunks + chunk) * K;
   if (in && mine != 0ull && rank < K) outp[rank] = mine;
   // ranks held by empty entries: write 0 (a chunk with fewer than K elements)
