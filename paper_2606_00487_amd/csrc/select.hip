@@ -108,6 +108,27 @@ __device__ inline int wave_inclusive_sum(int v) {
   return v;
 }
 
+// bitwise OR / AND over the lanes of a wave (DPP row shifts, then row broadcasts; lanes
+// without a source keep the identity), read from the last lane
+__device__ inline uint32_t wave_or_u32(uint32_t v) {
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false);
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false);
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, kWave - 1);
+}
+__device__ inline uint32_t wave_and_u32(uint32_t v) {
+  v &= (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x111, 0xf, 0xf, false);
+  v &= (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x112, 0xf, 0xf, false);
+  v &= (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x114, 0xf, 0xf, false);
+  v &= (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x118, 0xf, 0xf, false);
+  v &= (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x142, 0xa, 0xf, false);
+  v &= (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x143, 0xc, 0xf, false);
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, kWave - 1);
+}
+
 // inclusive prefix sum within each row of 16 lanes
 __device__ inline int row_inclusive_sum(int v) {
   v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
@@ -428,28 +449,36 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
       wave_fence();
       const size_t orow = ((size_t)b * D + i) * K;
       // More than a wave's worth of candidates (flat rows): the K-th largest of them, T2,
-      // by a descent over the key bits, two bits per step; the K entries >= T2 (keys are
-      // unique) replace the candidate list.
+      // by a descent over the key bits in which the candidates differ (the others are
+      // common to all of them, so T2 has them too); the K entries >= T2 (keys are unique)
+      // replace the candidate list.
       if (total > kWave) {   // uniform
         constexpr int JC = kRowCap / kWave;
         uint64_t cv[JC];
+        uint64_t lor = 0ull, land = ~0ull;   // over this lane's candidates
 #pragma unroll
         for (int j = 0; j < JC; ++j) {
           const int e = j * kWave + lane;
           const uint64_t x = A.rowc[wave][e];
           cv[j] = e < total ? x : 0ull;
+          lor |= e < total ? x : 0ull;
+          land &= e < total ? x : ~0ull;
         }
-        uint64_t T2 = 0ull;
-        for (int bit = 62; bit >= 0; bit -= 2) {
-          const uint64_t c1 = T2 | (1ull << bit), c2 = T2 | (2ull << bit), c3 = T2 | (3ull << bit);
-          int n1 = 0, n2 = 0, n3 = 0;
+        const uint64_t gor = ((uint64_t)wave_or_u32((uint32_t)(lor >> 32)) << 32) |
+                             wave_or_u32((uint32_t)lor);
+        const uint64_t gand = ((uint64_t)wave_and_u32((uint32_t)(land >> 32)) << 32) |
+                              wave_and_u32((uint32_t)land);
+        const uint64_t diff = gor ^ gand;
+        uint64_t T2 = gand & ~diff;
+        for (uint64_t m = diff; m != 0ull;) {   // uniform
+          const int bit = 63 - __clzll((long long)m);
+          m &= ~(1ull << bit);
+          const uint64_t c = T2 | (1ull << bit);
+          int nc = 0;
 #pragma unroll
-          for (int j = 0; j < JC; ++j) {
-            n1 += __popcll(__ballot(cv[j] >= c1));
-            n2 += __popcll(__ballot(cv[j] >= c2));
-            n3 += __popcll(__ballot(cv[j] >= c3));
-          }
-          T2 = n3 >= K ? c3 : (n2 >= K ? c2 : (n1 >= K ? c1 : T2));
+          for (int j = 0; j < JC; ++j)
+            if (j * kWave < total) nc += __popcll(__ballot(cv[j] >= c));
+          if (nc >= K) T2 = c;
         }
         wave_fence();   // every lane has read the list before it is overwritten
         int kept = 0;
