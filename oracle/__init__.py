@@ -11,6 +11,7 @@ Layout
                 utility (Eq. 3) and the greedy prefix-closed selection (Alg. 1)
   attention.py  tree-masked verification attention (Sec. 4.1, Sec. 4.3)
   walk.py       greedy acceptance walk (Sec. 1; Limitations, temperature 0)
+  commit.py     KV commit of the accepted path and the emitted tokens (Sec. 1)
 
 Pins (what fixes each part without trusting this code) live in
 tests/test_oracle_*.py.  Parity of the oracle against the paper's own numbers
@@ -23,3 +24,4 @@ from .select import (  # noqa: F401
 )
 from .attention import ancestor_sets, tree_attention  # noqa: F401
 from .walk import accept_walk  # noqa: F401
+from .commit import committed_path, kv_commit  # noqa: F401
