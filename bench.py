@@ -13,7 +13,9 @@ graph per input set (``--eager`` launches them directly).
 Prints one JSON line.  ``value`` is rounds/s (requests x steps per second);
 ``roofline`` covers the dominant kernel (the main tree-attention kernel), timed
 with HIP events around that kernel alone in a separate pass of the same
-launches; ``cpu_baseline`` times the CPU oracle on a bounded sample.
+launches; ``cpu_baseline`` times the CPU oracle on a bounded sample.  The
+round's state update (kv_commit of the accepted path) is not part of the step;
+``stages_us.kv_commit`` and ``kv_commit`` report it from its own timed pass.
 """
 from __future__ import annotations
 
@@ -97,6 +99,17 @@ def algorithmic_bytes(cfg, ctx_len, n_nodes):
     return marg, kv, qo
 
 
+def commit_moved_bytes(cfg, path, path_len):
+    """Algorithmic bytes of one kv_commit: every committed path entry that is not already at
+    its target row is read and written once, in K and in V."""
+    row = cfg.Hkv * cfg.head_dim * (2 if cfg.dtype == 0 else 4)
+    moved = 0
+    for b in range(cfg.batch):
+        m = int(path_len[b])
+        moved += sum(1 for j in range(1, m) if int(path[b][j]) != j)
+    return moved * row * 2 * 2
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -137,6 +150,8 @@ def main():
     att = taps.TreeAttention(cfg.batch, cfg.budget, cfg.Hq, cfg.Hkv, cfg.head_dim, max_ctx,
                              dtype=cfg.dtype, scale=cfg.scale)
     walk = taps.AcceptWalk(cfg.batch, cfg.budget, cfg.block)
+    commit = taps.KVCommit(cfg.batch, cfg.budget, cfg.block, cfg.Hkv, cfg.head_dim, max_ctx,
+                           dtype=cfg.dtype)
     sets = []
     for k in range(nsets):
         inp = inp0 if k == 0 else gen_round(cfg, seed=inp0.seed + k)
@@ -217,6 +232,33 @@ def main():
             walk(s["tree"], s["tgt"])
             e[5].record(stream)
         torch.cuda.synchronize()
+
+        # ---------------- the round's state update (kv_commit), timed on its own from a HIP
+        # graph of back-to-back calls per input set (eager events would include the host's
+        # launch overhead).  It moves tree rows of the cache in place and does not write
+        # ctx_len, so repeated calls do the same work; it runs after everything else.
+        commit_bytes, commit_us = [], []
+        CR = 20
+        for s in sets:
+            walk(s["tree"], s["tgt"])
+            torch.cuda.synchronize()
+            commit_bytes.append(commit_moved_bytes(cfg, walk.path.cpu().numpy(),
+                                                   walk.path_len.cpu().numpy()))
+            gc = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gc, stream=stream):
+                for _ in range(CR):
+                    commit(s["K"], s["V"], s["off"], s["ctx"], s["tree"], walk.path,
+                           walk.path_len, walk.bonus)
+            gc.replay()
+            c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            c0.record(stream)
+            for _ in range(3):
+                gc.replay()
+            c1.record(stream)
+            torch.cuda.synchronize()
+            commit_us.append(c0.elapsed_time(c1) * 1e3 / (3 * CR))
+    t_commit = float(np.mean(commit_us))
+    commit_b = float(np.mean(commit_bytes))
     t_sel = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e3
     t_attn = float(np.mean([e[2].elapsed_time(e[3]) for e in ev])) * 1e3
     t_attn_call = float(np.mean([e[1].elapsed_time(e[4]) for e in ev])) * 1e3
@@ -257,7 +299,11 @@ def main():
         "hbm_gbs_round": round(round_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "round_bytes": int(round_bytes),
         "stages_us": {"select": round(t_sel, 2), "attn_main_kernel": round(t_attn, 2),
-                      "attn_call": round(t_attn_call, 2), "walk": round(t_walk, 2)},
+                      "attn_call": round(t_attn_call, 2), "walk": round(t_walk, 2),
+                      "kv_commit": round(t_commit, 2)},
+        "kv_commit": {"bytes_per_launch": int(commit_b),
+                      "achieved_gbs": round(commit_b / (t_commit * 1e-6) / 1e9, 1),
+                      "avg_launch_us": round(t_commit, 3)},
         "roofline": {
             "bound": "hbm",
             "kernel": "attn_bf16_kernel" if bf else "attn_f32_kernel",

@@ -10,6 +10,8 @@
  *                     Sec. 4.3: verification needs a connected subtree at the root).
  *   accept_walk       greedy (temperature 0) acceptance of the longest matching root
  *                     path (Sec. 1: one prefix path is committed per round; Limitations).
+ *   kv_commit         the round's state update: the accepted path's tree K/V rows move
+ *                     to the rows right after the context, and the emitted tokens.
  *
  * Conventions shared by every call:
  *   - Pointers are DEVICE memory owned by the caller unless marked [host].
@@ -173,6 +175,39 @@ taps_status tree_verify_attn_timed(const void *Q_tree, const void *K_cache, cons
 taps_status accept_walk(const taps_tree *tree, int32_t batch, int32_t budget,
                         int32_t block, const int32_t *target_tokens, int32_t *path,
                         int32_t *path_len, int32_t *bonus, hipStream_t stream);
+
+/* KV commit of the accepted path: the round's state update after accept_walk (Sec. 1:
+ * each decoding round commits only one prefix path; the paper leaves the update itself
+ * to the serving system).
+ *   K_cache,
+ *   V_cache      [rows][Hkv][head_dim] in the layout of tree_verify_attn, updated in place:
+ *                for request b the rows of the m committed path nodes, kv_offset[b] +
+ *                ctx + path[b][j], move to rows kv_offset[b] + ctx + j (j = 0 .. m-1, the
+ *                root's row stays); no other row is written.  ctx = ctx_len[b] clamped to
+ *                [0, max_ctx].
+ *   kv_offset,
+ *   ctx_len      as for tree_verify_attn (not written)
+ *   tree         [host] struct; token is read ([batch][budget], node tokens)
+ *   path,
+ *   path_len,
+ *   bonus        accept_walk's outputs.  The committed path is the root followed by the
+ *                entries path[b][1 .. path_len[b]-1] up to (not including) the first one
+ *                that is not larger than the previous entry or not below budget; m is its
+ *                length (1 .. block+1)
+ *   new_ctx_len  [batch] ctx + m; must not be the ctx_len array (other workgroups of the
+ *                same request may still read ctx_len)
+ *   committed    [batch][block+1] the tokens the round emits: the drafted tokens of the
+ *                m-1 accepted nodes in path order, then the bonus token, then -1
+ *   n_committed  [batch] m (tokens emitted)
+ *   dtype        TAPS_BF16 or TAPS_FP32 (element size of the cache)
+ * K_cache and V_cache must be 16-byte aligned.  Calls that touch the same cache rows must
+ * not overlap in time. */
+taps_status kv_commit(void *K_cache, void *V_cache, const int64_t *kv_offset,
+                      const int32_t *ctx_len, const taps_tree *tree, const int32_t *path,
+                      const int32_t *path_len, const int32_t *bonus, int32_t batch,
+                      int32_t budget, int32_t block, int32_t Hkv, int32_t head_dim,
+                      int32_t max_ctx, int32_t dtype, int32_t *new_ctx_len,
+                      int32_t *committed, int32_t *n_committed, hipStream_t stream);
 
 /* Human-readable name of a status code (static string). */
 const char *taps_status_string(int32_t status);

@@ -10,6 +10,8 @@ memory and the current stream.
     O = att(Q, K, V, kv_offset, ctx_len, tree.parent, tree.n_nodes)   # tree_verify_attn
     walk = AcceptWalk(batch, budget, block)
     path, path_len, bonus = walk(tree, target_tokens)                 # accept_walk
+    com = KVCommit(batch, budget, block, Hkv, head_dim, max_ctx)
+    new_ctx, tokens, n = com(K, V, kv_offset, ctx_len, tree, path, path_len, bonus)  # kv_commit
 """
 from __future__ import annotations
 
@@ -156,3 +158,35 @@ class AcceptWalk:
             ctypes.byref(st), self.batch, self.budget, self.block, _ptr(target_tokens),
             _ptr(self.path), _ptr(self.path_len), _ptr(self.bonus), _stream()))
         return self.path, self.path_len, self.bonus
+
+
+class KVCommit:
+    """kv_commit: the accepted path's tree K/V rows move to the rows after the context
+    (in place), and the round's emitted tokens."""
+
+    def __init__(self, batch, budget, block, Hkv, head_dim, max_ctx, dtype=BF16, device="cuda"):
+        self.lib = load()
+        self.shape = (batch, budget, block, Hkv, head_dim, max_ctx, dtype)
+        self.new_ctx = torch.empty(batch, dtype=torch.int32, device=device)
+        self.committed = torch.empty(batch, block + 1, dtype=torch.int32, device=device)
+        self.n_committed = torch.empty(batch, dtype=torch.int32, device=device)
+
+    def __call__(self, K, V, kv_offset, ctx_len, tree: TreeBuffers, path, path_len, bonus):
+        batch, budget, block, Hkv, hd, max_ctx, dtype = self.shape
+        tdt = _TORCH_DT[dtype]
+        _need(K, "K_cache", tdt)
+        _need(V, "V_cache", tdt, tuple(K.shape))
+        if K.dim() != 3 or K.shape[1:] != (Hkv, hd):
+            raise ValueError(f"K_cache: expected [rows, {Hkv}, {hd}], got {tuple(K.shape)}")
+        _need(kv_offset, "kv_offset", torch.int64, (batch,))
+        _need(ctx_len, "ctx_len", torch.int32, (batch,))
+        _need(tree.token, "tree.token", torch.int32, (batch, budget))
+        _need(path, "path", torch.int32, (batch, block + 1))
+        _need(path_len, "path_len", torch.int32, (batch,))
+        _need(bonus, "bonus", torch.int32, (batch,))
+        st = tree.struct()
+        _lib.check(self.lib, "kv_commit", self.lib.kv_commit(
+            _ptr(K), _ptr(V), _ptr(kv_offset), _ptr(ctx_len), ctypes.byref(st), _ptr(path),
+            _ptr(path_len), _ptr(bonus), batch, budget, block, Hkv, hd, max_ctx, dtype,
+            _ptr(self.new_ctx), _ptr(self.committed), _ptr(self.n_committed), _stream()))
+        return self.new_ctx, self.committed, self.n_committed

@@ -27,7 +27,8 @@ MAX_BUDGET = 256
 EXPORTED = [
     "taps_select_workspace_bytes", "taps_select_validate", "taps_select",
     "tree_verify_attn_workspace_bytes", "tree_verify_attn_validate", "tree_verify_attn",
-    "tree_verify_attn_timed", "accept_walk", "taps_status_string", "taps_spec_exp_host",
+    "tree_verify_attn_timed", "accept_walk", "kv_commit", "taps_status_string",
+    "taps_spec_exp_host",
 ]
 
 
@@ -84,6 +85,9 @@ def load(path: str = LIB_PATH):
     lib.tree_verify_attn_timed.restype = i32
     lib.accept_walk.argtypes = [P(Tree), i32, i32, i32, vp, vp, vp, vp, vp]
     lib.accept_walk.restype = i32
+    lib.kv_commit.argtypes = [vp, vp, vp, vp, P(Tree), vp, vp, vp, i32, i32, i32, i32, i32, i32,
+                              i32, vp, vp, vp, vp]
+    lib.kv_commit.restype = i32
     lib.taps_status_string.argtypes = [i32]
     lib.taps_status_string.restype = ctypes.c_char_p
     lib.taps_spec_exp_host.argtypes = [f64]

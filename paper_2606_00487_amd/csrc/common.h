@@ -67,6 +67,12 @@ hipError_t launch_walk(const taps_tree& t, int batch, int budget, int block,
                        const int32_t* target, int32_t* path, int32_t* path_len, int32_t* bonus,
                        hipStream_t s);
 
+hipError_t launch_commit(void* K, void* V, const int64_t* off, const int32_t* ctx,
+                         const int32_t* token, const int32_t* path, const int32_t* path_len,
+                         const int32_t* bonus, int batch, int budget, int block, int Hkv,
+                         int head_dim, int elem_bytes, int max_ctx, int32_t* new_ctx,
+                         int32_t* committed, int32_t* n_committed, hipStream_t s);
+
 double spec_exp_host(double t);
 
 }  // namespace taps

@@ -118,6 +118,29 @@ def test_walk_validation(lib):
     assert lib.accept_walk(None, 0, 64, 16, None, None, None, None, None) == _lib.TAPS_OK
 
 
+def test_commit_validation(lib):
+    fake = 1 << 20          # aligned, never dereferenced: every case stops before a launch
+    t = _lib.Tree(fake, fake, fake, fake, fake, fake, fake, fake)
+    ok = (fake, fake, fake, fake, ctypes.byref(t), fake, fake, fake)
+    outs = (fake + 64, fake + 128, fake + 192, None)
+
+    def call(ptrs=ok, sizes=(1, 64, 16, 8, 128, 8192, 0), out=outs):
+        return lib.kv_commit(*ptrs, *sizes, *out)
+
+    assert call(sizes=(0, 64, 16, 8, 128, 8192, 0)) == _lib.TAPS_OK            # nothing to do
+    assert call(sizes=(-1, 64, 16, 8, 128, 8192, 0)) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(sizes=(1, 257, 16, 8, 128, 8192, 0)) == _lib.TAPS_ERR_UNSUPPORTED
+    assert call(sizes=(1, 64, 33, 8, 128, 8192, 0)) == _lib.TAPS_ERR_UNSUPPORTED
+    assert call(sizes=(1, 64, 16, 8, 96, 8192, 0)) == _lib.TAPS_ERR_UNSUPPORTED
+    assert call(sizes=(1, 64, 16, 8, 128, 8192, 5)) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(sizes=(1, 64, 16, 8, 128, -1, 0)) == _lib.TAPS_ERR_INVALID_ARG
+    # new_ctx_len may not be the ctx_len array; buffers must be present and aligned
+    assert call(out=(fake, fake + 128, fake + 192, None)) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(ptrs=(None,) + ok[1:]) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(ptrs=(fake + 8,) + ok[1:]) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(out=(None, fake + 128, fake + 192, None)) == _lib.TAPS_ERR_INVALID_ARG
+
+
 def test_status_strings(lib):
     assert lib.taps_status_string(0) == b"TAPS_OK"
     assert lib.taps_status_string(-3) == b"TAPS_ERR_WORKSPACE"
