@@ -20,6 +20,7 @@ round's state update (kv_commit of the accepted path) is not part of the step;
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -45,6 +46,11 @@ def parse():
     ap.add_argument("--steps", type=int, default=300)
     ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--config", default="qwen3_8b")
+    ap.add_argument("--budget", type=int, default=0,
+                    help="override the configuration's node budget N (1..256)")
+    ap.add_argument("--lambda2", type=float, default=None,
+                    help="override lambda2 of Eq. 3 (0 with --tau 0: no cost-aware pruning)")
+    ap.add_argument("--tau", type=float, default=None, help="override the utility threshold")
     ap.add_argument("--sets", type=int, default=0, help="input sets to rotate (0: enough to exceed the MALL)")
     ap.add_argument("--eager", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -128,6 +134,16 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cfg = CONFIGS[args.config]
+    over = {}
+    if args.budget:
+        over["budget"] = args.budget
+    if args.lambda2 is not None:
+        over["lambda2"] = args.lambda2
+    if args.tau is not None:
+        over["tau"] = args.tau
+    if over:   # a variant of the configuration: its name records the overrides
+        tag = ",".join(f"{k}={v}" for k, v in over.items())
+        cfg = dataclasses.replace(cfg, name=f"{cfg.name}[{tag}]", **over)
     bf = cfg.dtype == BF16
 
     def to_dev(a):
@@ -290,7 +306,8 @@ def main():
         "config": {
             "workload": f"{cfg.name}: batch {cfg.batch}, marginals [{cfg.block}, {cfg.vocab}] "
                         f"{'bf16 logits' if bf else 'fp32 probs'}, top-{cfg.K}, budget {cfg.budget}, "
-                        f"{cfg.Hq}/{cfg.Hkv} heads x {cfg.head_dim}, context {int(s['inp'].ctx_len.max())}",
+                        f"{cfg.Hq}/{cfg.Hkv} heads x {cfg.head_dim}, context {int(s['inp'].ctx_len.max())}"
+                        + (f", lambda2 {cfg.lambda2}, tau {cfg.tau}" if over else ""),
             "global_batch": cfg.batch,
             "budget": cfg.budget,
             "input_sets": nsets,

@@ -1059,11 +1059,26 @@ AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max
   p.wk = 1;
   p.mtile = 4 * 32;
   p.mtiles = (mrows + p.mtile - 1) / p.mtile;
-  // split the keys so that about 256 workgroups run, each with >= 2 stages
+  // Split the keys so that the workgroups (one per CU: the K/V rings fill its LDS) finish
+  // soonest: estimated time = rounds of 256 workgroups x (32-key stages per split + ~8
+  // stages' worth of prologue and partial writes).  Rounding the split count up to fill
+  // the chip can leave a second round of a few workgroups that doubles the time.
   const int keys = max_ctx + budget;
   const int step = kKT;
   const long long base = (long long)batch * Hkv * p.mtiles;
-  const int splits = (int)((256 + base - 1) / base);
+  int splits = 1;
+  long long best = -1;
+  for (int s = 1; s <= 64; ++s) {
+    int l = (keys + s - 1) / s;
+    l = ((l + step - 1) / step) * step;
+    if (l < 2 * step) l = 2 * step;
+    const long long rounds = (base * s + 255) / 256;
+    const long long cost = rounds * (l / step + 8);
+    if (best < 0 || cost < best) {
+      best = cost;
+      splits = s;
+    }
+  }
   int len = (keys + splits - 1) / splits;
   len = ((len + step - 1) / step) * step;
   if (len < 2 * step) len = 2 * step;

@@ -81,6 +81,20 @@ def _fuzz_marginals(rng, cfg, mode):
     return f32_to_bf16_bits(x) if cfg.dtype == BF16 else x
 
 
+@pytest.mark.parametrize("budget,lam2,tau", [(64, 0.0, 0.0), (128, 0.125, 0.0), (256, 0.125, 0.0),
+                                            (256, 0.0, 0.0)])
+def test_select_ablation_and_budget_variants(taps, budget, lam2, tau):
+    """The pruning ablation (lambda2 = 0 and tau = 0: the budget is filled by reach alone)
+    and the points of the budget sweep, on the Qwen3-8B marginals."""
+    import dataclasses
+    c = dataclasses.replace(CONFIGS["qwen3_8b"], budget=budget, lambda2=lam2, tau=tau)
+    say(f"[select-variant] budget={budget} lambda2={lam2} tau={tau}")
+    inp = gen_round(c, with_attention=False)
+    trees = U.oracle_trees(inp)
+    gpu, _, _ = run_select(taps, inp)
+    U.assert_tree_equal(gpu, trees, c)
+
+
 @pytest.mark.parametrize("seed", range(24))
 def test_select_fuzz(taps, seed):
     rng = np.random.default_rng(500 + seed)
