@@ -10,6 +10,13 @@ in the design notes):
 * Scorer stand-in: the edge logit is beta times the drafter logit of the child
   token (LOGITS input) or the child's probability is used directly (PROBS
   input).  The sibling softmax of Eq. 1 then depends only on (row, rank).
+* Marginal-confidence scorer (the scoring ablation of Sec. 5: the scorer is
+  removed and selection falls back to the drafter's marginal confidence, with
+  the same candidate pool and procedure): q_cond is the child's full-vocabulary
+  marginal probability, without the sibling renormalisation.  LOGITS:
+  EXP(x_r - M) / Z with M the row maximum and Z the sum over the whole row of
+  EXP(x_j - M), each term rounded to a multiple of 2^-42 and summed exactly (an
+  integer sum, so no summation order enters); PROBS: the probability itself.
 * Top-K order: value descending, then vocabulary index ascending; -0 equals
   +0; NaN ranks below -inf.
 * Ties in the greedy argmax of Alg. 1 are broken by the total order
@@ -28,10 +35,13 @@ from fractions import Fraction
 
 import numpy as np
 
-from .specexp import spec_exp
+from .specexp import spec_exp, spec_exp_array
 
 LOGITS = 0
 PROBS = 1
+SIBLING = 0     # scorer: sibling softmax over the K candidates (Eq. 1 stand-in)
+MARGINAL = 1    # scorer: the drafter's full-vocabulary marginal (Sec. 5 ablation)
+Z_GRID = 2.0 ** 42   # terms of the marginal normaliser are rounded to multiples of 1/Z_GRID
 
 
 @dataclasses.dataclass
@@ -95,6 +105,32 @@ def edge_factors(vals: np.ndarray, kind: int, beta: float) -> np.ndarray:
     return c
 
 
+def marginal_normaliser(row: np.ndarray, M: float) -> float:
+    """Z of the marginal scorer for one row of logits with maximum M: the sum over every
+    vocabulary entry of EXP(x_j - M) rounded to the nearest multiple of 2^-42 (half to
+    even), summed exactly as integers, then converted to the nearest double."""
+    t = spec_exp_array(np.asarray(row, dtype=np.float64) - M)
+    z = int(np.rint(t * Z_GRID).astype(np.int64).sum(dtype=np.int64))
+    return float(Fraction(z) / Fraction(int(Z_GRID)))
+
+
+def marginal_factors(vals: np.ndarray, rows: np.ndarray | None, kind: int) -> np.ndarray:
+    """q_cond of the marginal scorer, c[i][r]: the full-vocabulary probability of the
+    rank-r candidate of row i (0 for a row whose normaliser is 0 or not finite)."""
+    D, K = vals.shape
+    c = np.zeros((D, K), dtype=np.float64)
+    for i in range(D):
+        if kind == PROBS:
+            c[i] = [float(v) if float(v) > 0.0 else 0.0 for v in vals[i]]
+            continue
+        M = float(vals[i, 0])
+        Z = marginal_normaliser(rows[i], M)
+        if Z > 0.0 and np.isfinite(Z):
+            for r in range(K):
+                c[i, r] = spec_exp(float(vals[i, r]) - M) / Z
+    return c
+
+
 # ------------------------------------------------------------ Eq. 3 denominator
 def denominators(D: int, lambda1: float, lambda2: float) -> np.ndarray:
     return np.array([lambda1 + lambda2 * d for d in range(D + 1)], dtype=np.float64)
@@ -108,7 +144,7 @@ def _order_key(u: float, depth: int, path: tuple[int, ...]):
 # ------------------------------------------------------------ Alg. 1 (best-first form)
 def select_request(marg_rows: np.ndarray, K: int, budget: int, kind: int = LOGITS,
                    lambda1: float = 1.0, lambda2: float = 0.125, tau: float = 0.0,
-                   beta: float = 1.0) -> Tree:
+                   beta: float = 1.0, scorer: int = SIBLING) -> Tree:
     """Greedy prefix-closed selection of Alg. 1 for one request.
 
     The argmax of Alg. 1 over all unselected trie nodes always lies among the
@@ -124,7 +160,10 @@ def select_request(marg_rows: np.ndarray, K: int, budget: int, kind: int = LOGIT
     val = np.zeros((D, K), dtype=np.float64)
     for i in range(D):
         idx[i], val[i] = topk_row(marg_rows[i], K)
-    c = edge_factors(val, kind, beta)
+    if scorer == MARGINAL:
+        c = marginal_factors(val, marg_rows, kind)
+    else:
+        c = edge_factors(val, kind, beta)
     den = denominators(D, lambda1, lambda2)
 
     parent = [-1]

@@ -57,3 +57,23 @@ def spec_exp(t: float) -> float:
     for n in range(12, -1, -1):
         p = p * r + COEF[n]          # two roundings: Python never fuses
     return math.ldexp(p, k)
+
+
+def spec_exp_array(t) -> "np.ndarray":
+    """spec_exp applied elementwise to an array: the same operations in the same order
+    (NumPy rounds every operation on its own and never fuses), so every element equals
+    spec_exp of it bit for bit."""
+    import numpy as np
+    t = np.asarray(t, dtype=np.float64)
+    out = np.zeros(t.shape, dtype=np.float64)
+    ok = ~(np.isnan(t) | (t < T_MIN))
+    tt = t[ok]
+    k = np.rint(tt * INV_LN2)             # half to even, like Python round()
+    r = (tt - k * LN2_HI) - k * LN2_LO
+    p = np.full(tt.shape, COEF[13])
+    for n in range(12, -1, -1):
+        p = p * r + COEF[n]
+    res = np.ldexp(p, k.astype(np.int64))
+    res[tt == 0.0] = 1.0
+    out[ok] = res
+    return out
