@@ -16,7 +16,9 @@ in the design notes):
   marginal probability, without the sibling renormalisation.  LOGITS:
   EXP(x_r - M) / Z with M the row maximum and Z the sum over the whole row of
   EXP(x_j - M), each term rounded to a multiple of 2^-42 and summed exactly (an
-  integer sum, so no summation order enters); PROBS: the probability itself.
+  integer sum, so no summation order enters); PROBS: the probability itself,
+  clamped into [0, 1] (NaN counts 0), which keeps q_cond <= 1 as Alg. 1's
+  one-node-per-iteration property needs.
 * Top-K order: value descending, then vocabulary index ascending; -0 equals
   +0; NaN ranks below -inf.
 * Ties in the greedy argmax of Alg. 1 are broken by the total order
@@ -120,8 +122,8 @@ def marginal_factors(vals: np.ndarray, rows: np.ndarray | None, kind: int) -> np
     D, K = vals.shape
     c = np.zeros((D, K), dtype=np.float64)
     for i in range(D):
-        if kind == PROBS:
-            c[i] = [float(v) if float(v) > 0.0 else 0.0 for v in vals[i]]
+        if kind == PROBS:   # the probability, clamped into [0, 1] (NaN: 0)
+            c[i] = [min(float(v), 1.0) if float(v) > 0.0 else 0.0 for v in vals[i]]
             continue
         M = float(vals[i, 0])
         Z = marginal_normaliser(rows[i], M)

@@ -80,9 +80,11 @@ def test_marginal_factors_are_full_vocabulary_probabilities():
 
 
 def test_probs_marginal_is_the_probability_itself():
-    vals = np.array([[0.5, 0.25, 0.0, -0.1], [0.125, 0.125, 0.0625, 0.0]])
+    vals = np.array([[0.5, 0.25, 0.0, -0.1], [0.125, 0.125, 0.0625, 0.0],
+                     [math.inf, 3.0, 1.0, math.nan]])
     c = marginal_factors(vals, None, PROBS)
-    assert c.tolist() == [[0.5, 0.25, 0.0, 0.0], [0.125, 0.125, 0.0625, 0.0]]
+    assert c.tolist() == [[0.5, 0.25, 0.0, 0.0], [0.125, 0.125, 0.0625, 0.0],
+                          [1.0, 1.0, 1.0, 0.0]]
 
 
 @pytest.mark.parametrize("seed", range(10))
