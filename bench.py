@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--lambda2", type=float, default=None,
                     help="override lambda2 of Eq. 3 (0 with --tau 0: no cost-aware pruning)")
     ap.add_argument("--tau", type=float, default=None, help="override the utility threshold")
+    ap.add_argument("--scorer", choices=["sibling", "marginal"], default="sibling",
+                    help="marginal: q_cond is the full-vocabulary marginal (the scoring ablation)")
     ap.add_argument("--sets", type=int, default=0, help="input sets to rotate (0: enough to exceed the MALL)")
     ap.add_argument("--eager", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -141,8 +143,9 @@ def main():
         over["lambda2"] = args.lambda2
     if args.tau is not None:
         over["tau"] = args.tau
-    if over:   # a variant of the configuration: its name records the overrides
-        tag = ",".join(f"{k}={v}" for k, v in over.items())
+    scorer = 1 if args.scorer == "marginal" else 0
+    tag = ",".join([f"{k}={v}" for k, v in over.items()] + (["scorer=marginal"] if scorer else []))
+    if tag:    # a variant of the configuration: its name records the overrides
         cfg = dataclasses.replace(cfg, name=f"{cfg.name}[{tag}]", **over)
     bf = cfg.dtype == BF16
 
@@ -162,7 +165,7 @@ def main():
                       for k in range(nsets)))
     sel = taps.Selector(cfg.batch, cfg.block, cfg.vocab, cfg.K, cfg.budget, dtype=cfg.dtype,
                         kind=cfg.kind, lambda1=cfg.lambda1, lambda2=cfg.lambda2, tau=cfg.tau,
-                        beta=cfg.beta)
+                        beta=cfg.beta, scorer=scorer)
     att = taps.TreeAttention(cfg.batch, cfg.budget, cfg.Hq, cfg.Hkv, cfg.head_dim, max_ctx,
                              dtype=cfg.dtype, scale=cfg.scale)
     walk = taps.AcceptWalk(cfg.batch, cfg.budget, cfg.block)
@@ -307,7 +310,8 @@ def main():
             "workload": f"{cfg.name}: batch {cfg.batch}, marginals [{cfg.block}, {cfg.vocab}] "
                         f"{'bf16 logits' if bf else 'fp32 probs'}, top-{cfg.K}, budget {cfg.budget}, "
                         f"{cfg.Hq}/{cfg.Hkv} heads x {cfg.head_dim}, context {int(s['inp'].ctx_len.max())}"
-                        + (f", lambda2 {cfg.lambda2}, tau {cfg.tau}" if over else ""),
+                        + (f", lambda2 {cfg.lambda2}, tau {cfg.tau}" if over else "")
+                        + (", marginal scorer" if scorer else ""),
             "global_batch": cfg.batch,
             "budget": cfg.budget,
             "input_sets": nsets,
@@ -335,11 +339,11 @@ def main():
         "round_roofline_frac": round((round_bytes / HBM_PEAK_GBS / 1e3) / (ms_per_step * 1e3), 4),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, sets[0]["inp"], args.cpu_budget_s)
+        out["cpu_baseline"] = cpu_baseline(cfg, sets[0]["inp"], args.cpu_budget_s, scorer)
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(cfg, inp, budget_s):
+def cpu_baseline(cfg, inp, budget_s, scorer=0):
     """The oracle as it stands, on this host, over a bounded sample of one round."""
     import oracle
     from workloads import target_tokens
@@ -351,7 +355,8 @@ def cpu_baseline(cfg, inp, budget_s):
     x = inp.marginals_f64()
     t0 = time.perf_counter()
     trees = [oracle.select_request(x[b], cfg.K, cfg.budget, kind=cfg.kind, lambda1=cfg.lambda1,
-                                   lambda2=cfg.lambda2, tau=cfg.tau, beta=cfg.beta)
+                                   lambda2=cfg.lambda2, tau=cfg.tau, beta=cfg.beta,
+                                   scorer=scorer)
              for b in range(cfg.batch)]
     t_sel = time.perf_counter() - t0
     Qd, Kd, Vd = inp.qkv_f64()

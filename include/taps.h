@@ -44,6 +44,7 @@ typedef enum {
 
 typedef enum { TAPS_BF16 = 0, TAPS_FP32 = 1 } taps_dtype;
 typedef enum { TAPS_LOGITS = 0, TAPS_PROBS = 1 } taps_kind;
+typedef enum { TAPS_SCORER_SIBLING = 0, TAPS_SCORER_MARGINAL = 1 } taps_scorer;
 
 /* Limits of this build. */
 #define TAPS_MAX_BLOCK 32    /* draft positions D (tree depth)              */
@@ -65,11 +66,17 @@ typedef enum { TAPS_LOGITS = 0, TAPS_PROBS = 1 } taps_kind;
  *   lambda1  > 0, finite: per-node cost in Eq. 3
  *   lambda2  >= 0, finite: per-depth cost in Eq. 3 (negative values: UNSUPPORTED)
  *   tau      minimum utility; a node is added only while its utility is > tau (not NaN)
- *   beta     >= 0, finite scorer temperature for LOGITS */
+ *   beta     >= 0, finite scorer temperature for LOGITS
+ *   scorer   TAPS_SCORER_SIBLING (0; the default of a zeroed struct): q_cond is the
+ *            sibling softmax over the K candidates, below.  TAPS_SCORER_MARGINAL: the
+ *            scoring ablation of Sec. 5 (the scorer removed, selection by the drafter's
+ *            marginal confidence): q_cond is the candidate's full-vocabulary marginal,
+ *            below; LOGITS then needs beta = 1. */
 typedef struct {
   int32_t batch, block, vocab, K, budget;
   int32_t dtype, kind;
   double lambda1, lambda2, tau, beta;
+  int32_t scorer;
 } taps_select_params;
 
 /* Selected subtree S per request, breadth first: nodes ordered by depth, then by rank
@@ -96,7 +103,8 @@ typedef struct {
   float *topk_val;
 } taps_tree;
 
-/* Bytes of scratch taps_select needs (per-chunk top-K candidates). */
+/* Bytes of scratch taps_select needs (per-chunk top-K candidates; with the marginal scorer
+ * on logits also one 64-bit normaliser partial per chunk). */
 size_t taps_select_workspace_bytes(const taps_select_params *p);
 
 /* Host-only check of the parameters, no device access (the first step of taps_select). */
@@ -108,6 +116,9 @@ taps_status taps_select_validate(const taps_select_params *p);
  * Edge probability of a rank-r child of any depth-i node (sibling softmax, Eq. 1):
  *   LOGITS  e_r = EXP(beta * (x_r - x_0)), PROBS  e_r = x_r if x_r > 0 else 0;
  *   Z = e_0 + e_1 + ... (in rank order); q_cond = e_r / Z, or 0 when Z is 0 or not finite.
+ * Marginal scorer: LOGITS  q_cond = EXP(x_r - M) / Z, M the row maximum, Z = 2^-42 *
+ *   sum over the whole row of rint(2^42 * EXP(x_j - M)) (an exact integer sum; NaN
+ *   entries count 0), 0 when Z is 0; PROBS  q_cond = min(x_r, 1) if x_r > 0 else 0.
  * EXP is the shared fp64 exponential (Cody-Waite reduction, degree-13 Taylor, no FMA).
  * q_reach multiplies q_cond along the path (Eq. 2); utility = q_reach / (lambda1 +
  * lambda2 * depth) (Eq. 3); all in IEEE fp64.  Ties in the greedy argmax of Alg. 1 go to

@@ -111,7 +111,8 @@ def marginal_normaliser(row: np.ndarray, M: float) -> float:
     """Z of the marginal scorer for one row of logits with maximum M: the sum over every
     vocabulary entry of EXP(x_j - M) rounded to the nearest multiple of 2^-42 (half to
     even), summed exactly as integers, then converted to the nearest double."""
-    t = spec_exp_array(np.asarray(row, dtype=np.float64) - M)
+    with np.errstate(invalid="ignore"):     # inf - inf: NaN, which contributes 0
+        t = spec_exp_array(np.asarray(row, dtype=np.float64) - M)
     z = int(np.rint(t * Z_GRID).astype(np.int64).sum(dtype=np.int64))
     return float(Fraction(z) / Fraction(int(Z_GRID)))
 

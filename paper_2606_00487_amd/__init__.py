@@ -22,7 +22,8 @@ import torch
 
 from . import _lib
 from ._lib import (TAPS_BF16 as BF16, TAPS_FP32 as FP32, TAPS_LOGITS as LOGITS,  # noqa: F401
-                   TAPS_PROBS as PROBS, TapsError, load)
+                   TAPS_PROBS as PROBS, TAPS_SCORER_MARGINAL as MARGINAL,
+                   TAPS_SCORER_SIBLING as SIBLING, TapsError, load)
 
 _TORCH_DT = {BF16: torch.bfloat16, FP32: torch.float32}
 
@@ -78,10 +79,12 @@ class Selector:
     """taps_select: top-K, Eq. 1-3 and the budgeted prefix-closed selection of Alg. 1."""
 
     def __init__(self, batch, block, vocab, K, budget, dtype=BF16, kind=LOGITS, lambda1=1.0,
-                 lambda2=0.125, tau=0.0, beta=1.0, device="cuda"):
+                 lambda2=0.125, tau=0.0, beta=1.0, scorer=SIBLING, device="cuda"):
+        """scorer: SIBLING (sibling softmax over the K candidates) or MARGINAL (the
+        drafter's full-vocabulary marginal: the scoring ablation)."""
         self.lib = load()
         self.p = _lib.SelectParams(batch, block, vocab, K, budget, dtype, kind, lambda1, lambda2,
-                                   tau, beta)
+                                   tau, beta, scorer)
         _lib.check(self.lib, "taps_select_validate", self.lib.taps_select_validate(ctypes.byref(self.p)))
         self.ws_bytes = self.lib.taps_select_workspace_bytes(ctypes.byref(self.p))
         self.ws = torch.empty(max(self.ws_bytes, 8), dtype=torch.uint8, device=device)

@@ -20,6 +20,8 @@ TAPS_BF16 = 0
 TAPS_FP32 = 1
 TAPS_LOGITS = 0
 TAPS_PROBS = 1
+TAPS_SCORER_SIBLING = 0
+TAPS_SCORER_MARGINAL = 1
 MAX_BLOCK = 32
 MAX_K = 16
 MAX_BUDGET = 256
@@ -36,7 +38,8 @@ class SelectParams(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("block", ctypes.c_int32), ("vocab", ctypes.c_int32),
                 ("K", ctypes.c_int32), ("budget", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("kind", ctypes.c_int32), ("lambda1", ctypes.c_double),
-                ("lambda2", ctypes.c_double), ("tau", ctypes.c_double), ("beta", ctypes.c_double)]
+                ("lambda2", ctypes.c_double), ("tau", ctypes.c_double), ("beta", ctypes.c_double),
+                ("scorer", ctypes.c_int32)]
 
 
 class Tree(ctypes.Structure):

@@ -27,11 +27,18 @@ taps_status select_check(const taps_select_params* p) {
   if (std::isnan(p->tau)) return TAPS_ERR_INVALID_ARG;
   if (!finite(p->beta) || p->beta < 0.0) return TAPS_ERR_INVALID_ARG;
   if (p->kind == TAPS_PROBS && p->beta != 1.0) return TAPS_ERR_UNSUPPORTED;
+  if (p->scorer != TAPS_SCORER_SIBLING && p->scorer != TAPS_SCORER_MARGINAL)
+    return TAPS_ERR_INVALID_ARG;
+  if (p->scorer == TAPS_SCORER_MARGINAL && p->beta != 1.0) return TAPS_ERR_UNSUPPORTED;
   const int64_t rows = (int64_t)p->batch * p->block;
   if (rows > (int64_t)1 << 20) return TAPS_ERR_UNSUPPORTED;
   const TopkPlan plan = plan_topk(p->vocab, (int)rows > 0 ? (int)rows : 1, p->dtype);
   if (plan.chunks > kMaxChunks) return TAPS_ERR_UNSUPPORTED;
   return TAPS_OK;
+}
+
+bool needs_z(const taps_select_params* p) {
+  return p->scorer == TAPS_SCORER_MARGINAL && p->kind == TAPS_LOGITS;
 }
 
 taps_status attn_check(int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv, int32_t hd,
@@ -75,7 +82,8 @@ size_t taps_select_workspace_bytes(const taps_select_params* p) {
   if (select_check(p) != TAPS_OK || p->batch == 0) return 0;
   const int rows = p->batch * p->block;
   const TopkPlan plan = plan_topk(p->vocab, rows, p->dtype);
-  return (size_t)rows * plan.chunks * p->K * sizeof(uint64_t);
+  const size_t cand = (size_t)rows * plan.chunks * p->K * sizeof(uint64_t);
+  return cand + (needs_z(p) ? (size_t)rows * plan.chunks * sizeof(int64_t) : 0);
 }
 
 taps_status taps_select(const void* marginals, const taps_select_params* p, const taps_tree* out,
@@ -94,7 +102,14 @@ taps_status taps_select(const void* marginals, const taps_select_params* p, cons
   if (launch_topk_chunks(marginals, p->dtype, rows, p->vocab, p->K, plan, (uint64_t*)ws,
                          stream) != hipSuccess)
     return TAPS_ERR_HIP;
-  if (launch_select(marginals, *p, plan, (const uint64_t*)ws, *out, stream) != hipSuccess)
+  int64_t* zpart = nullptr;
+  if (needs_z(p)) {
+    zpart = (int64_t*)((char*)ws + (size_t)rows * plan.chunks * p->K * sizeof(uint64_t));
+    if (launch_marginal_z(marginals, p->dtype, rows, p->vocab, p->K, plan, (const uint64_t*)ws,
+                          zpart, stream) != hipSuccess)
+      return TAPS_ERR_HIP;
+  }
+  if (launch_select(marginals, *p, plan, (const uint64_t*)ws, zpart, *out, stream) != hipSuccess)
     return TAPS_ERR_HIP;
   return TAPS_OK;
 }

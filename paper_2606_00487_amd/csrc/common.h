@@ -38,7 +38,12 @@ hipError_t launch_topk_chunks(const void* marg, int dtype, int rows, int vocab, 
                               const TopkPlan& plan, uint64_t* cand, hipStream_t s);
 
 hipError_t launch_select(const void* marg, const taps_select_params& p, const TopkPlan& plan,
-                         const uint64_t* cand, const taps_tree& out, hipStream_t s);
+                         const uint64_t* cand, const int64_t* zpart, const taps_tree& out,
+                         hipStream_t s);
+
+hipError_t launch_marginal_z(const void* marg, int dtype, int rows, int vocab, int K,
+                             const TopkPlan& plan, const uint64_t* cand, int64_t* zpart,
+                             hipStream_t s);
 
 struct AttnPlan {
   int qb;          // 32-row query blocks per wave (1 or 2)

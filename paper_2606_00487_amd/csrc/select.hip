@@ -129,6 +129,16 @@ __device__ inline uint32_t wave_and_u32(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, kWave - 1);
 }
 
+// sum of a 64-bit integer over the lanes of a wave (exact), in every lane
+__device__ inline int64_t wave_sum_i64(int64_t v) {
+#pragma unroll
+  for (int m = kWave / 2; m >= 1; m >>= 1) {
+    const uint32_t lo = __shfl_xor((uint32_t)v, m), hi = __shfl_xor((uint32_t)((uint64_t)v >> 32), m);
+    v += (int64_t)(((uint64_t)hi << 32) | lo);
+  }
+  return v;
+}
+
 // inclusive prefix sum within each row of 16 lanes
 __device__ inline int row_inclusive_sum(int v) {
   v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
@@ -392,7 +402,8 @@ __device__ int select_sequential(Shared& sh, int D, int K, int N, double tau) {
 template <int SLOTS>
 __global__ __launch_bounds__(kThreadsA) void select_kernel(
     int D, int K, int N, int kind, double lambda1, double lambda2, double tau, double beta,
-    int chunks, const uint64_t* __restrict__ cand, int32_t* __restrict__ o_parent,
+    int chunks, int marginal, const uint64_t* __restrict__ cand,
+    const int64_t* __restrict__ zpart, int32_t* __restrict__ o_parent,
     int32_t* __restrict__ o_token, int32_t* __restrict__ o_depth, int32_t* __restrict__ o_rank,
     double* __restrict__ o_q, int32_t* __restrict__ o_n, int32_t* __restrict__ o_tidx,
     float* __restrict__ o_tval) {
@@ -535,7 +546,19 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
         sh.e[i][lane] = e;
       }
       wave_fence();
-      if (lane < K) {
+      if (zpart) {
+        // marginal scorer, logits (beta is 1): the full-vocabulary normaliser is the exact
+        // sum of the row's per-chunk integer partials (multiples of 2^-42)
+        const int64_t* zr = zpart + ((size_t)b * D + i) * chunks;
+        int64_t zp = 0;
+        for (int c0 = lane; c0 < chunks; c0 += kWave) zp += zr[c0];
+        const int64_t zi = wave_sum_i64(zp);
+        const double Z = (double)zi * 0x1p-42;
+        if (lane < K) sh.c[i][lane] = Z > 0.0 ? sh.e[i][lane] / Z : 0.0;
+      } else if (kind == TAPS_PROBS && marginal) {
+        // the probability itself (e = x if x > 0, else 0), clamped to 1
+        if (lane < K) sh.c[i][lane] = fmin(sh.e[i][lane], 1.0);
+      } else if (lane < K) {
         double Z = 0.0;
         for (int j = 0; j < K; ++j) Z = Z + sh.e[i][j];
         const bool ok = Z > 0.0 && Z <= 1.7976931348623157e308;
@@ -741,19 +764,83 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
   if (tid == 0) o_n[b] = n;
 }
 
+// Marginal scorer, logits: per (row, chunk) the integer partial of the full-vocabulary
+// normaliser, sum over the chunk's entries of rint(2^42 * EXP(x_j - M)), where M is the
+// row maximum (the largest chunk head the top-K pass wrote).  Integer sums are exact, so
+// the order of the additions (here, and of the partials in the selection) does not enter.
+// Grid: rows * chunks workgroups of 256 threads, the chunking of the top-K pass.
+template <int DT>
+__global__ __launch_bounds__(256) void marginal_z_kernel(const void* __restrict__ marg,
+                                                         int vocab, int K, int chunk_len,
+                                                         int chunks,
+                                                         const uint64_t* __restrict__ cand,
+                                                         int64_t* __restrict__ zpart) {
+  __shared__ double s_M;
+  __shared__ int64_t s_w[4];
+  const int row = blockIdx.x / chunks;
+  const int chunk = blockIdx.x - row * chunks;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  if (wave == 0) {
+    uint64_t h = 0ull;
+    for (int c = lane; c < chunks; c += kWave) {
+      const uint64_t x = cand[((size_t)row * chunks + c) * K];
+      h = x > h ? x : h;
+    }
+    h = wave_max_u64(h);
+    if (lane == 0) s_M = (double)value_from_key(h ? (uint32_t)(h >> 32) : 0u);
+  }
+  __syncthreads();
+  const double M = s_M;
+  const int start = chunk * chunk_len;
+  const int end = min(vocab, start + chunk_len);
+  int64_t acc = 0;
+  for (int e = start + tid; e < end; e += 256) {
+    double x;
+    if (DT == TAPS_BF16) {
+      const uint16_t u = ((const uint16_t*)marg)[(size_t)row * vocab + e];
+      x = (double)__uint_as_float((uint32_t)u << 16);
+    } else {
+      x = (double)((const float*)marg)[(size_t)row * vocab + e];
+    }
+    const double t = spec_exp(x - M);
+    acc += (int64_t)rint(t * 0x1p42);
+  }
+  acc = wave_sum_i64(acc);
+  if (lane == 0) s_w[wave] = acc;
+  __syncthreads();
+  if (tid == 0) zpart[(size_t)row * chunks + chunk] = s_w[0] + s_w[1] + s_w[2] + s_w[3];
+}
+
 }  // namespace
 
 double spec_exp_host(double t) { return spec_exp(t); }
 
+hipError_t launch_marginal_z(const void* marg, int dtype, int rows, int vocab, int K,
+                             const TopkPlan& plan, const uint64_t* cand, int64_t* zpart,
+                             hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  const dim3 grid((unsigned)(rows * plan.chunks)), block(256);
+  if (dtype == TAPS_BF16)
+    marginal_z_kernel<TAPS_BF16><<<grid, block, 0, s>>>(marg, vocab, K, plan.chunk_len,
+                                                        plan.chunks, cand, zpart);
+  else
+    marginal_z_kernel<TAPS_FP32><<<grid, block, 0, s>>>(marg, vocab, K, plan.chunk_len,
+                                                        plan.chunks, cand, zpart);
+  return hipGetLastError();
+}
+
 hipError_t launch_select(const void* /*marg*/, const taps_select_params& p, const TopkPlan& plan,
-                         const uint64_t* cand, const taps_tree& out, hipStream_t s) {
+                         const uint64_t* cand, const int64_t* zpart, const taps_tree& out,
+                         hipStream_t s) {
   dim3 grid((unsigned)p.batch), block(kThreadsA);
   const int slots = (p.budget + kWave - 1) / kWave;
+  const int marginal = p.scorer == TAPS_SCORER_MARGINAL;
 #define TAPS_SEL(SL)                                                                          \
   select_kernel<SL><<<grid, block, 0, s>>>(p.block, p.K, p.budget, p.kind, p.lambda1,         \
-                                           p.lambda2, p.tau, p.beta, plan.chunks, cand,       \
-                                           out.parent, out.token, out.depth, out.rank,        \
-                                           out.q_reach, out.n_nodes, out.topk_idx, out.topk_val)
+                                           p.lambda2, p.tau, p.beta, plan.chunks, marginal,   \
+                                           cand, zpart, out.parent, out.token, out.depth,     \
+                                           out.rank, out.q_reach, out.n_nodes, out.topk_idx,  \
+                                           out.topk_val)
   switch (slots) {
     case 1: TAPS_SEL(1); break;
     case 2: TAPS_SEL(2); break;

@@ -68,6 +68,18 @@ def test_select_validation(lib, kw, status):
         assert lib.taps_select(None, ctypes.byref(p), None, None, 0, None) == status
 
 
+def test_select_scorer_validation_and_workspace(lib):
+    assert lib.taps_select_validate(ctypes.byref(params(scorer=1))) == _lib.TAPS_OK
+    assert lib.taps_select_validate(ctypes.byref(params(scorer=2))) == _lib.TAPS_ERR_INVALID_ARG
+    assert lib.taps_select_validate(ctypes.byref(params(scorer=1, beta=2.0))) == \
+        _lib.TAPS_ERR_UNSUPPORTED
+    base = lib.taps_select_workspace_bytes(ctypes.byref(params()))
+    marg = lib.taps_select_workspace_bytes(ctypes.byref(params(scorer=1)))
+    assert marg == base + 2 * 16 * 10 * 8        # one int64 partial per (row, chunk)
+    probs = params(scorer=1, kind=_lib.TAPS_PROBS)
+    assert lib.taps_select_workspace_bytes(ctypes.byref(probs)) == base   # no normaliser
+
+
 def test_select_rejects_null_buffers_and_small_workspace(lib):
     p = params()
     assert lib.taps_select(None, ctypes.byref(p), None, None, 0, None) == _lib.TAPS_ERR_INVALID_ARG

@@ -95,6 +95,42 @@ def test_select_ablation_and_budget_variants(taps, budget, lam2, tau):
     U.assert_tree_equal(gpu, trees, c)
 
 
+@pytest.mark.parametrize("name", ["tiny", "qwen3_4b", "qwen3_8b", "stress"])
+def test_select_marginal_scorer_matches_oracle(taps, name):
+    """The scoring ablation: q_cond is the full-vocabulary marginal (the exact integer
+    normaliser for logits, the probability itself for probabilities)."""
+    say(f"[select-marginal] {name}")
+    inp = gen_round(name, with_attention=False)
+    c = inp.cfg
+    trees = U.oracle_trees(inp, scorer=oracle.select.MARGINAL)
+    gpu, _, _ = run_select(taps, inp, scorer=1)
+    U.assert_tree_equal(gpu, trees, c)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_select_marginal_fuzz(taps, seed):
+    rng = np.random.default_rng(900 + seed)
+    dtype = [BF16, FP32][seed % 2]
+    kind = [LOGITS, LOGITS, PROBS][seed % 3]
+    V = int(rng.choice([17, 1001, 70001]))
+    K = min(int(rng.integers(1, 17)), V)
+    D = int(rng.integers(1, 33))
+    N = int(rng.choice([1, 16, 64, 200]))
+    mode = ["ties", "deep", "specials", "plain"][seed % 4]
+    cfg = _fuzz_cfg(rng, dtype, kind, V, D, K, N)
+    say(f"[fuzz-marginal] seed={seed} dtype={dtype} kind={kind} V={V} K={K} D={D} N={N} "
+        f"mode={mode}")
+    m = _fuzz_marginals(rng, cfg, mode)
+    from workloads import bf16_bits_to_f32
+    x = bf16_bits_to_f32(m).astype(np.float64) if dtype == BF16 else m.astype(np.float64)
+    trees = [oracle.select_request(x[b], K, N, kind=kind, scorer=oracle.select.MARGINAL)
+             for b in range(cfg.batch)]
+    sel = taps.Selector(cfg.batch, D, V, K, N, dtype=dtype, kind=kind, scorer=1)
+    gpu = sel(U.to_dev(m, dtype == BF16))
+    torch.cuda.synchronize()
+    U.assert_tree_equal(gpu, trees, cfg)
+
+
 @pytest.mark.parametrize("seed", range(24))
 def test_select_fuzz(taps, seed):
     rng = np.random.default_rng(500 + seed)
