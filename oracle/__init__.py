@@ -12,6 +12,7 @@ Layout
   attention.py  tree-masked verification attention (Sec. 4.1, Sec. 4.3)
   walk.py       greedy acceptance walk (Sec. 1; Limitations, temperature 0)
   commit.py     KV commit of the accepted path and the emitted tokens (Sec. 1)
+  scorer.py     the learned-scorer hook: MLP on edge features, sibling softmax (Sec. 4.2)
 
 Pins (what fixes each part without trusting this code) live in
 tests/test_oracle_*.py.  Parity of the oracle against the paper's own numbers

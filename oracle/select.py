@@ -43,6 +43,7 @@ LOGITS = 0
 PROBS = 1
 SIBLING = 0     # scorer: sibling softmax over the K candidates (Eq. 1 stand-in)
 MARGINAL = 1    # scorer: the drafter's full-vocabulary marginal (Sec. 5 ablation)
+LEARNED = 2     # scorer: the learned-scorer hook, an MLP on edge features (Sec. 4.2)
 Z_GRID = 2.0 ** 42   # terms of the marginal normaliser are rounded to multiples of 1/Z_GRID
 
 
@@ -147,7 +148,7 @@ def _order_key(u: float, depth: int, path: tuple[int, ...]):
 # ------------------------------------------------------------ Alg. 1 (best-first form)
 def select_request(marg_rows: np.ndarray, K: int, budget: int, kind: int = LOGITS,
                    lambda1: float = 1.0, lambda2: float = 0.125, tau: float = 0.0,
-                   beta: float = 1.0, scorer: int = SIBLING) -> Tree:
+                   beta: float = 1.0, scorer: int = SIBLING, mlp=None, req: int = 0) -> Tree:
     """Greedy prefix-closed selection of Alg. 1 for one request.
 
     The argmax of Alg. 1 over all unselected trie nodes always lies among the
@@ -165,6 +166,9 @@ def select_request(marg_rows: np.ndarray, K: int, budget: int, kind: int = LOGIT
         idx[i], val[i] = topk_row(marg_rows[i], K)
     if scorer == MARGINAL:
         c = marginal_factors(val, marg_rows, kind)
+    elif scorer == LEARNED:        # c[depth][parent rank][child rank] (oracle.scorer)
+        from .scorer import scorer_table
+        c = scorer_table(mlp, req, marg_rows, idx, val)
     else:
         c = edge_factors(val, kind, beta)
     den = denominators(D, lambda1, lambda2)
@@ -185,7 +189,7 @@ def select_request(marg_rows: np.ndarray, K: int, budget: int, kind: int = LOGIT
         if d >= D:
             return
         for r in range(K):
-            qc = q[pos] * c[d, r]
+            qc = q[pos] * edge_q(c, d, paths[pos], r)
             uc = qc / den[d + 1]
             p = paths[pos] + (r,)
             k = _order_key(uc, d + 1, p)
@@ -229,10 +233,19 @@ def select_batch(marginals_f64: np.ndarray, K: int, budget: int, **kw) -> list[T
     return [select_request(marginals_f64[b], K, budget, **kw) for b in range(marginals_f64.shape[0])]
 
 
+def edge_q(c: np.ndarray, d: int, parent_path: tuple[int, ...], r: int) -> float:
+    """q_cond of the rank-r child of the node at rank path parent_path (depth d): c[d][r]
+    for the scorers whose factor depends on (row, rank) only, c[d][parent rank][r] for
+    the learned scorer's table (the root's parent rank is 0)."""
+    if c.ndim == 3:
+        return c[d, parent_path[-1] if parent_path else 0, r]
+    return c[d, r]
+
+
 # ------------------------------------------------------------ pins: literal Alg. 1 and brute force
 def enumerate_trie(c: np.ndarray, den: np.ndarray, max_depth: int | None = None):
     """Every node of the implicit trie: dict path -> (q_reach, utility)."""
-    D, K = c.shape
+    D, K = c.shape[0], c.shape[-1]
     max_depth = D if max_depth is None else max_depth
     nodes = {(): (1.0, 1.0 / den[0])}
     level = [()]
@@ -241,7 +254,7 @@ def enumerate_trie(c: np.ndarray, den: np.ndarray, max_depth: int | None = None)
         for p in level:
             qp = nodes[p][0]
             for r in range(K):
-                qc = qp * c[d, r]
+                qc = qp * edge_q(c, d, p, r)
                 nodes[p + (r,)] = (qc, qc / den[d + 1])
                 nxt.append(p + (r,))
         level = nxt

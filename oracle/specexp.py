@@ -77,3 +77,29 @@ def spec_exp_array(t) -> "np.ndarray":
     res[tt == 0.0] = 1.0
     out[ok] = res
     return out
+
+
+# ---------------------------------------------------------------- the shared fp64 logarithm
+# log x for finite x > 0, used by the learned scorer's log-probability and entropy
+# features: x = m * 2^e with m in [sqrt(1/2), sqrt(2)) (frexp, then one exact doubling),
+# s = (m - 1) / (m + 1), log m = 2 * atanh(s) = 2 * s * (1 + s^2/3 + ... + s^26/27) by
+# Horner in s^2 with coefficients fl(1/(2k+1)), k = 13 .. 0 (the next term, s^29/29, is
+# below 1e-24), result = e * LN2_HI + (e * LN2_LO + log m).  No fused multiply-add.
+SQRT_HALF = float.fromhex("0x1.6a09e667f3bcdp-1")   # nearest double to sqrt(1/2)
+LOG_COEF = [float(Fraction(1, 2 * k + 1)) for k in range(14)]
+
+
+def spec_log(x: float) -> float:
+    """log(x) for finite x > 0 under the shared fp64 contract described above."""
+    m, e = math.frexp(float(x))
+    if m < SQRT_HALF:
+        m *= 2.0
+        e -= 1
+    s = (m - 1.0) / (m + 1.0)
+    z = s * s
+    p = LOG_COEF[13]
+    for k in range(12, -1, -1):
+        p = p * z + LOG_COEF[k]
+    logm = 2.0 * (s * p)
+    ef = float(e)
+    return ef * LN2_HI + (ef * LN2_LO + logm)
