@@ -8,15 +8,18 @@ are not published, so the hook runs a small MLP with caller-given (here: seeded 
 weights.  Reading (the same on the GPU):
 
 * Features of an edge into row i (child depth i+1), in this order: the parent token's
-  embedding (d values; the root's token is given per request; an absent token has a zero
-  embedding), the child token's embedding (d values), the depth i+1, the child's
+  embedding (d values; the root's token is given per request; a token outside the
+  vocabulary has a zero embedding), the child token's embedding (d values), the depth i+1, the child's
   log-probability (x_v - M) - LOG(Z) and the row's entropy H = LOG(Z) - S / Z.  M is the
   row maximum, Z the marginal normaliser of the marginal scorer (terms EXP(x_j - M) on a
   2^-42 grid, summed as integers), S the same exact sum of the terms t_j * (x_j - M)
   (terms with t_j = 0 count 0).  LOG is the shared fp64 logarithm of oracle.specexp.
-* MLP: a_k = relu(b1[k] + sum_j W1[k][j] f_j), logit = b2 + sum_k w2[k] a_k, all in fp64
-  with the sums in index order and no fused multiply-add (weights are fp32, widened
-  exactly); relu maps NaN to 0.  A child that is not a candidate (fewer than K entries in
+* MLP: a_k = relu(((((b1[k] + P_k) + C_k) + W1[k][2d] * depth) + W1[k][2d+1] * logprob)
+  + W1[k][2d+2] * entropy), with P_k = sum_j W1[k][j] * pe_j and C_k = sum_j W1[k][d+j] *
+  ce_j (each summed from 0 in index order) over the parent and child embeddings; logit =
+  b2 + sum_k w2[k] a_k in index order.  fp64, no fused multiply-add (weights are fp32,
+  widened exactly); relu maps NaN to 0.  Grouping the embedding parts lets the GPU compute
+  P once per parent and C once per child instead of once per edge.  A child that is not a candidate (fewer than K entries in
   its row) gets the logit -inf.
 * Sibling softmax over the K candidates of the parent, as Eq. 1's stand-in does:
   e_r = EXP(l_r - max_r l_r), Z' = e_0 + e_1 + ... in rank order, q_cond = e_r / Z', or 0
@@ -48,15 +51,9 @@ class MLPScorer:
 
 
 def random_scorer(rng: np.random.Generator, vocab: int, d: int, h: int, batch: int) -> MLPScorer:
-    """Seeded random weights of the shapes the hook takes (no trained weights exist here)."""
-    F = 2 * d + 3
-    return MLPScorer(
-        emb=(rng.standard_normal((vocab, d)) * 0.5).astype(np.float32),
-        W1=(rng.standard_normal((h, F)) / np.sqrt(F)).astype(np.float32),
-        b1=(rng.standard_normal(h) * 0.1).astype(np.float32),
-        w2=(rng.standard_normal(h) / np.sqrt(h)).astype(np.float32),
-        b2=float(np.float32(rng.standard_normal() * 0.1)),
-        root_token=rng.integers(0, vocab, size=batch).astype(np.int32))
+    """The seeded random weights of ``workloads.gen_scorer_weights`` as an MLPScorer."""
+    from workloads import gen_scorer_weights
+    return MLPScorer(**gen_scorer_weights(rng, vocab, d, h, batch))
 
 
 def row_statistics(row: np.ndarray, M: float) -> tuple[float, float]:
@@ -77,7 +74,7 @@ def row_statistics(row: np.ndarray, M: float) -> tuple[float, float]:
 
 
 def _emb(mlp: MLPScorer, tok: int, d: int) -> np.ndarray:
-    if tok < 0:
+    if tok < 0 or tok >= mlp.emb.shape[0]:       # no token: a zero embedding
         return np.zeros(d, dtype=np.float64)
     return mlp.emb[tok].astype(np.float64)
 
@@ -89,17 +86,28 @@ def edge_logits(mlp: MLPScorer, parent_tok: int, child_tok: np.ndarray, depth: i
     h = mlp.W1.shape[0]
     K = len(child_tok)
     pe = _emb(mlp, int(parent_tok), d)
+    W = mlp.W1.astype(np.float64)
+    P = []
+    for k in range(h):
+        acc = 0.0
+        for j in range(d):
+            acc = acc + float(W[k, j]) * float(pe[j])
+        P.append(acc)
     out = np.full(K, -np.inf)
     for r in range(K):
         if child_tok[r] < 0:
             continue
-        f = np.concatenate([pe, _emb(mlp, int(child_tok[r]), d),
-                            [float(depth), float(logprob[r]), float(entropy)]])
+        ce = _emb(mlp, int(child_tok[r]), d)
         logit = float(mlp.b2)
         for k in range(h):
-            a = float(mlp.b1[k])
-            for j in range(len(f)):
-                a = a + float(mlp.W1[k, j]) * float(f[j])
+            C = 0.0
+            for j in range(d):
+                C = C + float(W[k, d + j]) * float(ce[j])
+            a = float(mlp.b1[k]) + P[k]
+            a = a + C
+            a = a + float(W[k, 2 * d]) * float(depth)
+            a = a + float(W[k, 2 * d + 1]) * float(logprob[r])
+            a = a + float(W[k, 2 * d + 2]) * float(entropy)
             a = a if a > 0.0 else 0.0
             logit = logit + float(mlp.w2[k]) * a
         out[r] = logit
@@ -108,7 +116,7 @@ def edge_logits(mlp: MLPScorer, parent_tok: int, child_tok: np.ndarray, depth: i
 
 def sibling_softmax(logits: np.ndarray) -> np.ndarray:
     K = len(logits)
-    m = max(float(x) for x in logits)
+    m = max((float(x) for x in logits if x == x), default=-np.inf)   # NaN logits ignored
     with np.errstate(invalid="ignore"):
         e = [spec_exp(float(x) - m) for x in logits]
     Z = 0.0
