@@ -51,8 +51,10 @@ def parse():
     ap.add_argument("--lambda2", type=float, default=None,
                     help="override lambda2 of Eq. 3 (0 with --tau 0: no cost-aware pruning)")
     ap.add_argument("--tau", type=float, default=None, help="override the utility threshold")
-    ap.add_argument("--scorer", choices=["sibling", "marginal"], default="sibling",
-                    help="marginal: q_cond is the full-vocabulary marginal (the scoring ablation)")
+    ap.add_argument("--scorer", choices=["sibling", "marginal", "learned"], default="sibling",
+                    help="marginal: q_cond is the full-vocabulary marginal (the scoring ablation); "
+                         "learned: the learned-scorer hook with seeded random weights "
+                         "(embedding 16, hidden 32)")
     ap.add_argument("--sets", type=int, default=0, help="input sets to rotate (0: enough to exceed the MALL)")
     ap.add_argument("--eager", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -143,8 +145,9 @@ def main():
         over["lambda2"] = args.lambda2
     if args.tau is not None:
         over["tau"] = args.tau
-    scorer = 1 if args.scorer == "marginal" else 0
-    tag = ",".join([f"{k}={v}" for k, v in over.items()] + (["scorer=marginal"] if scorer else []))
+    scorer = {"sibling": 0, "marginal": 1, "learned": 2}[args.scorer]
+    tag = ",".join([f"{k}={v}" for k, v in over.items()] +
+                   ([f"scorer={args.scorer}"] if scorer else []))
     if tag:    # a variant of the configuration: its name records the overrides
         cfg = dataclasses.replace(cfg, name=f"{cfg.name}[{tag}]", **over)
     bf = cfg.dtype == BF16
@@ -163,9 +166,17 @@ def main():
         nsets = args.sets or 1
     max_ctx = int(max(gen_round(cfg, seed=inp0.seed + k, with_attention=False).ctx_len.max()
                       for k in range(nsets)))
+    mlp = mlp_dev = None
+    if scorer == 2:       # seeded random weights: the paper's trained weights are not published
+        from workloads import gen_scorer_weights
+        mlp = gen_scorer_weights(np.random.default_rng(20260602), cfg.vocab, 16, 32, cfg.batch)
+        mlp_dev = taps.ScorerWeights(
+            emb=torch.from_numpy(mlp["emb"]).to(dev), W1=torch.from_numpy(mlp["W1"]).to(dev),
+            b1=torch.from_numpy(mlp["b1"]).to(dev), w2=torch.from_numpy(mlp["w2"]).to(dev),
+            b2=mlp["b2"], root_token=torch.from_numpy(mlp["root_token"]).to(dev))
     sel = taps.Selector(cfg.batch, cfg.block, cfg.vocab, cfg.K, cfg.budget, dtype=cfg.dtype,
                         kind=cfg.kind, lambda1=cfg.lambda1, lambda2=cfg.lambda2, tau=cfg.tau,
-                        beta=cfg.beta, scorer=scorer)
+                        beta=cfg.beta, scorer=scorer, mlp=mlp_dev)
     att = taps.TreeAttention(cfg.batch, cfg.budget, cfg.Hq, cfg.Hkv, cfg.head_dim, max_ctx,
                              dtype=cfg.dtype, scale=cfg.scale)
     walk = taps.AcceptWalk(cfg.batch, cfg.budget, cfg.block)
@@ -311,7 +322,7 @@ def main():
                         f"{'bf16 logits' if bf else 'fp32 probs'}, top-{cfg.K}, budget {cfg.budget}, "
                         f"{cfg.Hq}/{cfg.Hkv} heads x {cfg.head_dim}, context {int(s['inp'].ctx_len.max())}"
                         + (f", lambda2 {cfg.lambda2}, tau {cfg.tau}" if over else "")
-                        + (", marginal scorer" if scorer else ""),
+                        + (f", {args.scorer} scorer" if scorer else ""),
             "global_batch": cfg.batch,
             "budget": cfg.budget,
             "input_sets": nsets,
@@ -339,11 +350,11 @@ def main():
         "round_roofline_frac": round((round_bytes / HBM_PEAK_GBS / 1e3) / (ms_per_step * 1e3), 4),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, sets[0]["inp"], args.cpu_budget_s, scorer)
+        out["cpu_baseline"] = cpu_baseline(cfg, sets[0]["inp"], args.cpu_budget_s, scorer, mlp)
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(cfg, inp, budget_s, scorer=0):
+def cpu_baseline(cfg, inp, budget_s, scorer=0, mlp=None):
     """The oracle as it stands, on this host, over a bounded sample of one round."""
     import oracle
     from workloads import target_tokens
@@ -354,9 +365,13 @@ def cpu_baseline(cfg, inp, budget_s, scorer=0):
         threads = 1
     x = inp.marginals_f64()
     t0 = time.perf_counter()
+    w = None
+    if mlp is not None:
+        from oracle.scorer import MLPScorer
+        w = MLPScorer(**mlp)
     trees = [oracle.select_request(x[b], cfg.K, cfg.budget, kind=cfg.kind, lambda1=cfg.lambda1,
                                    lambda2=cfg.lambda2, tau=cfg.tau, beta=cfg.beta,
-                                   scorer=scorer)
+                                   scorer=scorer, mlp=w, req=b)
              for b in range(cfg.batch)]
     t_sel = time.perf_counter() - t0
     Qd, Kd, Vd = inp.qkv_f64()

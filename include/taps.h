@@ -44,12 +44,35 @@ typedef enum {
 
 typedef enum { TAPS_BF16 = 0, TAPS_FP32 = 1 } taps_dtype;
 typedef enum { TAPS_LOGITS = 0, TAPS_PROBS = 1 } taps_kind;
-typedef enum { TAPS_SCORER_SIBLING = 0, TAPS_SCORER_MARGINAL = 1 } taps_scorer;
+typedef enum {
+  TAPS_SCORER_SIBLING = 0,
+  TAPS_SCORER_MARGINAL = 1,
+  TAPS_SCORER_LEARNED = 2
+} taps_scorer;
 
 /* Limits of this build. */
 #define TAPS_MAX_BLOCK 32    /* draft positions D (tree depth)              */
 #define TAPS_MAX_K 16        /* candidates per position                     */
 #define TAPS_MAX_BUDGET 256  /* N_max, root included                        */
+
+/* [host] Weights of the learned-scorer hook (Sec. 4.2, "Scorer design"): a per-edge MLP
+ * whose trained weights are not published, so the caller brings its own.  DEVICE fp32
+ * arrays owned by the caller:
+ *   emb         [vocab][emb_dim] token embeddings
+ *   W1          [hidden][2*emb_dim + 3] first layer over the edge features, in this
+ *               order: parent token embedding, child token embedding, child depth,
+ *               child log-probability, positional entropy of the child's row
+ *   b1, w2      [hidden]; b2 the output bias
+ *   root_token  [batch] int32 token at each request's current position (the root's
+ *               token, the parent token of depth-1 children); outside [0, vocab): a
+ *               zero embedding
+ *   emb_dim     1..32;  hidden  1..64 */
+typedef struct {
+  const float *emb, *W1, *b1, *w2;
+  float b2;
+  const int32_t *root_token;
+  int32_t emb_dim, hidden;
+} taps_scorer_mlp;
 
 /* [host] Selection parameters (Sec. 4.1 Stage 1 and 3; Eq. 3; Alg. 1).
  *   batch    requests B >= 0 (0: nothing is enqueued)
@@ -71,12 +94,17 @@ typedef enum { TAPS_SCORER_SIBLING = 0, TAPS_SCORER_MARGINAL = 1 } taps_scorer;
  *            sibling softmax over the K candidates, below.  TAPS_SCORER_MARGINAL: the
  *            scoring ablation of Sec. 5 (the scorer removed, selection by the drafter's
  *            marginal confidence): q_cond is the candidate's full-vocabulary marginal,
- *            below; LOGITS then needs beta = 1. */
+ *            below; LOGITS then needs beta = 1.  TAPS_SCORER_LEARNED: the learned
+ *            scorer's MLP (mlp) gives each edge a logit, normalised over the parent's
+ *            candidate children by a sibling softmax; LOGITS only; block * K * K must
+ *            not exceed 7168 (its q_cond table lives in LDS)
+ *   mlp      [host] weights, read only with TAPS_SCORER_LEARNED */
 typedef struct {
   int32_t batch, block, vocab, K, budget;
   int32_t dtype, kind;
   double lambda1, lambda2, tau, beta;
   int32_t scorer;
+  const taps_scorer_mlp *mlp;
 } taps_select_params;
 
 /* Selected subtree S per request, breadth first: nodes ordered by depth, then by rank
@@ -104,7 +132,7 @@ typedef struct {
 } taps_tree;
 
 /* Bytes of scratch taps_select needs (per-chunk top-K candidates; with the marginal scorer
- * on logits also one 64-bit normaliser partial per chunk). */
+ * on logits also one 64-bit normaliser partial per chunk, with the learned scorer two). */
 size_t taps_select_workspace_bytes(const taps_select_params *p);
 
 /* Host-only check of the parameters, no device access (the first step of taps_select). */
@@ -116,6 +144,13 @@ taps_status taps_select_validate(const taps_select_params *p);
  * Edge probability of a rank-r child of any depth-i node (sibling softmax, Eq. 1):
  *   LOGITS  e_r = EXP(beta * (x_r - x_0)), PROBS  e_r = x_r if x_r > 0 else 0;
  *   Z = e_0 + e_1 + ... (in rank order); q_cond = e_r / Z, or 0 when Z is 0 or not finite.
+ * Learned scorer: features of an edge into row i (the parent token's embedding, the child
+ *   token's, i+1, the child's log-probability (x_v - M) - LOG(Z), the row's entropy
+ *   LOG(Z) - S / Z with S = 2^-42 * sum of rint(2^42 * t_j (x_j - M)), t_j = EXP(x_j - M),
+ *   terms with t_j = 0 counting 0); a_k = relu(b1[k] + sum_j W1[k][j] f_j) (NaN -> 0),
+ *   logit = b2 + sum_k w2[k] a_k, fp64 with sums in index order; q_cond = EXP(l_r - max l)
+ *   / (sum over the K siblings in rank order), NaN logits ignored in the max.  LOG is the
+ *   shared fp64 logarithm (frexp reduction to [sqrt(1/2), sqrt(2)), 2 atanh series to s^27).
  * Marginal scorer: LOGITS  q_cond = EXP(x_r - M) / Z, M the row maximum, Z = 2^-42 *
  *   sum over the whole row of rint(2^42 * EXP(x_j - M)) (an exact integer sum; NaN
  *   entries count 0), 0 when Z is 0; PROBS  q_cond = min(x_r, 1) if x_r > 0 else 0.

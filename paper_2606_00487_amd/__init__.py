@@ -22,8 +22,9 @@ import torch
 
 from . import _lib
 from ._lib import (TAPS_BF16 as BF16, TAPS_FP32 as FP32, TAPS_LOGITS as LOGITS,  # noqa: F401
-                   TAPS_PROBS as PROBS, TAPS_SCORER_MARGINAL as MARGINAL,
-                   TAPS_SCORER_SIBLING as SIBLING, TapsError, load)
+                   TAPS_PROBS as PROBS, TAPS_SCORER_LEARNED as LEARNED,
+                   TAPS_SCORER_MARGINAL as MARGINAL, TAPS_SCORER_SIBLING as SIBLING, TapsError,
+                   load)
 
 _TORCH_DT = {BF16: torch.bfloat16, FP32: torch.float32}
 
@@ -75,16 +76,42 @@ class TreeBuffers:
                          _ptr(self.topk_val))
 
 
+@dataclasses.dataclass
+class ScorerWeights:
+    """Device weights of the learned-scorer hook (taps_scorer_mlp): float32 emb [vocab][d],
+    W1 [h][2d+3], b1 [h], w2 [h], the float b2 and int32 root_token [batch]."""
+    emb: torch.Tensor
+    W1: torch.Tensor
+    b1: torch.Tensor
+    w2: torch.Tensor
+    b2: float
+    root_token: torch.Tensor
+
+    def struct(self) -> _lib.ScorerMLP:
+        d, h = self.emb.shape[1], self.W1.shape[0]
+        _need(self.emb, "emb", torch.float32)
+        _need(self.W1, "W1", torch.float32, (h, 2 * d + 3))
+        _need(self.b1, "b1", torch.float32, (h,))
+        _need(self.w2, "w2", torch.float32, (h,))
+        _need(self.root_token, "root_token", torch.int32)
+        return _lib.ScorerMLP(_ptr(self.emb), _ptr(self.W1), _ptr(self.b1), _ptr(self.w2),
+                              float(self.b2), _ptr(self.root_token), d, h)
+
+
 class Selector:
     """taps_select: top-K, Eq. 1-3 and the budgeted prefix-closed selection of Alg. 1."""
 
     def __init__(self, batch, block, vocab, K, budget, dtype=BF16, kind=LOGITS, lambda1=1.0,
-                 lambda2=0.125, tau=0.0, beta=1.0, scorer=SIBLING, device="cuda"):
-        """scorer: SIBLING (sibling softmax over the K candidates) or MARGINAL (the
-        drafter's full-vocabulary marginal: the scoring ablation)."""
+                 lambda2=0.125, tau=0.0, beta=1.0, scorer=SIBLING, mlp=None, device="cuda"):
+        """scorer: SIBLING (sibling softmax over the K candidates), MARGINAL (the drafter's
+        full-vocabulary marginal: the scoring ablation) or LEARNED (the learned-scorer hook,
+        whose weights `mlp` (ScorerWeights) must stay alive while the Selector is used)."""
         self.lib = load()
+        self.mlp = mlp
+        self._mlp_struct = mlp.struct() if mlp is not None else None
         self.p = _lib.SelectParams(batch, block, vocab, K, budget, dtype, kind, lambda1, lambda2,
-                                   tau, beta, scorer)
+                                   tau, beta, scorer,
+                                   ctypes.pointer(self._mlp_struct) if mlp is not None else None)
         _lib.check(self.lib, "taps_select_validate", self.lib.taps_select_validate(ctypes.byref(self.p)))
         self.ws_bytes = self.lib.taps_select_workspace_bytes(ctypes.byref(self.p))
         self.ws = torch.empty(max(self.ws_bytes, 8), dtype=torch.uint8, device=device)

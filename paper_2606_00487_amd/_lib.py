@@ -22,6 +22,7 @@ TAPS_LOGITS = 0
 TAPS_PROBS = 1
 TAPS_SCORER_SIBLING = 0
 TAPS_SCORER_MARGINAL = 1
+TAPS_SCORER_LEARNED = 2
 MAX_BLOCK = 32
 MAX_K = 16
 MAX_BUDGET = 256
@@ -34,12 +35,18 @@ EXPORTED = [
 ]
 
 
+class ScorerMLP(ctypes.Structure):
+    _fields_ = [("emb", ctypes.c_void_p), ("W1", ctypes.c_void_p), ("b1", ctypes.c_void_p),
+                ("w2", ctypes.c_void_p), ("b2", ctypes.c_float), ("root_token", ctypes.c_void_p),
+                ("emb_dim", ctypes.c_int32), ("hidden", ctypes.c_int32)]
+
+
 class SelectParams(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("block", ctypes.c_int32), ("vocab", ctypes.c_int32),
                 ("K", ctypes.c_int32), ("budget", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("kind", ctypes.c_int32), ("lambda1", ctypes.c_double),
                 ("lambda2", ctypes.c_double), ("tau", ctypes.c_double), ("beta", ctypes.c_double),
-                ("scorer", ctypes.c_int32)]
+                ("scorer", ctypes.c_int32), ("mlp", ctypes.POINTER(ScorerMLP))]
 
 
 class Tree(ctypes.Structure):

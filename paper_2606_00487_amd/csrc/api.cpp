@@ -27,9 +27,21 @@ taps_status select_check(const taps_select_params* p) {
   if (std::isnan(p->tau)) return TAPS_ERR_INVALID_ARG;
   if (!finite(p->beta) || p->beta < 0.0) return TAPS_ERR_INVALID_ARG;
   if (p->kind == TAPS_PROBS && p->beta != 1.0) return TAPS_ERR_UNSUPPORTED;
-  if (p->scorer != TAPS_SCORER_SIBLING && p->scorer != TAPS_SCORER_MARGINAL)
+  if (p->scorer != TAPS_SCORER_SIBLING && p->scorer != TAPS_SCORER_MARGINAL &&
+      p->scorer != TAPS_SCORER_LEARNED)
     return TAPS_ERR_INVALID_ARG;
   if (p->scorer == TAPS_SCORER_MARGINAL && p->beta != 1.0) return TAPS_ERR_UNSUPPORTED;
+  if (p->scorer == TAPS_SCORER_LEARNED) {
+    if (p->kind != TAPS_LOGITS) return TAPS_ERR_UNSUPPORTED;
+    if (p->block * p->K * p->K > kMaxLearnedEdges) return TAPS_ERR_UNSUPPORTED;
+    const taps_scorer_mlp* w = p->mlp;
+    if (!w || !w->emb || !w->W1 || !w->b1 || !w->w2 || !w->root_token)
+      return TAPS_ERR_INVALID_ARG;
+    if (w->emb_dim < 1 || w->hidden < 1) return TAPS_ERR_INVALID_ARG;
+    if (w->emb_dim > 32 || w->hidden > 64) return TAPS_ERR_UNSUPPORTED;
+    if (learned_chunk_units(p->block, p->K, w->emb_dim, w->hidden) < 1)
+      return TAPS_ERR_UNSUPPORTED;
+  }
   const int64_t rows = (int64_t)p->batch * p->block;
   if (rows > (int64_t)1 << 20) return TAPS_ERR_UNSUPPORTED;
   const TopkPlan plan = plan_topk(p->vocab, (int)rows > 0 ? (int)rows : 1, p->dtype);
@@ -38,7 +50,8 @@ taps_status select_check(const taps_select_params* p) {
 }
 
 bool needs_z(const taps_select_params* p) {
-  return p->scorer == TAPS_SCORER_MARGINAL && p->kind == TAPS_LOGITS;
+  return (p->scorer == TAPS_SCORER_MARGINAL && p->kind == TAPS_LOGITS) ||
+         p->scorer == TAPS_SCORER_LEARNED;
 }
 
 taps_status attn_check(int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv, int32_t hd,
@@ -83,7 +96,8 @@ size_t taps_select_workspace_bytes(const taps_select_params* p) {
   const int rows = p->batch * p->block;
   const TopkPlan plan = plan_topk(p->vocab, rows, p->dtype);
   const size_t cand = (size_t)rows * plan.chunks * p->K * sizeof(uint64_t);
-  return cand + (needs_z(p) ? (size_t)rows * plan.chunks * sizeof(int64_t) : 0);
+  const size_t part = (size_t)rows * plan.chunks * kZSub * sizeof(int64_t);
+  return cand + (needs_z(p) ? part : 0) + (p->scorer == TAPS_SCORER_LEARNED ? part : 0);
 }
 
 taps_status taps_select(const void* marginals, const taps_select_params* p, const taps_tree* out,
@@ -102,14 +116,16 @@ taps_status taps_select(const void* marginals, const taps_select_params* p, cons
   if (launch_topk_chunks(marginals, p->dtype, rows, p->vocab, p->K, plan, (uint64_t*)ws,
                          stream) != hipSuccess)
     return TAPS_ERR_HIP;
-  int64_t* zpart = nullptr;
+  int64_t *zpart = nullptr, *spart = nullptr;
   if (needs_z(p)) {
     zpart = (int64_t*)((char*)ws + (size_t)rows * plan.chunks * p->K * sizeof(uint64_t));
+    if (p->scorer == TAPS_SCORER_LEARNED) spart = zpart + (size_t)rows * plan.chunks * kZSub;
     if (launch_marginal_z(marginals, p->dtype, rows, p->vocab, p->K, plan, (const uint64_t*)ws,
-                          zpart, stream) != hipSuccess)
+                          zpart, spart, stream) != hipSuccess)
       return TAPS_ERR_HIP;
   }
-  if (launch_select(marginals, *p, plan, (const uint64_t*)ws, zpart, *out, stream) != hipSuccess)
+  if (launch_select(marginals, *p, plan, (const uint64_t*)ws, zpart, spart, *out, stream) !=
+      hipSuccess)
     return TAPS_ERR_HIP;
   return TAPS_OK;
 }

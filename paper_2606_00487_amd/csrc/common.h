@@ -38,12 +38,21 @@ hipError_t launch_topk_chunks(const void* marg, int dtype, int rows, int vocab, 
                               const TopkPlan& plan, uint64_t* cand, hipStream_t s);
 
 hipError_t launch_select(const void* marg, const taps_select_params& p, const TopkPlan& plan,
-                         const uint64_t* cand, const int64_t* zpart, const taps_tree& out,
-                         hipStream_t s);
+                         const uint64_t* cand, const int64_t* zpart, const int64_t* spart,
+                         const taps_tree& out, hipStream_t s);
+
+// Integer partials of a row's full-vocabulary sums per top-K chunk (one workgroup each)
+constexpr int kZSub = 4;
+
+// Largest q_cond table D*K*K of the learned scorer (fp64, in dynamic LDS)
+constexpr int kMaxLearnedEdges = 7168;
+
+// Hidden units per chunk of the learned scorer's working set (0: it does not fit)
+int learned_chunk_units(int D, int K, int emb_dim, int hidden);
 
 hipError_t launch_marginal_z(const void* marg, int dtype, int rows, int vocab, int K,
                              const TopkPlan& plan, const uint64_t* cand, int64_t* zpart,
-                             hipStream_t s);
+                             int64_t* spart, hipStream_t s);
 
 struct AttnPlan {
   int qb;          // 32-row query blocks per wave (1 or 2)

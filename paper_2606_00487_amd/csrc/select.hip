@@ -64,6 +64,31 @@ __host__ __device__ inline double spec_exp(double t) {
   return ldexp(p, (int)kf);
 }
 
+// ------------------------------------------------------------------ shared logarithm
+// log x for finite x > 0: x = m 2^e, m in [sqrt(1/2), sqrt(2)); s = (m-1)/(m+1);
+// log m = 2 s (1 + s^2/3 + ... + s^26/27) by Horner in s^2 (coefficients 1/(2k+1) rounded to
+// double); result = e LN2_HI + (e LN2_LO + log m).  No fused multiply-add.
+__host__ __device__ inline double spec_log(double x) {
+  const double LN2_HI = 0x1.62e42ffp-1;
+  const double LN2_LO = -0x1.718432a1b0e26p-35;
+  const double SQRT_HALF = 0x1.6a09e667f3bcdp-1;
+  int e;
+  double m = frexp(x, &e);
+  if (m < SQRT_HALF) {
+    m = m * 2.0;
+    e = e - 1;
+  }
+  const double s = (m - 1.0) / (m + 1.0);
+  const double z = s * s;
+  double p = 1.0 / 27.0;
+  const double C[13] = {1.0, 1.0 / 3.0, 1.0 / 5.0, 1.0 / 7.0, 1.0 / 9.0, 1.0 / 11.0, 1.0 / 13.0,
+                        1.0 / 15.0, 1.0 / 17.0, 1.0 / 19.0, 1.0 / 21.0, 1.0 / 23.0, 1.0 / 25.0};
+  for (int k = 12; k >= 0; --k) p = p * z + C[k];
+  const double logm = 2.0 * (s * p);
+  const double ef = (double)e;
+  return ef * LN2_HI + (ef * LN2_LO + logm);
+}
+
 template <int V>
 struct IntC {
   static constexpr int value = V;
@@ -237,6 +262,7 @@ struct Shared {
   double e[TAPS_MAX_BLOCK][TAPS_MAX_K];
   double c[TAPS_MAX_BLOCK][TAPS_MAX_K];
   double den[TAPS_MAX_BLOCK + 1];
+  double lz[TAPS_MAX_BLOCK], ent[TAPS_MAX_BLOCK];   // learned scorer: LOG(Z), entropy
   int wsum[2][kWaves];
   int n;
   Scratch x;
@@ -259,16 +285,52 @@ __device__ inline int find_bstar(const Level& L, int N) {
   return C * 16 + 15 - (__ffsll((long long)ok2) - 1);
 }
 
+// Weights of the learned-scorer hook (device fp32 arrays) and its sizes
+struct ScorerArgs {
+  const float* emb;          // [vocab][d]
+  const float* W1;           // [h][2d + 3]
+  const float* b1;           // [h]
+  const float* w2;           // [h]
+  float b2;
+  const int32_t* root_token; // [batch]
+  int d, h, vocab;
+};
+
+// Working set of the learned scorer in the scratch area: float counts of the weight block
+// (W1, b1, w2) and of the embedding block (row stride ES), the parent slots np and all
+// slots S of the hidden-unit parts, and the units KC per chunk (below 1: does not fit)
+struct LearnedLayout {
+  int wsz, ES, esz, np, S, KC;
+};
+__host__ __device__ inline LearnedLayout learned_layout(int D, int K, int d, int h) {
+  LearnedLayout l;
+  l.wsz = (h * (2 * d + 3) + 2 * h + 1) & ~1;
+  l.ES = d | 1;
+  l.esz = ((D * K + 1) * l.ES + 1) & ~1;
+  l.np = 1 + (D - 1) * K;
+  l.S = l.np + D * K;
+  const long long left = (long long)sizeof(Scratch) - 4ll * (l.wsz + l.esz);
+  const long long kc = left > 0 ? left / (8ll * l.S) : 0;
+  l.KC = (int)(kc < h ? kc : h);
+  return l;
+}
+
+// q_cond of the rank-r child of a depth-d node of rank pr (the root: pr = 0): the scorer's
+// table c3[d][pr][r] for the learned scorer, else c[d][r]
+__device__ inline double qcond(const Shared& sh, const double* c3, int K, int d, int pr, int r) {
+  return c3 ? c3[(d * K + pr) * K + r] : sh.c[d][r];
+}
+
 // ------------------------------------------------------------------ Phase C fallback
 // Sequential best-first selection (one wave) for expansions larger than kCap; emits
 // S through sh.x.s in breadth-first order and returns n.
 template <int SLOTS>
-__device__ int select_sequential(Shared& sh, int D, int K, int N, double tau) {
+__device__ int select_sequential(Shared& sh, const double* c3, int D, int K, int N, double tau) {
   Seq& S = sh.x.s;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   if (wave == 0) {
     if (lane < K) {
-      const double q = 1.0 * sh.c[0][lane];
+      const double q = 1.0 * qcond(sh, c3, K, 0, 0, lane);
       S.Q[0][lane] = q;
       S.U[0][lane] = ubits(q / sh.den[1]) + 1ull;
     }
@@ -354,7 +416,7 @@ __device__ int select_sequential(Shared& sh, int D, int K, int N, double tau) {
       }
       if (lane < K) {
         if (dm < D) {
-          const double q = qm * sh.c[dm][lane];
+          const double q = qm * qcond(sh, c3, K, dm, r_w, lane);
           S.Q[m][lane] = q;
           S.U[m][lane] = ubits(q / sh.den[dm + 1]) + 1ull;
         } else {
@@ -403,7 +465,8 @@ template <int SLOTS>
 __global__ __launch_bounds__(kThreadsA) void select_kernel(
     int D, int K, int N, int kind, double lambda1, double lambda2, double tau, double beta,
     int chunks, int marginal, const uint64_t* __restrict__ cand,
-    const int64_t* __restrict__ zpart, int32_t* __restrict__ o_parent,
+    const int64_t* __restrict__ zpart, const int64_t* __restrict__ spart, ScorerArgs mlp,
+    int32_t* __restrict__ o_parent,
     int32_t* __restrict__ o_token, int32_t* __restrict__ o_depth, int32_t* __restrict__ o_rank,
     double* __restrict__ o_q, int32_t* __restrict__ o_n, int32_t* __restrict__ o_tidx,
     float* __restrict__ o_tval) {
@@ -546,12 +609,31 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
         sh.e[i][lane] = e;
       }
       wave_fence();
-      if (zpart) {
+      if (spart) {
+        // learned scorer: LOG(Z) and the entropy LOG(Z) - S / Z of the row from the exact
+        // sums of its integer partials (multiples of 2^-42); q_cond comes later
+        const int zn = chunks * kZSub;
+        const int64_t* zr = zpart + ((size_t)b * D + i) * zn;
+        const int64_t* sr = spart + ((size_t)b * D + i) * zn;
+        int64_t zp = 0, sp = 0;
+        for (int c0 = lane; c0 < zn; c0 += kWave) {
+          zp += zr[c0];
+          sp += sr[c0];
+        }
+        const int64_t zi = wave_sum_i64(zp), si = wave_sum_i64(sp);
+        if (lane == 0) {
+          const double Z = (double)zi * 0x1p-42, S = (double)si * 0x1p-42;
+          const double lz = zi > 0 ? spec_log(Z) : __longlong_as_double(0x7FF8000000000000ll);
+          sh.lz[i] = lz;
+          sh.ent[i] = lz - S / Z;
+        }
+      } else if (zpart) {
         // marginal scorer, logits (beta is 1): the full-vocabulary normaliser is the exact
-        // sum of the row's per-chunk integer partials (multiples of 2^-42)
-        const int64_t* zr = zpart + ((size_t)b * D + i) * chunks;
+        // sum of the row's integer partials (multiples of 2^-42)
+        const int zn = chunks * kZSub;
+        const int64_t* zr = zpart + ((size_t)b * D + i) * zn;
         int64_t zp = 0;
-        for (int c0 = lane; c0 < chunks; c0 += kWave) zp += zr[c0];
+        for (int c0 = lane; c0 < zn; c0 += kWave) zp += zr[c0];
         const int64_t zi = wave_sum_i64(zp);
         const double Z = (double)zi * 0x1p-42;
         if (lane < K) sh.c[i][lane] = Z > 0.0 ? sh.e[i][lane] / Z : 0.0;
@@ -573,6 +655,129 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
   // Eq. 3 denominators lambda1 + lambda2 * depth
   if (tid <= D) sh.den[tid] = lambda1 + lambda2 * (double)tid;
   __syncthreads();
+  // ---------------- learned scorer: q_cond table c3[i][parent rank][child rank] (all waves)
+  extern __shared__ double s_c3[];
+  double* c3 = spart ? s_c3 : nullptr;
+  if (c3) {
+    const int F = 2 * mlp.d + 3, d = mlp.d, h = mlp.h;
+    const int edges = D * K * K, DK = D * K;
+    // The scratch area (free until Phase C) holds, in order: the weights (W1, b1, w2 as
+    // fp32), the embeddings of the root's token (slot 0) and of each candidate (slot
+    // 1 + i*K + r; zeros for no token) at an odd row stride, and per hidden unit k the
+    // parent part b1[k] + P_k of each possible parent (0: the root, 1 + (i-1)*K + pr: the
+    // rank-pr candidate of row i-1) followed by the child part C_k of each candidate, for
+    // a chunk of KC units at a time.  Each edge then adds its five terms per unit.
+    const LearnedLayout lay = learned_layout(D, K, d, h);
+    float* Ws = reinterpret_cast<float*>(&sh.x);
+    const int ES = lay.ES, np = lay.np, S = lay.S, KC = lay.KC;
+    float* Es = Ws + lay.wsz;
+    double* part = reinterpret_cast<double*>(Es + lay.esz);
+    for (int j = tid; j < h * F; j += kThreadsA) Ws[j] = mlp.W1[j];
+    for (int j = tid; j < h; j += kThreadsA) {
+      Ws[h * F + j] = mlp.b1[j];
+      Ws[h * F + h + j] = mlp.w2[j];
+    }
+    for (int j = tid; j < (DK + 1) * d; j += kThreadsA) {
+      const int es = j / d, jj = j - es * d;
+      int tok = -1;
+      if (es == 0) {
+        tok = mlp.root_token[b];
+        if (tok >= mlp.vocab) tok = -1;   // outside the vocabulary: a zero embedding
+      } else {
+        const uint64_t kc = sh.top[(es - 1) / K][(es - 1) % K];
+        if (kc) tok = (int)cand_index(kc);
+      }
+      Es[es * ES + jj] = tok >= 0 ? mlp.emb[(size_t)tok * d + jj] : 0.0f;
+    }
+    for (int ed = tid; ed < edges; ed += kThreadsA) {
+      const int i = ed / (K * K), pr = (ed / K) % K, r = ed % K;
+      c3[ed] = sh.top[i][r] && (i > 0 || pr == 0) ? (double)mlp.b2 : -INFINITY;
+    }
+    __syncthreads();
+    for (int k0 = 0; k0 < h; k0 += KC) {
+      const int kn = min(KC, h - k0);
+      // the embedding sums, in index order from 0: one slot and eight units per thread
+      // (units past the chunk are computed on a clamped unit and dropped)
+      constexpr int U = 8;
+      const int G = (kn + U - 1) / U;
+      for (int t = tid; t < G * S; t += kThreadsA) {
+        const int g = t / S, sl = t - g * S;
+        const bool child = sl >= np;
+        const float* e = Es + (child ? 1 + sl - np : sl) * ES;
+        const float* w[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) w[u] = Ws + min(k0 + g * U + u, h - 1) * F + (child ? d : 0);
+        double acc[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc[u] = 0.0;
+        for (int j = 0; j < d; ++j) {
+          const double ej = (double)e[j];
+#pragma unroll
+          for (int u = 0; u < U; ++u) acc[u] = acc[u] + (double)w[u][j] * ej;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int kk = g * U + u;
+          if (kk < kn) part[kk * S + sl] = child ? acc[u] : (double)Ws[h * F + k0 + kk] + acc[u];
+        }
+      }
+      __syncthreads();
+      // each edge's logit over the chunk's units, four units at a time
+      for (int ed = tid; ed < edges; ed += kThreadsA) {
+        const int i = ed / (K * K), pr = (ed / K) % K, r = ed % K;
+        const uint64_t kc = sh.top[i][r];
+        if (!kc || (i == 0 && pr > 0)) continue;
+        const double M = (double)value_from_key((uint32_t)(sh.top[i][0] >> 32));
+        const double x = (double)value_from_key((uint32_t)(kc >> 32));
+        const double lp = (x - M) - sh.lz[i];
+        const double depth = (double)(i + 1), H = sh.ent[i];
+        const int ps = i == 0 ? 0 : 1 + (i - 1) * K + pr, cs = np + i * K + r;
+        double logit = c3[ed];
+        for (int kk = 0; kk < kn; kk += 4) {
+          double av[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int k = min(kk + u, kn - 1);
+            const float* w = Ws + (k0 + k) * F + 2 * d;
+            double a = part[k * S + ps] + part[k * S + cs];
+            a = a + (double)w[0] * depth;
+            a = a + (double)w[1] * lp;
+            a = a + (double)w[2] * H;
+            av[u] = a > 0.0 ? a : 0.0;
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (kk + u < kn) logit = logit + (double)Ws[h * F + h + k0 + kk + u] * av[u];
+        }
+        c3[ed] = logit;
+      }
+      __syncthreads();
+    }
+    // sibling softmax of each parent's K logits, one child per thread: the terms EXP(l - max)
+    // into the scratch area (the weights are no longer needed; D*K*K doubles fit), then the
+    // rank-order sum and the quotients.  Row 0 has only the root as parent; its other parent
+    // ranks take the root's entries.
+    double* ex = reinterpret_cast<double*>(&sh.x);
+    static_assert(sizeof(Scratch) >= kMaxLearnedEdges * sizeof(double), "terms fit the scratch");
+    for (int t = tid; t < edges; t += kThreadsA) {
+      const int pi = t / K, r = t - pi * K;
+      if (pi < K && pi > 0) continue;
+      const double* lg = c3 + (size_t)pi * K;
+      double m = -INFINITY;
+      for (int j = 0; j < K; ++j) m = fmax(m, lg[j]);   // NaN logits ignored
+      ex[t] = spec_exp(lg[r] - m);
+    }
+    __syncthreads();
+    for (int t = tid; t < edges; t += kThreadsA) {
+      const int pi = t / K, r = t - pi * K;
+      const double* e = ex + (size_t)(pi < K ? 0 : pi) * K;
+      double Z = 0.0;
+      for (int j = 0; j < K; ++j) Z = Z + e[j];
+      const bool ok = Z > 0.0 && Z <= 1.7976931348623157e308;
+      c3[t] = ok ? e[r] / Z : 0.0;
+    }
+    __syncthreads();
+  }
   // The selection proper runs on the first four waves.  The other waves end here; a
   // workgroup barrier waits only for the waves that have not ended, so the barriers
   // below synchronize the remaining four.
@@ -625,7 +830,8 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
           if (++rr == K) { rr = 0; ++pp; }
           const int pc = min(p, p1 - 1);
           const uint64_t pu = L.u[pc];
-          const double qp = L.q[pc], cr = sh.c[d][r];
+          const double qp = L.q[pc];
+          const double cr = c3 ? c3[(d * K + (L.meta[pc] & 0xFF)) * K + r] : sh.c[d][r];
           const double q = qp * cr;
           const double u = q / den1;
           const int bn = ubin(u);
@@ -745,7 +951,7 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
     }
   } else {
     __syncthreads();
-    n = select_sequential<SLOTS>(sh, D, K, N, tau);
+    n = select_sequential<SLOTS>(sh, c3, D, K, N, tau);
     Seq& S = sh.x.s;
     for (int j = tid; j < n; j += kThreads) {
       const size_t g = (size_t)b * N + S.order[j];
@@ -774,11 +980,13 @@ __global__ __launch_bounds__(256) void marginal_z_kernel(const void* __restrict_
                                                          int vocab, int K, int chunk_len,
                                                          int chunks,
                                                          const uint64_t* __restrict__ cand,
-                                                         int64_t* __restrict__ zpart) {
+                                                         int64_t* __restrict__ zpart,
+                                                         int64_t* __restrict__ spart) {
   __shared__ double s_M;
-  __shared__ int64_t s_w[4];
-  const int row = blockIdx.x / chunks;
-  const int chunk = blockIdx.x - row * chunks;
+  __shared__ int64_t s_w[4], s_s[4];
+  const int row = blockIdx.x / (chunks * kZSub);
+  const int part = blockIdx.x - row * (chunks * kZSub);   // chunk * kZSub + sub-range
+  const int chunk = part / kZSub;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   if (wave == 0) {
     uint64_t h = 0ull;
@@ -791,9 +999,10 @@ __global__ __launch_bounds__(256) void marginal_z_kernel(const void* __restrict_
   }
   __syncthreads();
   const double M = s_M;
-  const int start = chunk * chunk_len;
-  const int end = min(vocab, start + chunk_len);
-  int64_t acc = 0;
+  const int sub_len = chunk_len / kZSub;
+  const int start = chunk * chunk_len + (part - chunk * kZSub) * sub_len;
+  const int end = min(vocab, start + sub_len);
+  int64_t acc = 0, accs = 0;
   for (int e = start + tid; e < end; e += 256) {
     double x;
     if (DT == TAPS_BF16) {
@@ -802,13 +1011,23 @@ __global__ __launch_bounds__(256) void marginal_z_kernel(const void* __restrict_
     } else {
       x = (double)((const float*)marg)[(size_t)row * vocab + e];
     }
-    const double t = spec_exp(x - M);
+    const double dx = x - M;
+    const double t = spec_exp(dx);
     acc += (int64_t)rint(t * 0x1p42);
+    // the entropy's sum (learned scorer): t (x - M) on the same grid, 0 where t is 0
+    if (spart) accs += t > 0.0 ? (int64_t)rint((t * dx) * 0x1p42) : 0;
   }
   acc = wave_sum_i64(acc);
-  if (lane == 0) s_w[wave] = acc;
+  accs = wave_sum_i64(accs);
+  if (lane == 0) {
+    s_w[wave] = acc;
+    s_s[wave] = accs;
+  }
   __syncthreads();
-  if (tid == 0) zpart[(size_t)row * chunks + chunk] = s_w[0] + s_w[1] + s_w[2] + s_w[3];
+  if (tid == 0) {
+    zpart[(size_t)row * chunks * kZSub + part] = s_w[0] + s_w[1] + s_w[2] + s_w[3];
+    if (spart) spart[(size_t)row * chunks * kZSub + part] = s_s[0] + s_s[1] + s_s[2] + s_s[3];
+  }
 }
 
 }  // namespace
@@ -817,30 +1036,44 @@ double spec_exp_host(double t) { return spec_exp(t); }
 
 hipError_t launch_marginal_z(const void* marg, int dtype, int rows, int vocab, int K,
                              const TopkPlan& plan, const uint64_t* cand, int64_t* zpart,
-                             hipStream_t s) {
+                             int64_t* spart, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  const dim3 grid((unsigned)(rows * plan.chunks)), block(256);
+  const dim3 grid((unsigned)(rows * plan.chunks * kZSub)), block(256);
   if (dtype == TAPS_BF16)
     marginal_z_kernel<TAPS_BF16><<<grid, block, 0, s>>>(marg, vocab, K, plan.chunk_len,
-                                                        plan.chunks, cand, zpart);
+                                                        plan.chunks, cand, zpart, spart);
   else
     marginal_z_kernel<TAPS_FP32><<<grid, block, 0, s>>>(marg, vocab, K, plan.chunk_len,
-                                                        plan.chunks, cand, zpart);
+                                                        plan.chunks, cand, zpart, spart);
   return hipGetLastError();
 }
 
+int learned_chunk_units(int D, int K, int d, int h) { return learned_layout(D, K, d, h).KC; }
+
 hipError_t launch_select(const void* /*marg*/, const taps_select_params& p, const TopkPlan& plan,
-                         const uint64_t* cand, const int64_t* zpart, const taps_tree& out,
-                         hipStream_t s) {
+                         const uint64_t* cand, const int64_t* zpart, const int64_t* spart,
+                         const taps_tree& out, hipStream_t s) {
   dim3 grid((unsigned)p.batch), block(kThreadsA);
   const int slots = (p.budget + kWave - 1) / kWave;
   const int marginal = p.scorer == TAPS_SCORER_MARGINAL;
+  ScorerArgs mlp{};
+  size_t dyn = 0;
+  if (p.scorer == TAPS_SCORER_LEARNED) {
+    const taps_scorer_mlp& w = *p.mlp;
+    mlp = ScorerArgs{w.emb, w.W1, w.b1, w.w2, w.b2, w.root_token, w.emb_dim, w.hidden, p.vocab};
+    dyn = (size_t)p.block * p.K * p.K * sizeof(double);
+  }
 #define TAPS_SEL(SL)                                                                          \
-  select_kernel<SL><<<grid, block, 0, s>>>(p.block, p.K, p.budget, p.kind, p.lambda1,         \
-                                           p.lambda2, p.tau, p.beta, plan.chunks, marginal,   \
-                                           cand, zpart, out.parent, out.token, out.depth,     \
-                                           out.rank, out.q_reach, out.n_nodes, out.topk_idx,  \
-                                           out.topk_val)
+  do {                                                                                        \
+    if (dyn && hipFuncSetAttribute((const void*)select_kernel<SL>,                            \
+                                   hipFuncAttributeMaxDynamicSharedMemorySize,                \
+                                   (int)dyn) != hipSuccess)                                    \
+      return hipErrorInvalidValue;                                                            \
+    select_kernel<SL><<<grid, block, dyn, s>>>(                                               \
+        p.block, p.K, p.budget, p.kind, p.lambda1, p.lambda2, p.tau, p.beta, plan.chunks,     \
+        marginal, cand, zpart, spart, mlp, out.parent, out.token, out.depth, out.rank,        \
+        out.q_reach, out.n_nodes, out.topk_idx, out.topk_val);                                \
+  } while (0)
   switch (slots) {
     case 1: TAPS_SEL(1); break;
     case 2: TAPS_SEL(2); break;

@@ -75,9 +75,38 @@ def test_select_scorer_validation_and_workspace(lib):
         _lib.TAPS_ERR_UNSUPPORTED
     base = lib.taps_select_workspace_bytes(ctypes.byref(params()))
     marg = lib.taps_select_workspace_bytes(ctypes.byref(params(scorer=1)))
-    assert marg == base + 2 * 16 * 10 * 8        # one int64 partial per (row, chunk)
+    assert marg == base + 2 * 16 * 10 * 4 * 8    # four int64 partials per (row, chunk)
     probs = params(scorer=1, kind=_lib.TAPS_PROBS)
     assert lib.taps_select_workspace_bytes(ctypes.byref(probs)) == base   # no normaliser
+
+
+def test_select_learned_scorer_validation_and_workspace(lib):
+    fake = 1 << 20
+    w = _lib.ScorerMLP(fake, fake, fake, fake, 0.5, fake, 16, 32)
+
+    def p(**kw):
+        q = params(scorer=2, **kw)
+        q.mlp = ctypes.pointer(w)
+        return q
+
+    assert lib.taps_select_validate(ctypes.byref(p())) == _lib.TAPS_OK
+    assert lib.taps_select_validate(ctypes.byref(p(kind=_lib.TAPS_PROBS))) == \
+        _lib.TAPS_ERR_UNSUPPORTED
+    assert lib.taps_select_validate(ctypes.byref(p(block=32, K=16))) == \
+        _lib.TAPS_ERR_UNSUPPORTED                     # a 32 x 16 x 16 table exceeds the LDS
+    assert lib.taps_select_validate(ctypes.byref(params(scorer=2))) == \
+        _lib.TAPS_ERR_INVALID_ARG                     # no weights
+    w.emb_dim = 33
+    assert lib.taps_select_validate(ctypes.byref(p())) == _lib.TAPS_ERR_UNSUPPORTED
+    w.emb_dim, w.hidden = 16, 0
+    assert lib.taps_select_validate(ctypes.byref(p())) == _lib.TAPS_ERR_INVALID_ARG
+    w.hidden = 32
+    base = lib.taps_select_workspace_bytes(ctypes.byref(params()))
+    assert lib.taps_select_workspace_bytes(ctypes.byref(p())) == base + 2 * (2 * 16 * 10 * 4 * 8)
+    # the largest tables of each K fit the scratch area at the largest weights
+    w.emb_dim, w.hidden = 32, 64
+    for blk, k in ((32, 8), (28, 16), (32, 4)):
+        assert lib.taps_select_validate(ctypes.byref(p(block=blk, K=k))) == _lib.TAPS_OK
 
 
 def test_select_rejects_null_buffers_and_small_workspace(lib):

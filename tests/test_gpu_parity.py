@@ -131,6 +131,60 @@ def test_select_marginal_fuzz(taps, seed):
     U.assert_tree_equal(gpu, trees, cfg)
 
 
+def _learned_weights(taps, mlp):
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    return taps.ScorerWeights(emb=dev(mlp.emb), W1=dev(mlp.W1), b1=dev(mlp.b1), w2=dev(mlp.w2),
+                              b2=mlp.b2, root_token=dev(mlp.root_token))
+
+
+@pytest.mark.parametrize("name,d,h", [("qwen3_4b", 16, 32), ("qwen3_8b", 16, 32),
+                                      ("qwen3_8b", 32, 64)])
+def test_select_learned_scorer_matches_oracle(taps, name, d, h):
+    """The learned-scorer hook with seeded random weights: q_cond per (row, parent rank,
+    child rank) from the MLP and the sibling softmax; trees bit-exact."""
+    from oracle.scorer import random_scorer
+    say(f"[select-learned] {name} d={d} h={h}")
+    inp = gen_round(name, with_attention=False)
+    c = inp.cfg
+    mlp = random_scorer(np.random.default_rng(31 + d + h), c.vocab, d, h, c.batch)
+    x = inp.marginals_f64()
+    trees = [oracle.select_request(x[b], c.K, c.budget, kind=c.kind, lambda1=c.lambda1,
+                                   lambda2=c.lambda2, tau=c.tau, scorer=oracle.select.LEARNED,
+                                   mlp=mlp, req=b) for b in range(c.batch)]
+    w = _learned_weights(taps, mlp)
+    gpu, _, _ = run_select(taps, inp, scorer=2, mlp=w)
+    U.assert_tree_equal(gpu, trees, c)
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_select_learned_fuzz(taps, seed):
+    from oracle.scorer import random_scorer
+    rng = np.random.default_rng(1300 + seed)
+    dtype = [BF16, FP32][seed % 2]
+    V = int(rng.choice([17, 1001, 70001]))
+    K = min(int(rng.integers(1, 13)), V)
+    D = int(rng.integers(1, 33))
+    while D * K * K > 7168:
+        D -= 1
+    N = int(rng.choice([1, 16, 64, 200]))
+    mode = ["ties", "deep", "specials", "plain"][seed % 4]
+    d, h = int(rng.integers(1, 9)), int(rng.integers(1, 17))
+    cfg = _fuzz_cfg(rng, dtype, LOGITS, V, D, K, N)
+    say(f"[fuzz-learned] seed={seed} dtype={dtype} V={V} K={K} D={D} N={N} mode={mode} "
+        f"d={d} h={h}")
+    m = _fuzz_marginals(rng, cfg, mode)
+    mlp = random_scorer(rng, V, d, h, cfg.batch)
+    from workloads import bf16_bits_to_f32
+    x = bf16_bits_to_f32(m).astype(np.float64) if dtype == BF16 else m.astype(np.float64)
+    trees = [oracle.select_request(x[b], K, N, kind=LOGITS, scorer=oracle.select.LEARNED,
+                                   mlp=mlp, req=b) for b in range(cfg.batch)]
+    sel = taps.Selector(cfg.batch, D, V, K, N, dtype=dtype, kind=LOGITS, scorer=2,
+                        mlp=_learned_weights(taps, mlp))
+    gpu = sel(U.to_dev(m, dtype == BF16))
+    torch.cuda.synchronize()
+    U.assert_tree_equal(gpu, trees, cfg)
+
+
 @pytest.mark.parametrize("seed", range(24))
 def test_select_fuzz(taps, seed):
     rng = np.random.default_rng(500 + seed)

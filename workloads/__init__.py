@@ -230,6 +230,20 @@ def gen_round(cfg: Config | str, seed: int = BASE_SEED, with_attention: bool = T
     return RoundInputs(cfg, marg, ctx, off, p, Q, K, V, seed)
 
 
+def gen_scorer_weights(rng: np.random.Generator, vocab: int, d: int, h: int, batch: int) -> dict:
+    """Seeded random weights for the learned-scorer hook (no trained weights exist here):
+    float32 emb [vocab][d], W1 [h][2d+3], b1 [h], w2 [h], the float32 b2 and int32 root
+    tokens [batch]."""
+    F = 2 * d + 3
+    return dict(
+        emb=(rng.standard_normal((vocab, d)) * 0.5).astype(np.float32),
+        W1=(rng.standard_normal((h, F)) / np.sqrt(F)).astype(np.float32),
+        b1=(rng.standard_normal(h) * 0.1).astype(np.float32),
+        w2=(rng.standard_normal(h) / np.sqrt(h)).astype(np.float32),
+        b2=float(np.float32(rng.standard_normal() * 0.1)),
+        root_token=rng.integers(0, vocab, size=batch).astype(np.int32))
+
+
 def rank_paths(parent: np.ndarray, rank: np.ndarray, n: int) -> list[tuple[int, ...]]:
     """Rank path of every emitted node, read off parent pointers (node 0 is the root)."""
     paths: list[tuple[int, ...]] = [()]
