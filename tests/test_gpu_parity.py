@@ -185,6 +185,30 @@ def test_select_learned_fuzz(taps, seed):
     U.assert_tree_equal(gpu, trees, cfg)
 
 
+@pytest.mark.parametrize("D,K,mode", [(32, 8, "plain"), (12, 16, "deep")])
+def test_select_learned_large_tables(taps, D, K, mode):
+    """The largest weights (d = 32, h = 64) on large q_cond tables, so that the hidden units
+    are taken in several chunks, the last one shorter than 8 and 4 units; root tokens
+    outside the vocabulary (above it and negative) have zero embeddings."""
+    from oracle.scorer import random_scorer
+    rng = np.random.default_rng(1400 + D + K)
+    V, N, d, h = 70001, 128, 32, 64
+    cfg = _fuzz_cfg(rng, BF16, LOGITS, V, D, K, N)
+    say(f"[learned-large] D={D} K={K} mode={mode} d={d} h={h}")
+    m = _fuzz_marginals(rng, cfg, mode)
+    mlp = random_scorer(rng, V, d, h, cfg.batch)
+    mlp.root_token[:] = [V + 5, -3]
+    from workloads import bf16_bits_to_f32
+    x = bf16_bits_to_f32(m).astype(np.float64)
+    trees = [oracle.select_request(x[b], K, N, kind=LOGITS, scorer=oracle.select.LEARNED,
+                                   mlp=mlp, req=b) for b in range(cfg.batch)]
+    sel = taps.Selector(cfg.batch, D, V, K, N, dtype=BF16, kind=LOGITS, scorer=2,
+                        mlp=_learned_weights(taps, mlp))
+    gpu = sel(U.to_dev(m, True))
+    torch.cuda.synchronize()
+    U.assert_tree_equal(gpu, trees, cfg)
+
+
 @pytest.mark.parametrize("seed", range(24))
 def test_select_fuzz(taps, seed):
     rng = np.random.default_rng(500 + seed)
