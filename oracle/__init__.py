@@ -13,6 +13,8 @@ Layout
   walk.py       greedy acceptance walk (Sec. 1; Limitations, temperature 0)
   commit.py     KV commit of the accepted path and the emitted tokens (Sec. 1)
   scorer.py     the learned-scorer hook: MLP on edge features, sibling softmax (Sec. 4.2)
+  layer.py      one Qwen3-style attention layer over the tree: projections, per-head
+                RMSNorm, rotary positions by tree depth, tree attention, output projection
 
 Pins (what fixes each part without trusting this code) live in
 tests/test_oracle_*.py.  Parity of the oracle against the paper's own numbers
