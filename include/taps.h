@@ -12,6 +12,9 @@
  *                     path (Sec. 1: one prefix path is committed per round; Limitations).
  *   kv_commit         the round's state update: the accepted path's tree K/V rows move
  *                     to the rows right after the context, and the emitted tokens.
+ *   verify_layer      one attention layer of the target over the tree: projections,
+ *                     per-head RMSNorm, rotary positions by tree depth, tree attention,
+ *                     output projection (the verification forward's layer slice).
  *
  * Conventions shared by every call:
  *   - Pointers are DEVICE memory owned by the caller unless marked [host].
@@ -254,6 +257,52 @@ taps_status kv_commit(void *K_cache, void *V_cache, const int64_t *kv_offset,
                       int32_t budget, int32_t block, int32_t Hkv, int32_t head_dim,
                       int32_t max_ctx, int32_t dtype, int32_t *new_ctx_len,
                       int32_t *committed, int32_t *n_committed, hipStream_t stream);
+
+/* [host] Weights of one attention layer of the target, a Qwen3-style block.  DEVICE bf16
+ * arrays owned by the caller, row-major [out][in], 16-byte aligned:
+ *   Wq [Hq*head_dim][hidden], Wk and Wv [Hkv*head_dim][hidden], Wo [hidden][Hq*head_dim]
+ *   q_norm, k_norm [head_dim] per-head RMSNorm weights of the queries and keys
+ *   rope_theta  rotary base, finite and > 1 (Qwen3: 1e6)
+ *   norm_eps    RMSNorm epsilon, finite and >= 0 (Qwen3: 1e-6)
+ *   hidden      model width, a multiple of 64, at most 16384 */
+typedef struct {
+  const void *Wq, *Wk, *Wv, *Wo, *q_norm, *k_norm;
+  double rope_theta;
+  float norm_eps;
+  int32_t hidden;
+} taps_layer_weights;
+
+/* Bytes of scratch verify_layer needs (projection partials, Q, O, attention partials);
+ * 0 for sizes verify_layer rejects. */
+size_t verify_layer_workspace_bytes(int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv,
+                                    int32_t head_dim, int32_t hidden, int32_t max_ctx);
+
+/* One attention layer of the target over the selected trees: the layer slice of the
+ * verification forward (Sec. 4.1, the verification stage, and Sec. 4.3 run the target once
+ * over the tree with tree attention).  bf16 storage, fp32 accumulation.
+ *   X          [batch][budget][hidden] bf16 hidden states of the tree nodes (tree order),
+ *              16-byte aligned
+ *   w          the layer's weights (above)
+ *   K_cache,
+ *   V_cache    as for tree_verify_attn (bf16); the key and value of node i < n_nodes[b]
+ *              are written to row kv_offset[b] + ctx_len[b] + i, no other row is written
+ *   kv_offset, ctx_len, max_ctx, scale: as for tree_verify_attn
+ *   tree       parent, depth and n_nodes of the selected trees (taps_tree; other fields
+ *              are not read)
+ *   head_dim   128
+ *   Y          [batch][budget][hidden] bf16, 16-byte aligned; rows i >= n_nodes[b] are not
+ *              defined
+ *   ws         verify_layer_workspace_bytes(...) bytes, 256-byte aligned
+ * Steps: q, k, v = X W^T per node; RMSNorm of each query and key head; rotary embedding
+ * at position ctx_len[b] + depth (the root right after the context, siblings at one
+ * position; pairs (j, j + head_dim/2) turn by pos * rope_theta^(-2j/head_dim)); Q, K and
+ * V rounded to bf16; tree attention as tree_verify_attn; O rounded to bf16; Y = O Wo^T
+ * rounded to bf16. */
+taps_status verify_layer(const void *X, const taps_layer_weights *w, void *K_cache,
+                         void *V_cache, const int64_t *kv_offset, const int32_t *ctx_len,
+                         const taps_tree *tree, int32_t batch, int32_t budget, int32_t Hq,
+                         int32_t Hkv, int32_t head_dim, int32_t max_ctx, float scale, void *Y,
+                         void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* Human-readable name of a status code (static string). */
 const char *taps_status_string(int32_t status);

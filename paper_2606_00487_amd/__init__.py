@@ -12,6 +12,8 @@ memory and the current stream.
     path, path_len, bonus = walk(tree, target_tokens)                 # accept_walk
     com = KVCommit(batch, budget, block, Hkv, head_dim, max_ctx)
     new_ctx, tokens, n = com(K, V, kv_offset, ctx_len, tree, path, path_len, bonus)  # kv_commit
+    lay = VerifyLayer(batch, budget, Hq, Hkv, head_dim, hidden, max_ctx)
+    Y = lay(X, LayerWeights(Wq, Wk, Wv, Wo, q_norm, k_norm), K, V, kv_offset, ctx_len, tree)
 """
 from __future__ import annotations
 
@@ -220,3 +222,62 @@ class KVCommit:
             _ptr(path_len), _ptr(bonus), batch, budget, block, Hkv, hd, max_ctx, dtype,
             _ptr(self.new_ctx), _ptr(self.committed), _ptr(self.n_committed), _stream()))
         return self.new_ctx, self.committed, self.n_committed
+
+
+@dataclasses.dataclass
+class LayerWeights:
+    """Device bf16 weights of one attention layer (taps_layer_weights), row-major [out][in]:
+    Wq [Hq*hd][hidden], Wk and Wv [Hkv*hd][hidden], Wo [hidden][Hq*hd], q_norm and k_norm
+    [hd]."""
+    Wq: torch.Tensor
+    Wk: torch.Tensor
+    Wv: torch.Tensor
+    Wo: torch.Tensor
+    q_norm: torch.Tensor
+    k_norm: torch.Tensor
+    rope_theta: float = 1e6
+    norm_eps: float = 1e-6
+
+    def struct(self) -> _lib.LayerWeights:
+        hidden = self.Wq.shape[1]
+        for name in ("Wq", "Wk", "Wv", "Wo", "q_norm", "k_norm"):
+            _need(getattr(self, name), name, torch.bfloat16)
+        _need(self.Wo, "Wo", torch.bfloat16, (hidden, self.Wq.shape[0]))
+        return _lib.LayerWeights(_ptr(self.Wq), _ptr(self.Wk), _ptr(self.Wv), _ptr(self.Wo),
+                                 _ptr(self.q_norm), _ptr(self.k_norm), float(self.rope_theta),
+                                 float(self.norm_eps), hidden)
+
+
+class VerifyLayer:
+    """verify_layer: one attention layer of the target over the selected trees
+    (projections, per-head RMSNorm, rotary positions by tree depth, tree attention,
+    output projection)."""
+
+    def __init__(self, batch, budget, Hq, Hkv, head_dim, hidden, max_ctx, scale=None,
+                 device="cuda"):
+        self.lib = load()
+        self.scale = float(scale if scale is not None else head_dim ** -0.5)
+        self.shape = (batch, budget, Hq, Hkv, head_dim, hidden, max_ctx)
+        nbytes = self.lib.verify_layer_workspace_bytes(batch, budget, Hq, Hkv, head_dim, hidden,
+                                                       max_ctx)
+        if batch > 0 and nbytes == 0:
+            raise TapsError("verify_layer_workspace_bytes", _lib.TAPS_ERR_UNSUPPORTED)
+        self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        self.Y = torch.empty((batch, budget, hidden), dtype=torch.bfloat16, device=device)
+
+    def __call__(self, X, w: LayerWeights, K, V, kv_offset, ctx_len, tree: TreeBuffers):
+        batch, budget, Hq, Hkv, hd, hidden, max_ctx = self.shape
+        _need(X, "X", torch.bfloat16, (batch, budget, hidden))
+        _need(K, "K_cache", torch.bfloat16)
+        _need(V, "V_cache", torch.bfloat16, tuple(K.shape))
+        _need(kv_offset, "kv_offset", torch.int64, (batch,))
+        _need(ctx_len, "ctx_len", torch.int32, (batch,))
+        ws = w.struct()
+        if ws.hidden != hidden:
+            raise ValueError(f"weights: hidden {ws.hidden}, expected {hidden}")
+        st = tree.struct()
+        _lib.check(self.lib, "verify_layer", self.lib.verify_layer(
+            _ptr(X), ctypes.byref(ws), _ptr(K), _ptr(V), _ptr(kv_offset), _ptr(ctx_len),
+            ctypes.byref(st), batch, budget, Hq, Hkv, hd, max_ctx, self.scale, _ptr(self.Y),
+            _ptr(self.ws), self.ws.numel(), _stream()))
+        return self.Y

@@ -31,8 +31,15 @@ EXPORTED = [
     "taps_select_workspace_bytes", "taps_select_validate", "taps_select",
     "tree_verify_attn_workspace_bytes", "tree_verify_attn_validate", "tree_verify_attn",
     "tree_verify_attn_timed", "accept_walk", "kv_commit", "taps_status_string",
-    "taps_spec_exp_host",
+    "taps_spec_exp_host", "verify_layer_workspace_bytes", "verify_layer",
 ]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [("Wq", ctypes.c_void_p), ("Wk", ctypes.c_void_p), ("Wv", ctypes.c_void_p),
+                ("Wo", ctypes.c_void_p), ("q_norm", ctypes.c_void_p), ("k_norm", ctypes.c_void_p),
+                ("rope_theta", ctypes.c_double), ("norm_eps", ctypes.c_float),
+                ("hidden", ctypes.c_int32)]
 
 
 class ScorerMLP(ctypes.Structure):
@@ -98,6 +105,11 @@ def load(path: str = LIB_PATH):
     lib.kv_commit.argtypes = [vp, vp, vp, vp, P(Tree), vp, vp, vp, i32, i32, i32, i32, i32, i32,
                               i32, vp, vp, vp, vp]
     lib.kv_commit.restype = i32
+    lib.verify_layer_workspace_bytes.argtypes = [i32] * 7
+    lib.verify_layer_workspace_bytes.restype = ctypes.c_size_t
+    lib.verify_layer.argtypes = [vp, P(LayerWeights), vp, vp, vp, vp, P(Tree), i32, i32, i32, i32,
+                                 i32, i32, ctypes.c_float, vp, vp, ctypes.c_size_t, vp]
+    lib.verify_layer.restype = i32
     lib.taps_status_string.argtypes = [i32]
     lib.taps_status_string.restype = ctypes.c_char_p
     lib.taps_spec_exp_host.argtypes = [f64]

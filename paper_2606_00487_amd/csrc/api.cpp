@@ -1,4 +1,5 @@
 // C ABI entry points: host-side validation, workspace sizing and kernel dispatch.
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 
@@ -69,6 +70,34 @@ taps_status attn_check(int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv, i
   if ((int64_t)budget * Hq * hd * 2 >= ((int64_t)1 << 31)) return TAPS_ERR_UNSUPPORTED;
   // one split's K or V rows, with the kernel's look-ahead, must span < 2^31 bytes
   if ((int64_t)Hkv * hd * 2 * 6 * 64 >= ((int64_t)1 << 31)) return TAPS_ERR_UNSUPPORTED;
+  return TAPS_OK;
+}
+
+struct LayerWs {
+  size_t part, q, o, attn, total;
+};
+
+LayerWs layer_ws(int batch, int budget, int Hq, int Hkv, int hd, int hidden, int max_ctx) {
+  const int M = batch * budget, Nqkv = (Hq + 2 * Hkv) * hd;
+  const GemmPlan a = plan_gemm(M, Nqkv, hidden), o = plan_gemm(M, hidden, Hq * hd);
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  LayerWs w;
+  w.part = al(std::max((size_t)a.splits * M * Nqkv, (size_t)o.splits * M * hidden) * 4);
+  w.q = al((size_t)M * Hq * hd * 2);
+  w.o = w.q;
+  w.attn = al(tree_verify_attn_workspace_bytes(batch, budget, Hq, Hkv, hd, max_ctx, TAPS_BF16));
+  w.total = w.part + w.q + w.o + w.attn;
+  return w;
+}
+
+taps_status layer_check(int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv, int32_t hd,
+                        int32_t hidden, int32_t max_ctx, float scale) {
+  const taps_status st = attn_check(batch, budget, Hq, Hkv, hd, max_ctx, TAPS_BF16, scale);
+  if (st != TAPS_OK) return st;
+  if (hd != 128) return TAPS_ERR_UNSUPPORTED;
+  if (hidden < 64 || hidden % 64 != 0) return TAPS_ERR_INVALID_ARG;
+  if (hidden > 16384) return TAPS_ERR_UNSUPPORTED;
+  if ((int64_t)batch * budget > ((int64_t)1 << 20)) return TAPS_ERR_UNSUPPORTED;
   return TAPS_OK;
 }
 
@@ -228,6 +257,62 @@ taps_status kv_commit(void* K_cache, void* V_cache, const int64_t* kv_offset,
                        committed, n_committed, stream) == hipSuccess
              ? TAPS_OK
              : TAPS_ERR_HIP;
+}
+
+size_t verify_layer_workspace_bytes(int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv,
+                                    int32_t head_dim, int32_t hidden, int32_t max_ctx) {
+  if (layer_check(batch, budget, Hq, Hkv, head_dim, hidden, max_ctx, 1.0f) != TAPS_OK ||
+      batch == 0)
+    return 0;
+  return layer_ws(batch, budget, Hq, Hkv, head_dim, hidden, max_ctx).total;
+}
+
+taps_status verify_layer(const void* X, const taps_layer_weights* w, void* K_cache,
+                         void* V_cache, const int64_t* kv_offset, const int32_t* ctx_len,
+                         const taps_tree* tree, int32_t batch, int32_t budget, int32_t Hq,
+                         int32_t Hkv, int32_t head_dim, int32_t max_ctx, float scale, void* Y,
+                         void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!w) return TAPS_ERR_INVALID_ARG;
+  const taps_status st = layer_check(batch, budget, Hq, Hkv, head_dim, w->hidden, max_ctx, scale);
+  if (st != TAPS_OK) return st;
+  if (!std::isfinite(w->rope_theta) || !(w->rope_theta > 1.0)) return TAPS_ERR_INVALID_ARG;
+  if (!std::isfinite(w->norm_eps) || w->norm_eps < 0.f) return TAPS_ERR_INVALID_ARG;
+  if (batch == 0) return TAPS_OK;
+  if (!X || !Y || !K_cache || !V_cache || !kv_offset || !ctx_len || !tree || !tree->parent ||
+      !tree->depth || !tree->n_nodes || !w->Wq || !w->Wk || !w->Wv || !w->Wo || !w->q_norm ||
+      !w->k_norm)
+    return TAPS_ERR_INVALID_ARG;
+  const uintptr_t a16 = (uintptr_t)X | (uintptr_t)Y | (uintptr_t)K_cache | (uintptr_t)V_cache |
+                        (uintptr_t)w->Wq | (uintptr_t)w->Wk | (uintptr_t)w->Wv | (uintptr_t)w->Wo;
+  if ((a16 & 15) != 0 || (((uintptr_t)w->q_norm | (uintptr_t)w->k_norm) & 1) != 0)
+    return TAPS_ERR_INVALID_ARG;
+  const int hidden = w->hidden;
+  const LayerWs L = layer_ws(batch, budget, Hq, Hkv, head_dim, hidden, max_ctx);
+  if (!ws || ws_bytes < L.total || ((uintptr_t)ws & 255) != 0) return TAPS_ERR_WORKSPACE;
+  const int M = batch * budget, Nq = Hq * head_dim, Nk = Hkv * head_dim;
+  float* part = (float*)ws;
+  char* Q = (char*)ws + L.part;
+  char* O = Q + L.q;
+  char* aws = O + L.o;
+  const GemmPlan a = plan_gemm(M, Nq + 2 * Nk, hidden);
+  if (launch_gemm_bf16(X, M, hidden, w->Wq, Nq, w->Wk, Nk, w->Wv, Nk, a, part, stream) !=
+      hipSuccess)
+    return TAPS_ERR_HIP;
+  if (launch_qkv_rope(part, a.splits, batch, budget, Hq, Hkv, w->q_norm, w->k_norm,
+                      w->rope_theta, w->norm_eps, kv_offset, ctx_len, tree->depth,
+                      tree->n_nodes, max_ctx, Q, K_cache, V_cache, stream) != hipSuccess)
+    return TAPS_ERR_HIP;
+  const AttnPlan pl = plan_attn(batch, budget, Hq, Hkv, head_dim, max_ctx);
+  if (launch_attn_bf16(Q, K_cache, V_cache, kv_offset, ctx_len, tree->parent, tree->n_nodes,
+                       batch, budget, Hq, Hkv, head_dim, max_ctx, scale, pl, O, aws,
+                       stream) != hipSuccess)
+    return TAPS_ERR_HIP;
+  const GemmPlan o = plan_gemm(M, hidden, Nq);
+  if (launch_gemm_bf16(O, M, Nq, w->Wo, hidden, nullptr, 0, nullptr, 0, o, part, stream) !=
+      hipSuccess)
+    return TAPS_ERR_HIP;
+  return launch_reduce_bf16(part, o.splits, M, hidden, Y, stream) == hipSuccess ? TAPS_OK
+                                                                                : TAPS_ERR_HIP;
 }
 
 }  // extern "C"

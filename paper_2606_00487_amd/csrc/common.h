@@ -87,6 +87,24 @@ hipError_t launch_commit(void* K, void* V, const int64_t* off, const int32_t* ct
                          int head_dim, int elem_bytes, int max_ctx, int32_t* new_ctx,
                          int32_t* committed, int32_t* n_committed, hipStream_t s);
 
+// Layer slice: split-K skinny GEMM (fp32 partials [splits][M][N]), the projection
+// epilogue (RMSNorm, rotary positions, bf16 Q and cache rows) and the output reduction
+struct GemmPlan {
+  int splits;   // K splits (partials), each a multiple of 64 K values
+  int unroll;   // 16-value MFMA steps per load batch
+};
+GemmPlan plan_gemm(int M, int N, int K);
+hipError_t launch_gemm_bf16(const void* X, int M, int K, const void* w0, int n0, const void* w1,
+                            int n1, const void* w2, int n2, const GemmPlan& p, float* part,
+                            hipStream_t s);
+hipError_t launch_qkv_rope(const float* part, int splits, int batch, int budget, int Hq, int Hkv,
+                           const void* q_norm, const void* k_norm, double theta, float eps,
+                           const int64_t* off, const int32_t* ctx, const int32_t* depth,
+                           const int32_t* n, int max_ctx, void* Q, void* Kc, void* Vc,
+                           hipStream_t s);
+hipError_t launch_reduce_bf16(const float* part, int splits, int M, int N, void* Y,
+                              hipStream_t s);
+
 double spec_exp_host(double t);
 
 }  // namespace taps
