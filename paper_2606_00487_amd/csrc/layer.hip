@@ -59,19 +59,33 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
   f32x16 acc0, acc1;
 #pragma unroll
   for (int v = 0; v < 16; ++v) acc0[v] = acc1[v] = 0.f;
-  for (int k = 0; k < kper; k += 16 * U) {
-    bf16x8 wv[U], a0[U], a1[U];
+  // two register batches of U steps: the next batch's loads are in flight while the
+  // current one feeds the MFMAs
+  bf16x8 wA[U], xA0[U], xA1[U], wB[U], xB0[U], xB1[U];
+  auto load = [&](bf16x8 (&w)[U], bf16x8 (&y0)[U], bf16x8 (&y1)[U], int k)
+      __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      wv[u] = *(const bf16x8*)(wp + k + 16 * u);
-      a0[u] = *(const bf16x8*)(x0 + k + 16 * u);
-      a1[u] = *(const bf16x8*)(x1 + k + 16 * u);
+      w[u] = *(const bf16x8*)(wp + k + 16 * u);
+      y0[u] = *(const bf16x8*)(x0 + k + 16 * u);
+      y1[u] = *(const bf16x8*)(x1 + k + 16 * u);
     }
+  };
+  auto mma = [&](const bf16x8 (&w)[U], const bf16x8 (&y0)[U], const bf16x8 (&y1)[U])
+      __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[u], wv[u], acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[u], wv[u], acc1, 0, 0, 0);
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y0[u], w[u], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y1[u], w[u], acc1, 0, 0, 0);
     }
+  };
+  load(wA, xA0, xA1, 0);
+  for (int k = 0; k < kper; k += 32 * U) {
+    const bool second = k + 16 * U < kper;
+    if (second) load(wB, xB0, xB1, k + 16 * U);
+    mma(wA, xA0, xA1);
+    if (k + 32 * U < kper) load(wA, xA0, xA1, k + 32 * U);
+    if (second) mma(wB, xB0, xB1);
   }
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
@@ -89,9 +103,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
   }
 }
 
-// One workgroup per tree node (row = b * budget + i); wave w takes heads w, w + 4, ...
-// of the Hq query, Hkv key and Hkv value heads.  head_dim 128: lane l holds dims l and
-// l + 64, which are the rotary pair.
+// One wave per (tree node, head): blockIdx.x is the node (row = b * budget + i), and
+// wave w of workgroup blockIdx.y takes head 4 blockIdx.y + w of the Hq query, Hkv key and
+// Hkv value heads.  head_dim 128: lane l holds dims l and l + 64, the rotary pair.
 __global__ __launch_bounds__(256) void qkv_rope_kernel(
     const float* __restrict__ part, int splits, int M, int budget, int Hq, int Hkv,
     const uint16_t* __restrict__ q_norm, const uint16_t* __restrict__ k_norm, double theta,
@@ -105,6 +119,8 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(
   const int ctx = min(max(ctxp[b], 0), max_ctx);
   const int pos = ctx + max(depthp[(size_t)b * budget + i], 0);
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int hs = blockIdx.y * 4 + wave;
+  if (hs >= Hq + 2 * Hkv) return;
   const int N = (Hq + 2 * Hkv) * HD;
   const size_t crow = (size_t)(off[b] + ctx + i) * Hkv;   // first head of the node's cache row
   // rotation of the pair (lane, lane + 64) at this position, from fp64 angles
@@ -112,7 +128,7 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(
   double sd, cd;
   sincos(ang, &sd, &cd);
   const float sn = (float)sd, cs = (float)cd;
-  for (int hs = wave; hs < Hq + 2 * Hkv; hs += 4) {
+  {
     float x0 = 0.f, x1 = 0.f;
     for (int s = 0; s < splits; ++s) {
       const float* pr = part + ((size_t)s * M + row) * N + (size_t)hs * HD;
@@ -123,7 +139,7 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(
       const size_t o = (crow + (hs - Hq - Hkv)) * HD;
       Vc[o + lane] = f32_to_bf16(x0);
       Vc[o + lane + 64] = f32_to_bf16(x1);
-      continue;
+      return;
     }
     float ss = x0 * x0 + x1 * x1;
 #pragma unroll
@@ -164,7 +180,7 @@ GemmPlan plan_gemm(int M, int N, int K) {
   p.splits = 1;
   while (p.splits < 16 && tiles * p.splits < 512 && K % (2 * p.splits * 64) == 0) p.splits *= 2;
   const int steps = K / (p.splits * 4 * 16);
-  p.unroll = 8;
+  p.unroll = 4;   // two batches of 4 steps in registers keep two waves per SIMD
   while (steps % p.unroll) p.unroll /= 2;
   return p;
 }
@@ -177,7 +193,6 @@ hipError_t launch_gemm_bf16(const void* X, int M, int K, const void* w0, int n0,
   const dim3 grid((unsigned)(N / 32), (unsigned)p.splits, (unsigned)((M + 63) / 64));
   const uint16_t* x = (const uint16_t*)X;
   switch (p.unroll) {
-    case 8: gemm_kernel<8><<<grid, 256, 0, s>>>(x, M, K, ws, N, p.splits, part); break;
     case 4: gemm_kernel<4><<<grid, 256, 0, s>>>(x, M, K, ws, N, p.splits, part); break;
     case 2: gemm_kernel<2><<<grid, 256, 0, s>>>(x, M, K, ws, N, p.splits, part); break;
     default: gemm_kernel<1><<<grid, 256, 0, s>>>(x, M, K, ws, N, p.splits, part); break;
@@ -191,7 +206,8 @@ hipError_t launch_qkv_rope(const float* part, int splits, int batch, int budget,
                            const int32_t* n, int max_ctx, void* Q, void* Kc, void* Vc,
                            hipStream_t s) {
   const int M = batch * budget;
-  qkv_rope_kernel<<<M, 256, 0, s>>>(part, splits, M, budget, Hq, Hkv, (const uint16_t*)q_norm,
+  const dim3 grid((unsigned)M, (unsigned)((Hq + 2 * Hkv + 3) / 4));
+  qkv_rope_kernel<<<grid, 256, 0, s>>>(part, splits, M, budget, Hq, Hkv, (const uint16_t*)q_norm,
                                     (const uint16_t*)k_norm, theta, eps, off, ctx, depth, n,
                                     max_ctx, (uint16_t*)Q, (uint16_t*)Kc, (uint16_t*)Vc);
   return hipGetLastError();
