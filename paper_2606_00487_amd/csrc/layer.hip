@@ -38,68 +38,82 @@ struct WSeg {
   int end0, end1;
 };
 
-template <int U>
+template <int U, int NB>
 __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ X, int M, int K,
                                                    WSeg ws, int N, int splits,
                                                    float* __restrict__ part) {
   __shared__ float red[4][2][16][kWave];
-  const int c0 = blockIdx.x * 32, split = blockIdx.y, m0 = blockIdx.z * 64;
+  const int c0 = blockIdx.x * 32 * NB, split = blockIdx.y, m0 = blockIdx.z * 64;
   const uint16_t* W = c0 < ws.end0 ? ws.w0 + (size_t)c0 * K
                       : c0 < ws.end1 ? ws.w1 + (size_t)(c0 - ws.end0) * K
                                      : ws.w2 + (size_t)(c0 - ws.end1) * K;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int l32 = lane & 31, hl = lane >> 5;
-  const int kper = K / (splits * 4);                 // K values per wave, a multiple of 16 U
+  const int kper = K / (splits * 4);                 // K values per wave, a multiple of 32 U
   const int kb = split * (K / splits) + wave * kper + 8 * hl;
   // MFMA operands: lane (l32, hl) holds 8 consecutive K values at 8 hl of each 16-value
-  // step, of output row l32 (X) and of output column l32 (W); rows past M repeat row M-1
+  // step, of output row l32 (X) and of output column l32 of each 32-column block (W);
+  // rows past M repeat row M-1
   const uint16_t* wp = W + (size_t)l32 * K + kb;
+  const size_t wnb = (size_t)32 * K;                 // next 32-column block
   const uint16_t* x0 = X + (size_t)min(m0 + l32, M - 1) * K + kb;
   const uint16_t* x1 = X + (size_t)min(m0 + 32 + l32, M - 1) * K + kb;
-  f32x16 acc0, acc1;
+  f32x16 acc[2][NB];
 #pragma unroll
-  for (int v = 0; v < 16; ++v) acc0[v] = acc1[v] = 0.f;
+  for (int r = 0; r < 2; ++r)
+#pragma unroll
+    for (int c = 0; c < NB; ++c)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[r][c][v] = 0.f;
   // two register batches of U steps: the next batch's loads are in flight while the
   // current one feeds the MFMAs
-  bf16x8 wA[U], xA0[U], xA1[U], wB[U], xB0[U], xB1[U];
-  auto load = [&](bf16x8 (&w)[U], bf16x8 (&y0)[U], bf16x8 (&y1)[U], int k)
-      __attribute__((always_inline)) {
+  bf16x8 wA[NB][U], xA[2][U], wB[NB][U], xB[2][U];
+  auto load = [&](bf16x8 (&w)[NB][U], bf16x8 (&y)[2][U], int k) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      w[u] = *(const bf16x8*)(wp + k + 16 * u);
-      y0[u] = *(const bf16x8*)(x0 + k + 16 * u);
-      y1[u] = *(const bf16x8*)(x1 + k + 16 * u);
+#pragma unroll
+      for (int c = 0; c < NB; ++c) w[c][u] = *(const bf16x8*)(wp + c * wnb + k + 16 * u);
+      y[0][u] = *(const bf16x8*)(x0 + k + 16 * u);
+      y[1][u] = *(const bf16x8*)(x1 + k + 16 * u);
     }
   };
-  auto mma = [&](const bf16x8 (&w)[U], const bf16x8 (&y0)[U], const bf16x8 (&y1)[U])
+  auto mma = [&](const bf16x8 (&w)[NB][U], const bf16x8 (&y)[2][U])
       __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y0[u], w[u], acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y1[u], w[u], acc1, 0, 0, 0);
-    }
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int c = 0; c < NB; ++c)
+#pragma unroll
+        for (int r = 0; r < 2; ++r)
+          acc[r][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y[r][u], w[c][u], acc[r][c], 0, 0, 0);
   };
-  load(wA, xA0, xA1, 0);
+  load(wA, xA, 0);
   for (int k = 0; k < kper; k += 32 * U) {
     const bool second = k + 16 * U < kper;
-    if (second) load(wB, xB0, xB1, k + 16 * U);
-    mma(wA, xA0, xA1);
-    if (k + 32 * U < kper) load(wA, xA0, xA1, k + 32 * U);
-    if (second) mma(wB, xB0, xB1);
+    if (second) load(wB, xB, k + 16 * U);
+    mma(wA, xA);
+    if (k + 32 * U < kper) load(wA, xA, k + 32 * U);
+    if (second) mma(wB, xB);
   }
+  // the four waves' partials are added in LDS in a fixed order, one 32-column block at a
+  // time; accumulator element v of lane l is row 8 (v / 4) + 4 (l / 32) + v % 4, column
+  // l % 32
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    red[wave][0][v][lane] = acc0[v];
-    red[wave][1][v][lane] = acc1[v];
-  }
-  __syncthreads();
-  // accumulator element v of lane l is row 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32
-  for (int e = tid; e < 2 * 16 * kWave; e += 256) {
-    const int ln = e & (kWave - 1), v = (e / kWave) & 15, rb = e / (16 * kWave);
-    const float s = ((red[0][rb][v][ln] + red[1][rb][v][ln]) + red[2][rb][v][ln]) +
-                    red[3][rb][v][ln];
-    const int row = m0 + rb * 32 + 8 * (v >> 2) + 4 * (ln >> 5) + (v & 3);
-    if (row < M) part[((size_t)split * M + row) * N + c0 + (ln & 31)] = s;
+  for (int c = 0; c < NB; ++c) {
+    if (c > 0) __syncthreads();
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      red[wave][0][v][lane] = acc[0][c][v];
+      red[wave][1][v][lane] = acc[1][c][v];
+    }
+    __syncthreads();
+    for (int e = tid; e < 2 * 16 * kWave; e += 256) {
+      const int ln = e & (kWave - 1), v = (e / kWave) & 15, rb = e / (16 * kWave);
+      const float sum = ((red[0][rb][v][ln] + red[1][rb][v][ln]) + red[2][rb][v][ln]) +
+                        red[3][rb][v][ln];
+      const int row = m0 + rb * 32 + 8 * (v >> 2) + 4 * (ln >> 5) + (v & 3);
+      if (row < M) part[((size_t)split * M + row) * N + c0 + 32 * c + (ln & 31)] = sum;
+    }
   }
 }
 
@@ -176,11 +190,13 @@ __global__ __launch_bounds__(256) void reduce_kernel(const float* __restrict__ p
 
 GemmPlan plan_gemm(int M, int N, int K) {
   GemmPlan p;
-  const long long tiles = (long long)(N / 32) * ((M + 63) / 64);
+  // 64 columns per workgroup halve the re-reads of X against 32; N is a multiple of 64
+  p.cols = N % 64 == 0 ? 64 : 32;
+  const long long tiles = (long long)(N / p.cols) * ((M + 63) / 64);
   p.splits = 1;
-  while (p.splits < 16 && tiles * p.splits < 512 && K % (2 * p.splits * 64) == 0) p.splits *= 2;
+  while (p.splits < 16 && tiles * p.splits < 384 && K % (2 * p.splits * 64) == 0) p.splits *= 2;
   const int steps = K / (p.splits * 4 * 16);
-  p.unroll = 4;   // two batches of 4 steps in registers keep two waves per SIMD
+  p.unroll = p.cols == 64 ? 2 : 4;   // two batches in registers keep two waves per SIMD
   while (steps % p.unroll) p.unroll /= 2;
   return p;
 }
@@ -190,13 +206,22 @@ hipError_t launch_gemm_bf16(const void* X, int M, int K, const void* w0, int n0,
                             hipStream_t s) {
   const WSeg ws{(const uint16_t*)w0, (const uint16_t*)w1, (const uint16_t*)w2, n0, n0 + n1};
   const int N = n0 + n1 + n2;
-  const dim3 grid((unsigned)(N / 32), (unsigned)p.splits, (unsigned)((M + 63) / 64));
+  const dim3 grid((unsigned)(N / p.cols), (unsigned)p.splits, (unsigned)((M + 63) / 64));
   const uint16_t* x = (const uint16_t*)X;
-  switch (p.unroll) {
-    case 4: gemm_kernel<4><<<grid, 256, 0, s>>>(x, M, K, ws, N, p.splits, part); break;
-    case 2: gemm_kernel<2><<<grid, 256, 0, s>>>(x, M, K, ws, N, p.splits, part); break;
-    default: gemm_kernel<1><<<grid, 256, 0, s>>>(x, M, K, ws, N, p.splits, part); break;
+#define TAPS_GEMM(UU, NBB) gemm_kernel<UU, NBB><<<grid, 256, 0, s>>>(x, M, K, ws, N, p.splits, part)
+  if (p.cols == 64) {
+    switch (p.unroll) {
+      case 2: TAPS_GEMM(2, 2); break;
+      default: TAPS_GEMM(1, 2); break;
+    }
+  } else {
+    switch (p.unroll) {
+      case 4: TAPS_GEMM(4, 1); break;
+      case 2: TAPS_GEMM(2, 1); break;
+      default: TAPS_GEMM(1, 1); break;
+    }
   }
+#undef TAPS_GEMM
   return hipGetLastError();
 }
 
