@@ -202,3 +202,38 @@ def test_library_exponential_matches_oracle_bitwise(lib):
         a, b = lib.taps_spec_exp_host(float(t)), spec_exp(float(t))
         assert a == b or (math.isnan(a) and math.isnan(b)), (t, a, b)
         assert np.float64(a).view(np.int64) == np.float64(b).view(np.int64), t
+
+
+def test_layer_validation_and_workspace(lib):
+    fake = 1 << 20          # aligned, never dereferenced: every case stops before a launch
+    t = _lib.Tree(fake, fake, fake, fake, fake, fake, fake, fake)
+    w = _lib.LayerWeights(fake, fake, fake, fake, fake, fake, 1e6, 1e-6, 4096)
+    ws_need = lib.verify_layer_workspace_bytes(1, 64, 32, 8, 128, 4096, 8192)
+    assert ws_need > 2 * 64 * 32 * 128 * 2          # at least Q and O in bf16
+    assert lib.verify_layer_workspace_bytes(0, 64, 32, 8, 128, 4096, 8192) == 0
+    assert lib.verify_layer_workspace_bytes(1, 64, 32, 8, 64, 4096, 8192) == 0    # head_dim 128
+    assert lib.verify_layer_workspace_bytes(1, 64, 32, 8, 128, 4000, 8192) == 0   # hidden % 64
+
+    def call(batch=1, hidden=4096, hd=128, scale=0.088, ws=fake, ws_bytes=ws_need, X=fake,
+             tree=ctypes.byref(t), weights=None):
+        w.hidden = hidden
+        return lib.verify_layer(X, weights if weights is not None else ctypes.byref(w), fake,
+                                fake, fake, fake, tree, batch, 64, 32, 8, hd, 8192, scale,
+                                fake, ws, ws_bytes, None)
+
+    assert call(batch=0) == _lib.TAPS_OK
+    assert call(hidden=4000) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(hidden=32768) == _lib.TAPS_ERR_UNSUPPORTED
+    assert call(hd=64) == _lib.TAPS_ERR_UNSUPPORTED
+    assert call(scale=0.0) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(X=fake + 8) == _lib.TAPS_ERR_INVALID_ARG            # misaligned
+    assert call(X=None) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(tree=None) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(ws_bytes=ws_need - 1) == _lib.TAPS_ERR_WORKSPACE
+    assert call(ws=fake + 16) == _lib.TAPS_ERR_WORKSPACE             # 256-byte aligned
+    w.rope_theta = 1.0
+    assert call() == _lib.TAPS_ERR_INVALID_ARG
+    w.rope_theta, w.norm_eps = 1e6, float("nan")
+    assert call() == _lib.TAPS_ERR_INVALID_ARG
+    w.norm_eps, w.Wo = 1e-6, None
+    assert call() == _lib.TAPS_ERR_INVALID_ARG
