@@ -194,7 +194,7 @@ GemmPlan plan_gemm(int M, int N, int K) {
   p.cols = N % 64 == 0 ? 64 : 32;
   const long long tiles = (long long)(N / p.cols) * ((M + 63) / 64);
   p.splits = 1;
-  while (p.splits < 16 && tiles * p.splits < 384 && K % (2 * p.splits * 64) == 0) p.splits *= 2;
+  while (p.splits < 16 && tiles * p.splits < 256 && K % (2 * p.splits * 64) == 0) p.splits *= 2;
   const int steps = K / (p.splits * 4 * 16);
   p.unroll = p.cols == 64 ? 2 : 4;   // two batches in registers keep two waves per SIMD
   while (steps % p.unroll) p.unroll /= 2;
