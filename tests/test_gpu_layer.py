@@ -139,3 +139,39 @@ def test_layer_qwen3_8b_shape(taps):
     picks = sorted({0, 63, *[int(x) for x in rng.integers(1, 63, 6)]})
     _run(taps, rng, B=1, N=64, H=4096, Hq=32, Hkv=8, ctx=[8192], n=[64],
          sample_nodes=lambda b: picks)
+
+
+def test_layer_graph_replays_match_eager(taps):
+    """verify_layer captured in a HIP graph: three replays, with eager work and
+    synchronisations between them, each give the eager output bit for bit."""
+    rng = np.random.default_rng(9)
+    B, N, H, Hq, Hkv, hd, ctx = 2, 16, 256, 4, 2, 128, 40
+    dev = lambda *s, sc=1.0: _to_dev(_bf16(rng, *s, scale=sc), torch.bfloat16)
+    w = taps.LayerWeights(dev(Hq * hd, H, sc=H ** -0.5), dev(Hkv * hd, H, sc=H ** -0.5),
+                          dev(Hkv * hd, H, sc=H ** -0.5), dev(H, Hq * hd, sc=(Hq * hd) ** -0.5),
+                          dev(hd), dev(hd))
+    rows = B * (ctx + N)
+    K, V = dev(rows, Hkv, hd), dev(rows, Hkv, hd)
+    off = torch.tensor([0, ctx + N], dtype=torch.int64, device="cuda")
+    cl = torch.full((B,), ctx, dtype=torch.int32, device="cuda")
+    tree = taps.TreeBuffers.empty(B, 1, 1, N)
+    p, d = _tree(rng, N, N)
+    tree.parent.copy_(torch.from_numpy(np.stack([p, p])))
+    tree.depth.copy_(torch.from_numpy(np.stack([d, d])))
+    tree.n_nodes.fill_(N)
+    X = dev(B, N, H)
+    lay = taps.VerifyLayer(B, N, Hq, Hkv, hd, H, ctx)
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        want = lay(X, w, K, V, off, cl, tree).clone()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            lay(X, w, K, V, off, cl, tree)
+        for rep in range(3):
+            lay.Y.zero_()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(lay.Y[:, :N], want[:, :N]), f"replay {rep}"
+            _ = (X.float() * 2).sum().item()          # eager work between replays
