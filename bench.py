@@ -15,7 +15,9 @@ Prints one JSON line.  ``value`` is rounds/s (requests x steps per second);
 with HIP events around that kernel alone in a separate pass of the same
 launches; ``cpu_baseline`` times the CPU oracle on a bounded sample.  The
 round's state update (kv_commit of the accepted path) is not part of the step;
-``stages_us.kv_commit`` and ``kv_commit`` report it from its own timed pass.
+``stages_us.kv_commit`` and ``kv_commit`` report it from its own timed pass.  ``layer``
+reports one attention layer of the target over the tree (verify_layer, hidden = Hq x
+head_dim, seeded random bf16 weights), also timed on its own and not part of the step.
 """
 from __future__ import annotations
 
@@ -287,6 +289,46 @@ def main():
             c1.record(stream)
             torch.cuda.synchronize()
             commit_us.append(c0.elapsed_time(c1) * 1e3 / (3 * CR))
+        # ---------------- one attention layer of the target over the tree (verify_layer),
+        # Qwen3-style with hidden = Hq * head_dim and seeded random bf16 weights, timed on its
+        # own like kv_commit; it rewrites the tree rows of the cache with its own keys and
+        # values, so it runs last.
+        layer_us, layer_b = [], []
+        if bf and cfg.head_dim == 128:
+            H = cfg.Hq * cfg.head_dim
+            gen = torch.Generator(device=dev)
+            gen.manual_seed(20260603)
+
+            def rnd(*shape, scale=1.0):
+                return (torch.randn(*shape, generator=gen, device=dev) * scale).to(torch.bfloat16)
+
+            hd = cfg.head_dim
+            lw = taps.LayerWeights(rnd(cfg.Hq * hd, H, scale=H ** -0.5),
+                                   rnd(cfg.Hkv * hd, H, scale=H ** -0.5),
+                                   rnd(cfg.Hkv * hd, H, scale=H ** -0.5),
+                                   rnd(H, cfg.Hq * hd, scale=(cfg.Hq * hd) ** -0.5),
+                                   (1 + 0.1 * torch.randn(hd, generator=gen, device=dev)).to(torch.bfloat16),
+                                   (1 + 0.1 * torch.randn(hd, generator=gen, device=dev)).to(torch.bfloat16))
+            lay = taps.VerifyLayer(cfg.batch, cfg.budget, cfg.Hq, cfg.Hkv, hd, H, max_ctx,
+                                   scale=cfg.scale)
+            Xl = rnd(cfg.batch, cfg.budget, H)
+            w_bytes = 2 * H * (cfg.Hq + 2 * cfg.Hkv) * hd + 2 * H * cfg.Hq * hd
+            LR = 10
+            for sl in sets[:3]:
+                p = algorithmic_bytes(cfg, sl["inp"].ctx_len, sl["n"])
+                layer_b.append(w_bytes + 4 * cfg.batch * cfg.budget * H + p[1] + p[2])
+                gl = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(gl, stream=stream):
+                    for _ in range(LR):
+                        lay(Xl, lw, sl["K"], sl["V"], sl["off"], sl["ctx"], sl["tree"])
+                gl.replay()
+                c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                c0.record(stream)
+                for _ in range(3):
+                    gl.replay()
+                c1.record(stream)
+                torch.cuda.synchronize()
+                layer_us.append(c0.elapsed_time(c1) * 1e3 / (3 * LR))
     t_commit = float(np.mean(commit_us))
     commit_b = float(np.mean(commit_bytes))
     t_sel = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e3
@@ -336,6 +378,12 @@ def main():
         "kv_commit": {"bytes_per_launch": int(commit_b),
                       "achieved_gbs": round(commit_b / (t_commit * 1e-6) / 1e9, 1),
                       "avg_launch_us": round(t_commit, 3)},
+        "layer": None if not layer_us else {
+            "what": f"one attention layer over the tree: hidden {cfg.Hq * cfg.head_dim}, "
+                    "projections + RMSNorm + rotary + tree attention + output projection",
+            "bytes_per_launch": int(np.mean(layer_b)),
+            "achieved_gbs": round(float(np.mean(layer_b)) / (float(np.mean(layer_us)) * 1e-6) / 1e9, 1),
+            "avg_launch_us": round(float(np.mean(layer_us)), 3)},
         "roofline": {
             "bound": "hbm",
             "kernel": "attn_bf16_kernel" if bf else "attn_f32_kernel",
