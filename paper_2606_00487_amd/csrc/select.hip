@@ -1002,7 +1002,10 @@ __global__ __launch_bounds__(256) void marginal_z_kernel(const void* __restrict_
   const int sub_len = chunk_len / kZSub;
   const int start = chunk * chunk_len + (part - chunk * kZSub) * sub_len;
   const int end = min(vocab, start + sub_len);
-  int64_t acc = 0, accs = 0;
+  // The terms are integers (multiples of 2^-42 scaled by 2^42) below 2^42 in magnitude,
+  // and a thread adds at most 64 of them, so fp64 holds its sums exactly; they become
+  // int64 once per thread.
+  double accd = 0.0, accsd = 0.0;
   for (int e = start + tid; e < end; e += 256) {
     double x;
     if (DT == TAPS_BF16) {
@@ -1013,12 +1016,12 @@ __global__ __launch_bounds__(256) void marginal_z_kernel(const void* __restrict_
     }
     const double dx = x - M;
     const double t = spec_exp(dx);
-    acc += (int64_t)rint(t * 0x1p42);
+    accd += rint(t * 0x1p42);
     // the entropy's sum (learned scorer): t (x - M) on the same grid, 0 where t is 0
-    if (spart) accs += t > 0.0 ? (int64_t)rint((t * dx) * 0x1p42) : 0;
+    if (spart) accsd += t > 0.0 ? rint((t * dx) * 0x1p42) : 0.0;
   }
-  acc = wave_sum_i64(acc);
-  accs = wave_sum_i64(accs);
+  const int64_t acc = wave_sum_i64((int64_t)accd);
+  const int64_t accs = wave_sum_i64((int64_t)accsd);
   if (lane == 0) {
     s_w[wave] = acc;
     s_s[wave] = accs;
