@@ -1006,19 +1006,29 @@ __global__ __launch_bounds__(256) void marginal_z_kernel(const void* __restrict_
   // and a thread adds at most 64 of them, so fp64 holds its sums exactly; they become
   // int64 once per thread.
   double accd = 0.0, accsd = 0.0;
-  for (int e = start + tid; e < end; e += 256) {
-    double x;
-    if (DT == TAPS_BF16) {
-      const uint16_t u = ((const uint16_t*)marg)[(size_t)row * vocab + e];
-      x = (double)__uint_as_float((uint32_t)u << 16);
-    } else {
-      x = (double)((const float*)marg)[(size_t)row * vocab + e];
+  // four elements per thread at a time (clamped loads, masked terms) so that their
+  // exponentials overlap; the exact sums do not depend on the order
+  for (int e0 = start + tid; e0 < end; e0 += 4 * 256) {
+    double xv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = min(e0 + j * 256, end - 1);
+      if (DT == TAPS_BF16) {
+        const uint16_t u = ((const uint16_t*)marg)[(size_t)row * vocab + e];
+        xv[j] = (double)__uint_as_float((uint32_t)u << 16);
+      } else {
+        xv[j] = (double)((const float*)marg)[(size_t)row * vocab + e];
+      }
     }
-    const double dx = x - M;
-    const double t = spec_exp(dx);
-    accd += rint(t * 0x1p42);
-    // the entropy's sum (learned scorer): t (x - M) on the same grid, 0 where t is 0
-    if (spart) accsd += t > 0.0 ? rint((t * dx) * 0x1p42) : 0.0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (e0 + j * 256 >= end) continue;
+      const double dx = xv[j] - M;
+      const double t = spec_exp(dx);
+      accd += rint(t * 0x1p42);
+      // the entropy's sum (learned scorer): t (x - M) on the same grid, 0 where t is 0
+      if (spart) accsd += t > 0.0 ? rint((t * dx) * 0x1p42) : 0.0;
+    }
   }
   const int64_t acc = wave_sum_i64((int64_t)accd);
   const int64_t accs = wave_sum_i64((int64_t)accsd);
