@@ -120,3 +120,70 @@ def test_learned_selection_equals_brute_force_and_alg1(seed):
     assert got == best_val and chosen in best_sets
     S, added = select_literal_alg1(c, den, budget, tau)
     assert not added and frozenset(S) == chosen
+
+
+def test_child_embedding_network_gives_the_hand_computed_softmax():
+    """Only the child-embedding weights W1[:, d:2d] are non-zero, so each edge's logit is a
+    function of its child's token alone (Sec. 4.2: the scorer sees the child token).  Hand
+    example: d = h = 1, logit = relu(emb[child]) with embeddings 0, 3 ln2, ln2, 2 ln2 for the
+    candidates of rank 0..3, so q_cond is (1, 8, 2, 4) / 15 in rank order, under every
+    parent.  The weights are not monotone in rank, and a scorer reading any other token's
+    embedding (the parent's, or the rank-0 candidate's) gives another table."""
+    V, K, D = 30, 4, 3
+    rng = np.random.default_rng(11)
+    rows = np.round(rng.standard_normal((D, V)) - 5.0, 3)
+    for i in range(D):                      # disjoint candidates: tokens 7i + 1, 7i + 2, ...
+        rows[i, 7 * i + 1:7 * i + 1 + K] = [4.0, 3.5, 3.0, 2.5]
+    from oracle.select import topk_row
+    idx = np.array([topk_row(rows[i], K)[0] for i in range(D)])
+    emb = np.zeros((V, 1), np.float32)
+    ln2 = math.log(2.0)
+    for i in range(D):
+        for r, k in enumerate((0, 3, 1, 2)):
+            emb[idx[i, r], 0] = np.float32(k * ln2)
+    mlp = MLPScorer(emb=emb, W1=np.array([[0.0, 1.0, 0.0, 0.0, 0.0]], np.float32),
+                    b1=np.zeros(1, np.float32), w2=np.ones(1, np.float32), b2=0.0,
+                    root_token=np.array([idx[0, 0]], np.int32))
+    c, _ = _table(mlp, rows, K)
+    want = np.array([1.0, 8.0, 2.0, 4.0]) / 15.0
+    for i in range(D):
+        for pr in range(K):
+            np.testing.assert_allclose(c[i, pr], want, rtol=2e-7)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_child_embedding_network_matches_a_high_precision_softmax(seed):
+    """Random child-embedding weights (two hidden units, biases, output weights); the
+    expected table is written out in 100-bit arithmetic from the same fp32 weights."""
+    d, h, V, K, D = 3, 2, 60, 5, 4
+    rng = np.random.default_rng(70 + seed)
+    W1 = np.zeros((h, 2 * d + 3), np.float32)
+    W1[:, d:2 * d] = rng.standard_normal((h, d)).astype(np.float32)
+    b1 = (rng.standard_normal(h) * 0.5).astype(np.float32)
+    w2 = rng.standard_normal(h).astype(np.float32)
+    emb = (rng.standard_normal((V, d)) * 2).astype(np.float32)
+    mlp = MLPScorer(emb=emb, W1=W1, b1=b1, w2=w2, b2=0.375,
+                    root_token=np.array([3], np.int32))
+    rows = _rows(90 + seed, D, V)
+    from oracle.select import topk_row
+    idx = np.array([topk_row(rows[i], K)[0] for i in range(D)])
+    c, _ = _table(mlp, rows, K)
+    mpmath.mp.prec = 100
+    mp = mpmath.mpf
+    for i in range(D):
+        logits = []
+        for r in range(K):
+            ce = [mp(float(x)) for x in emb[idx[i, r]]]
+            acc = mp(0.375)
+            for k in range(h):
+                a = mp(float(b1[k])) + mpmath.fsum(mp(float(W1[k, d + j])) * ce[j]
+                                                   for j in range(d))
+                acc += mp(float(w2[k])) * (a if a > 0 else mp(0))
+            logits.append(acc)
+        m = max(logits)
+        e = [mpmath.e ** (x - m) for x in logits]
+        Z = mpmath.fsum(e)
+        want = np.array([float(x / Z) for x in e])
+        assert len(set(np.round(want, 6))) > 1          # the children are told apart
+        for pr in range(K):
+            np.testing.assert_allclose(c[i, pr], want, rtol=1e-13, atol=1e-300)
