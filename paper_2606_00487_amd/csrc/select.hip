@@ -244,12 +244,12 @@ struct Level {                 // expanded trie nodes, stored depth by depth
   int hist[kBins];             // nodes per utility bin
   int chist[kCoarse];          // nodes per group of 16 bins
 };
-struct Seq {                   // sequential fallback: candidate children per selected node
-  uint64_t U[TAPS_MAX_BUDGET][TAPS_MAX_K];
-  double Q[TAPS_MAX_BUDGET][TAPS_MAX_K];
-  uint32_t path[TAPS_MAX_BUDGET][4];
+struct Seq {                   // sequential fallback, per selected node (selection order)
+  double q[TAPS_MAX_BUDGET];                 // q_reach
+  uint32_t path[TAPS_MAX_BUDGET][4];         // rank path, 4 bits per level from the root
   int depth[TAPS_MAX_BUDGET], par[TAPS_MAX_BUDGET], rank[TAPS_MAX_BUDGET];
-  int order[TAPS_MAX_BUDGET];
+  int order[TAPS_MAX_BUDGET];                // breadth-first position
+  uint8_t ord[TAPS_MAX_BUDGET][TAPS_MAX_K];  // child ranks by (utility desc, rank asc)
 };
 union Scratch {
   PhaseA a;
@@ -322,19 +322,40 @@ __device__ inline double qcond(const Shared& sh, const double* c3, int K, int d,
 }
 
 // ------------------------------------------------------------------ Phase C fallback
-// Sequential best-first selection (one wave) for expansions larger than kCap; emits
-// S through sh.x.s in breadth-first order and returns n.
+// Sequential best-first selection (one wave) for expansions larger than kCap; emits S
+// through sh.x.s in breadth-first order and returns n.  The frontier holds, for every
+// selected node, its best child not yet selected: the children of a node are visited in
+// the order (utility descending, rank ascending), which is the order Alg. 1's argmax and
+// its tie-break give siblings.  With the sibling and marginal scorers that order is the
+// rank order; the learned scorer's table need not fall with rank.  Lane l owns the nodes
+// l, l + 64, ... (slot s: node s * 64 + l); head[s] holds the utility bits + 1 of that
+// node's next child (0: none left), nxt[s] its position in the node's child order.
 template <int SLOTS>
 __device__ int select_sequential(Shared& sh, const double* c3, int D, int K, int N, double tau) {
   Seq& S = sh.x.s;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   if (wave == 0) {
-    if (lane < K) {
-      const double q = 1.0 * qcond(sh, c3, K, 0, 0, lane);
-      S.Q[0][lane] = q;
-      S.U[0][lane] = ubits(q / sh.den[1]) + 1ull;
-    }
+    // utility key (bits + 1; 0: none) of the rank-r child of node j, whose rank is pr and
+    // depth d (d < D)
+    auto child_key = [&](int j, int d, int pr, int r) -> uint64_t {
+      const double q = S.q[j] * qcond(sh, c3, K, d, pr, r);
+      return ubits(q / sh.den[d + 1]) + 1ull;
+    };
+    // order the K children of node j (lanes < K, one child each) into S.ord[j]; returns, in
+    // every lane, the key of the first child in that order
+    auto order_children = [&](int j, int d, int pr) -> uint64_t {
+      const uint64_t mine = lane < K && d < D ? child_key(j, d, pr, lane) : 0ull;
+      int pos = 0;
+      for (int r = 0; r < K; ++r) {
+        const uint64_t o = read_lane_u64(mine, r);
+        pos += (o > mine || (o == mine && r < lane)) ? 1 : 0;
+      }
+      if (lane < K) S.ord[j][pos] = (uint8_t)lane;
+      const uint64_t first = __ballot(lane < K && pos == 0);
+      return read_lane_u64(mine, __ffsll((long long)first) - 1);
+    };
     if (lane == 0) {
+      S.q[0] = 1.0;
       S.depth[0] = 0; S.par[0] = -1; S.rank[0] = -1;
       S.path[0][0] = S.path[0][1] = S.path[0][2] = S.path[0][3] = 0u;
     }
@@ -343,7 +364,11 @@ __device__ int select_sequential(Shared& sh, const double* c3, int D, int K, int
     int nxt[SLOTS];
 #pragma unroll
     for (int s = 0; s < SLOTS; ++s) { head[s] = 0ull; nxt[s] = 0; }
-    if (lane == 0) head[0] = S.U[0][0];
+    {
+      const uint64_t h0 = order_children(0, 0, 0);
+      if (lane == 0) head[0] = h0;
+    }
+    wave_fence();
     int m = 1;
     while (m < N) {
       uint64_t best = 0ull;
@@ -366,6 +391,7 @@ __device__ int select_sequential(Shared& sh, const double* c3, int D, int K, int
         const int wl = __ffsll((long long)bal) - 1;
         win = __shfl(myslot, wl) * kWave + wl;
       } else {
+        // equal utilities: the shallower child, then the smaller rank path
         uint32_t key[SLOTS][5];
         bool alive[SLOTS];
 #pragma unroll
@@ -378,7 +404,7 @@ __device__ int select_sequential(Shared& sh, const double* c3, int D, int K, int
 #pragma unroll
             for (int w = 0; w < 4; ++w) key[s][w + 1] = S.path[j][w];
             const int lvl = d - 1;
-            key[s][1 + lvl / 8] |= (uint32_t)nxt[s] << (28 - 4 * (lvl % 8));
+            key[s][1 + lvl / 8] |= (uint32_t)S.ord[j][nxt[s]] << (28 - 4 * (lvl % 8));
           } else {
 #pragma unroll
             for (int w = 0; w < 5; ++w) key[s][w] = 0xFFFFFFFFu;
@@ -401,42 +427,40 @@ __device__ int select_sequential(Shared& sh, const double* c3, int D, int K, int
         win = __shfl(ws, wl) * kWave + wl;
       }
       const int wlane = win % kWave, wslot = win / kWave;
-      int r_w = 0;
+      int pos_w = 0;
 #pragma unroll
-      for (int s = 0; s < SLOTS; ++s) if (s == wslot) r_w = nxt[s];
-      r_w = __shfl(r_w, wlane);
-      const double qm = S.Q[win][r_w];
-      const int dm = S.depth[win] + 1;
+      for (int s = 0; s < SLOTS; ++s) if (s == wslot) pos_w = nxt[s];
+      pos_w = __shfl(pos_w, wlane);
+      const int r_w = S.ord[win][pos_w];
+      const int dw = S.depth[win];
+      const int dm = dw + 1;
       if (lane == 0) {
+        S.q[m] = S.q[win] * qcond(sh, c3, K, dw, dw == 0 ? 0 : S.rank[win], r_w);
         S.depth[m] = dm; S.par[m] = win; S.rank[m] = r_w;
 #pragma unroll
         for (int w = 0; w < 4; ++w) S.path[m][w] = S.path[win][w];
         const int lvl = dm - 1;
         S.path[m][lvl / 8] |= (uint32_t)r_w << (28 - 4 * (lvl % 8));
       }
-      if (lane < K) {
-        if (dm < D) {
-          const double q = qm * qcond(sh, c3, K, dm, r_w, lane);
-          S.Q[m][lane] = q;
-          S.U[m][lane] = ubits(q / sh.den[dm + 1]) + 1ull;
-        } else {
-          S.Q[m][lane] = 0.0;
-          S.U[m][lane] = 0ull;
-        }
-      }
       wave_fence();
+      const uint64_t hm = order_children(m, dm, r_w);   // 0 when dm == D
+      // the winner's next child in its order
+      uint64_t hw = 0ull;
+      if (lane == wlane && pos_w + 1 < K)
+        hw = child_key(win, dw, dw == 0 ? 0 : S.rank[win], S.ord[win][pos_w + 1]);
       const int mlane = m % kWave, mslot = m / kWave;
 #pragma unroll
       for (int s = 0; s < SLOTS; ++s) {
         if (lane == wlane && s == wslot) {
-          nxt[s] = r_w + 1;
-          head[s] = nxt[s] < K ? S.U[win][nxt[s]] : 0ull;
+          nxt[s] = pos_w + 1;
+          head[s] = hw;
         }
         if (lane == mlane && s == mslot) {
           nxt[s] = 0;
-          head[s] = S.U[m][0];
+          head[s] = hm;
         }
       }
+      wave_fence();
       ++m;
     }
     if (lane == 0) sh.n = m;
@@ -959,7 +983,7 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
       o_depth[g] = S.depth[j];
       o_rank[g] = S.rank[j];
       o_token[g] = j == 0 ? -1 : (int32_t)cand_index(sh.top[S.depth[j] - 1][S.rank[j]]);
-      o_q[g] = j == 0 ? 1.0 : S.Q[S.par[j]][S.rank[j]];
+      o_q[g] = S.q[j];
     }
   }
   // ---------------- Phase D: pad the unused slots
