@@ -1,11 +1,12 @@
 """Tree-masked verification attention (Sec. 4.1 Stage 3; Sec. 4.3), plain fp64.
 
-Reading of the paper's "tree attention": every selected node attends to all
-cached context rows of its request plus the tree rows of its ancestors and
-itself, never to siblings or cousins (a connected subtree rooted at the
-current position is what verification needs).  The tree nodes' keys and
-values sit in the request's cache rows ctx + i, in tree order.  Query head h
-reads KV head h // (Hq / Hkv).  Softmax is max-subtracted, O = p @ V.
+Reading of the tree attention used for verification (Sec. 4.3 requires the
+selected set to be prefix closed, so each node's ancestors are all present):
+a node's query sees every cached context row of its request and the tree rows
+of the nodes on its own root path, itself included, and no other tree row.
+The tree nodes' keys and values sit in the request's cache rows ctx + i, in
+tree order.  Query head h reads KV head h // (Hq / Hkv).  Softmax is
+max-subtracted, O = p @ V.
 """
 from __future__ import annotations
 

@@ -1,11 +1,11 @@
 """Learned-scorer hook (Sec. 4.2, "Scorer design"; the first loop of Alg. 1) -- TEST
 INFRASTRUCTURE ONLY (see oracle/__init__.py).
 
-The paper's scorer maps each candidate edge (u -> v) to a logit from the parent and child
-tokens, the edge depth, the child's log-probability and the positional entropy, then
-normalises the logits of a parent's children with a sibling softmax.  Its trained weights
-are not published, so the hook runs a small MLP with caller-given (here: seeded random)
-weights.  Reading (the same on the GPU):
+Sec. 4.2 scores an edge from five inputs (the two tokens it joins, its depth, the drafter's
+log-probability of the child and the entropy of the child's position) and turns the scores
+of one parent's children into probabilities with a softmax over those siblings.  No
+trained weights are available, so the hook takes an MLP whose weights the caller supplies
+(here: seeded random ones).  Reading (the same on the GPU):
 
 * Features of an edge into row i (child depth i+1), in this order: the parent token's
   embedding (d values; the root's token is given per request; a token outside the

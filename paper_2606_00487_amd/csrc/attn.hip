@@ -940,9 +940,15 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int s0 = 0; s0 < nspl; s0 += CH) {
     if (s0 > 0) load_group(s0);
+    // splits past the request's keys were not written by this call: their slots hold
+    // whatever the workspace held before (possibly NaN bits), so values and weights are
+    // both replaced, not multiplied by a zero weight
 #pragma unroll
     for (int t = 0; t < CH; ++t)
-      if (s0 + t >= nspl) ml[t] = make_float2(-INFINITY, 0.f);
+      if (s0 + t >= nspl) {
+        ml[t] = make_float2(-INFINITY, 0.f);
+        ov[t] = make_uint2(0u, 0u);
+      }
     float Mc = M;
 #pragma unroll
     for (int t = 0; t < CH; ++t) Mc = fmaxf(Mc, ml[t].x);
