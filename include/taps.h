@@ -165,6 +165,21 @@ taps_status taps_select(const void *marginals, const taps_select_params *p,
                         const taps_tree *out, void *ws, size_t ws_bytes,
                         hipStream_t stream);
 
+/* taps_select for callers that cannot allocate: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same arguments, results and errors as
+ * taps_select, without the workspace: the selection's scratch is a static device array of
+ * TAPS_SELECT_SCRATCH_BYTES per GPU, which the library holds until the process ends (the
+ * first call on a device looks up its address).  The call allocates nothing.
+ *   - Parameters whose taps_select_workspace_bytes exceed TAPS_SELECT_SCRATCH_BYTES return
+ *     TAPS_ERR_WORKSPACE before anything is enqueued.
+ *   - The array is shared by every call on the same GPU and keeps the last call's
+ *     contents (no call reads what another left): calls that may overlap in time on one
+ *     GPU (other streams, other host threads) race and must be serialized by the caller.
+ *   - The device is the one current on the calling thread; `stream` must belong to it. */
+#define TAPS_SELECT_SCRATCH_BYTES (8u << 20)
+taps_status taps_select_noalloc(const void *marginals, const taps_select_params *p,
+                                const taps_tree *out, hipStream_t stream);
+
 /* Bytes of scratch tree_verify_attn needs (split-KV partial outputs). */
 size_t tree_verify_attn_workspace_bytes(int32_t batch, int32_t budget, int32_t Hq,
                                         int32_t Hkv, int32_t head_dim, int32_t max_ctx,

@@ -130,6 +130,18 @@ class Selector:
                                         _ptr(self.ws), self.ws_bytes, _stream()))
         return t
 
+    def noalloc(self, marginals: torch.Tensor, tree: TreeBuffers | None = None) -> TreeBuffers:
+        """taps_select_noalloc: the same selection with the library's static scratch instead
+        of this Selector's workspace (for callers that cannot allocate)."""
+        p = self.p
+        _need(marginals, "marginals", _TORCH_DT[p.dtype], (p.batch, p.block, p.vocab))
+        t = tree or self.tree
+        st = t.struct() if tree is not None else self._tree_struct
+        _lib.check(self.lib, "taps_select_noalloc",
+                   self.lib.taps_select_noalloc(_ptr(marginals), ctypes.byref(p),
+                                                ctypes.byref(st), _stream()))
+        return t
+
 
 class TreeAttention:
     """tree_verify_attn: tree-masked verification attention."""

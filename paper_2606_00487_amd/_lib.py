@@ -31,8 +31,9 @@ EXPORTED = [
     "taps_select_workspace_bytes", "taps_select_validate", "taps_select",
     "tree_verify_attn_workspace_bytes", "tree_verify_attn_validate", "tree_verify_attn",
     "tree_verify_attn_timed", "accept_walk", "kv_commit", "taps_status_string",
-    "taps_spec_exp_host", "verify_layer_workspace_bytes", "verify_layer",
+    "taps_spec_exp_host", "verify_layer_workspace_bytes", "verify_layer", "taps_select_noalloc",
 ]
+SELECT_SCRATCH_BYTES = 8 << 20   # TAPS_SELECT_SCRATCH_BYTES
 
 
 class LayerWeights(ctypes.Structure):
@@ -91,6 +92,8 @@ def load(path: str = LIB_PATH):
     lib.taps_select_validate.restype = i32
     lib.taps_select.argtypes = [vp, P(SelectParams), P(Tree), vp, sz, vp]
     lib.taps_select.restype = i32
+    lib.taps_select_noalloc.argtypes = [vp, P(SelectParams), P(Tree), vp]
+    lib.taps_select_noalloc.restype = i32
     lib.tree_verify_attn_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32, i32]
     lib.tree_verify_attn_workspace_bytes.restype = sz
     lib.tree_verify_attn_validate.argtypes = [i32, i32, i32, i32, i32, i32, i32, f32]

@@ -30,7 +30,8 @@ PER_FILE = {
     # the AGPR form would copy its accumulators back and forth around every softmax
     "attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
-SOURCES = ["topk.hip", "select.hip", "attn.hip", "walk.hip", "commit.hip", "layer.hip", "api.cpp"]
+SOURCES = ["topk.hip", "select.hip", "attn.hip", "walk.hip", "commit.hip", "layer.hip",
+           "noalloc.hip", "api.cpp"]
 
 
 def hipcc() -> str:

@@ -237,3 +237,22 @@ def test_layer_validation_and_workspace(lib):
     assert call() == _lib.TAPS_ERR_INVALID_ARG
     w.norm_eps, w.Wo = 1e-6, None
     assert call() == _lib.TAPS_ERR_INVALID_ARG
+
+
+def test_noalloc_select_validates_before_touching_the_device(lib):
+    """taps_select_noalloc refuses bad parameters, missing outputs and selections larger
+    than its static scratch on the host, before any device call (this runs without a GPU)."""
+    import ctypes
+    fake = 4096                       # never dereferenced: every case returns before
+    tree = _lib.Tree(fake, fake, fake, fake, fake, fake, fake, fake)
+    big = params(batch=4096, block=32, K=16)
+    assert lib.taps_select_workspace_bytes(ctypes.byref(big)) > _lib.SELECT_SCRATCH_BYTES
+    assert lib.taps_select_noalloc(fake, ctypes.byref(big), ctypes.byref(tree), None) == \
+        _lib.TAPS_ERR_WORKSPACE
+    assert lib.taps_select_noalloc(fake, ctypes.byref(params(K=17)), ctypes.byref(tree),
+                                   None) == _lib.TAPS_ERR_UNSUPPORTED
+    assert lib.taps_select_noalloc(None, ctypes.byref(params()), ctypes.byref(tree), None) == \
+        _lib.TAPS_ERR_INVALID_ARG
+    assert lib.taps_select_noalloc(fake, ctypes.byref(params(batch=0)), None, None) == _lib.TAPS_OK
+    assert lib.taps_select_workspace_bytes(ctypes.byref(params(batch=16))) <= \
+        _lib.SELECT_SCRATCH_BYTES
