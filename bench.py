@@ -49,7 +49,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--config", default="qwen3_8b")
     ap.add_argument("--budget", type=int, default=0,
-                    help="override the configuration's node budget N (1..256)")
+                    help="override the configuration's node budget N (1..512)")
     ap.add_argument("--lambda2", type=float, default=None,
                     help="override lambda2 of Eq. 3 (0 with --tau 0: no cost-aware pruning)")
     ap.add_argument("--tau", type=float, default=None, help="override the utility threshold")

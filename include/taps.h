@@ -56,7 +56,7 @@ typedef enum {
 /* Limits of this build. */
 #define TAPS_MAX_BLOCK 32    /* draft positions D (tree depth)              */
 #define TAPS_MAX_K 16        /* candidates per position                     */
-#define TAPS_MAX_BUDGET 256  /* N_max, root included                        */
+#define TAPS_MAX_BUDGET 512  /* N_max, root included                        */
 
 /* [host] Weights of the learned-scorer hook (Sec. 4.2, "Scorer design"): a per-edge MLP
  * whose trained weights are not published, so the caller brings its own.  DEVICE fp32

@@ -25,7 +25,7 @@ TAPS_SCORER_MARGINAL = 1
 TAPS_SCORER_LEARNED = 2
 MAX_BLOCK = 32
 MAX_K = 16
-MAX_BUDGET = 256
+MAX_BUDGET = 512
 
 EXPORTED = [
     "taps_select_workspace_bytes", "taps_select_validate", "taps_select",

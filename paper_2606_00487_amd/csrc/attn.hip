@@ -38,40 +38,34 @@ constexpr int kKT = 64;  // keys per tile
 constexpr float kLog2e = 1.4426950408889634f;
 
 
-// word w (0..3) of a 256-bit mask held in registers, without dynamic register indexing
-__device__ inline uint64_t mask_word(const uint64_t (&a)[4], int w) {
-  const uint64_t lo = (w & 1) ? a[1] : a[0];
-  const uint64_t hi = (w & 1) ? a[3] : a[2];
-  return (w & 2) ? hi : lo;
-}
+constexpr int kAncWords = TAPS_MAX_BUDGET / 64;   // 64-bit words of one node's mask
 
-// ancestor-or-self mask of node i from parent pointers (a parent outside [0, node)
-// ends the walk); par(j) reads the parent of node j
+// ancestor-or-self mask of node i from parent pointers (a parent outside [0, node) ends
+// the walk), kAncWords words in registers; par(j) reads the parent of node j
 template <typename F>
-__device__ inline void ancestor_mask(int i, F par, uint64_t (&a)[4]) {
-  a[0] = a[1] = a[2] = a[3] = 0ull;
+__device__ inline void ancestor_mask(int i, F par, uint64_t (&a)[kAncWords]) {
+#pragma unroll
+  for (int w = 0; w < kAncWords; ++w) a[w] = 0ull;
   int cur = i;
   for (;;) {
     const uint64_t bit = 1ull << (cur & 63);
-    const int w = cur >> 6;
-    a[0] |= w == 0 ? bit : 0ull;
-    a[1] |= w == 1 ? bit : 0ull;
-    a[2] |= w == 2 ? bit : 0ull;
-    a[3] |= w == 3 ? bit : 0ull;
+    const int cw = cur >> 6;
+#pragma unroll
+    for (int w = 0; w < kAncWords; ++w) a[w] |= cw == w ? bit : 0ull;
     const int p = par(cur);
     if (p < 0 || p >= cur) break;
     cur = p;
   }
 }
 
-// 64 keys of the 256-bit ancestor-or-self mask a[], starting at bit t0 (t0 may be negative:
-// bits below 0 read as 0)
-__device__ inline uint64_t mask_window(const uint64_t (&a)[4], int t0) {
-  if (t0 <= -64 || t0 >= 256) return 0ull;
-  if (t0 < 0) return a[0] << (-t0);
+// 64 tree rows of a node's ancestor-or-self mask (kAncWords words in LDS), starting at
+// row t0 (t0 may be negative: rows below 0 read as 0)
+__device__ inline uint64_t mask_window(const uint64_t* anc, int t0) {
+  if (t0 <= -64 || t0 >= 64 * kAncWords) return 0ull;
+  if (t0 < 0) return anc[0] << (-t0);
   const int w = t0 >> 6, sh = t0 & 63;
-  const uint64_t lo = mask_word(a, w);
-  const uint64_t hi = w < 3 ? mask_word(a, w + 1) : 0ull;
+  const uint64_t lo = anc[w];
+  const uint64_t hi = w + 1 < kAncWords ? anc[w + 1] : 0ull;
   return sh ? (lo >> sh) | (hi << (64 - sh)) : lo;
 }
 
@@ -206,7 +200,7 @@ __global__ __launch_bounds__(256) void attn_bf16_w4_kernel(
   constexpr int STEP = kKT;           // keys per stage
   static_assert(TILEB % (BLK * NW) == 0 && LPH >= 1 && 7 * LPH <= 63, "direct loads per wave");
   static_assert(BLK % ROWB == 0, "a direct load covers whole rows");
-  static_assert(NT >= TAPS_MAX_BUDGET, "one parent pointer per thread");
+  constexpr int PPT = (TAPS_MAX_BUDGET + NT - 1) / NT;   // parent pointers per thread
   // separate LDS objects, and every access names its buffer statically: the compiler can
   // then tell that reads of one buffer do not overlap the loads in flight into another
   __shared__ __attribute__((aligned(16))) unsigned char s_k0[TILEB];
@@ -217,7 +211,7 @@ __global__ __launch_bounds__(256) void attn_bf16_w4_kernel(
   __shared__ __attribute__((aligned(16))) unsigned char s_v1[TILEB];
   __shared__ __attribute__((aligned(16))) unsigned char s_v2[TILEB];
   __shared__ __attribute__((aligned(16))) unsigned char s_v3[TILEB];
-  __shared__ uint64_t s_anc[TAPS_MAX_BUDGET][4];
+  __shared__ uint64_t s_anc[MT + 1][kAncWords];   // masks of this tile's nodes
   __shared__ int s_par[TAPS_MAX_BUDGET];
 
   // ---- which (request, KV head, split, row tile) this workgroup owns
@@ -285,9 +279,17 @@ __global__ __launch_bounds__(256) void attn_bf16_w4_kernel(
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) q[kk] = *(const bf16x8*)(qp + kk * 16 + hl * 8);
   }
-  // parent pointers for the ancestor masks (at most one per thread: budget <= NT)
+  // parent pointers for the ancestor masks
   const bool tree_split = k_end > ctx;
-  const int my_par = tree_split && tid < n ? parentp[(size_t)b * N + tid] : -1;
+  int my_par[PPT];
+#pragma unroll
+  for (int j = 0; j < PPT; ++j) {
+    const int i = tid + j * NT;
+    my_par[j] = tree_split && i < n ? parentp[(size_t)b * N + i] : -1;
+  }
+  // the tile's nodes: query rows row0 .. row0 + MT - 1 belong to nodes node0 .. node0 + MT
+  const int node0 = row0 / G;
+  const int node_end = min(n, (row0 + MT - 1) / G + 1);
   // the first stages load while the masks are set up; the queries and parents were
   // issued first, so waiting for them leaves these loads in flight.  The order K(0),
   // [V(0) K(1)], [V(1) K(2)], [V(2) K(3)] matches the steps' [V(i+3) K(i+4)].
@@ -302,13 +304,15 @@ __global__ __launch_bounds__(256) void attn_bf16_w4_kernel(
 
   // ---- ancestor-or-self masks of the tree rows, in LDS (read only by masked tiles)
   if (tree_split) {
-    if (tid < n) s_par[tid] = my_par;
+#pragma unroll
+    for (int j = 0; j < PPT; ++j)
+      if (tid + j * NT < n) s_par[tid + j * NT] = my_par[j];
     __syncthreads();
-    for (int i = tid; i < n; i += NT) {
-      uint64_t a[4];
+    for (int i = node0 + tid; i < node_end; i += NT) {
+      uint64_t a[kAncWords];
       ancestor_mask(i, [&](int j) { return s_par[j]; }, a);
 #pragma unroll
-      for (int w = 0; w < 4; ++w) s_anc[i][w] = a[w];
+      for (int w = 0; w < kAncWords; ++w) s_anc[i - node0][w] = a[w];
     }
     __syncthreads();
   }
@@ -356,12 +360,9 @@ __global__ __launch_bounds__(256) void attn_bf16_w4_kernel(
     // ---- mask (only tiles that reach the tree rows or the split end)
     const bool need_mask = base + kKT > ctx || base + kKT > k_end;
     if (need_mask) {
-      uint64_t anc[4] = {0ull, 0ull, 0ull, 0ull};
-      if (base + kKT > ctx && qnode < n) {
-#pragma unroll
-        for (int w = 0; w < 4; ++w) anc[w] = s_anc[qnode][w];
-      }
-      uint64_t A = (low_bits(ctx - base) | mask_window(anc, base - ctx)) & low_bits(k_end - base);
+      const uint64_t win =
+          base + kKT > ctx && qnode < n ? mask_window(s_anc[qnode - node0], base - ctx) : 0ull;
+      uint64_t A = (low_bits(ctx - base) | win) & low_bits(k_end - base);
       A >>= 4 * hl;   // this lane's keys are kb*32 + 8*(v/4) + 4*hl + v%4
       const uint32_t mlo = (uint32_t)A, mhi = (uint32_t)(A >> 32);
 #pragma unroll
@@ -553,11 +554,12 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
   constexpr int BLK = kWave * 16;     // bytes one wave writes per direct load
   static_assert(TILEB == 8 * BLK, "one direct load per wave and slot");
   static_assert(NT >= TAPS_MAX_BUDGET, "one parent pointer per thread");
+  static_assert(TAPS_MAX_BUDGET <= 8 * 64, "the eight waves load 64 parent pointers each");
   __shared__ __attribute__((aligned(16))) unsigned char s_k0[TILEB], s_k1[TILEB], s_k2[TILEB],
       s_k3[TILEB], s_k4[TILEB], s_k5[TILEB], s_k6[TILEB], s_k7[TILEB];
   __shared__ __attribute__((aligned(16))) unsigned char s_v0[TILEB], s_v1[TILEB], s_v2[TILEB],
       s_v3[TILEB], s_v4[TILEB], s_v5[TILEB], s_v6[TILEB], s_v7[TILEB];
-  __shared__ uint64_t s_anc[TAPS_MAX_BUDGET][4];
+  __shared__ uint64_t s_anc[MT + 1][kAncWords];   // masks of this tile's nodes
   __shared__ int s_par[TAPS_MAX_BUDGET];
   __shared__ float2 s_ml[8 * 64];
 
@@ -611,6 +613,8 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     const int qr = min(row0 + rg * 32 + l32, N * G - 1);
     qnode = dm.div(qr, G, dm.g);
   }
+  // the tile's nodes: query rows row0 .. row0 + MT - 1 belong to nodes node0 .. node0 + MT
+  const int node0 = dm.div(row0, G, dm.g);
 
   int ctx_raw, n_raw;
   int64_t kv0;
@@ -662,11 +666,12 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
 
   // ---- ancestor-or-self masks of the tree rows, in LDS (read only by masked tiles)
   if (tree_split) {
-    for (int i = tid; i < n; i += NT) {
-      uint64_t a[4];
+    const int node_end = min(n, dm.div(row0 + MT - 1, G, dm.g) + 1);
+    for (int i = node0 + tid; i < node_end; i += NT) {
+      uint64_t a[kAncWords];
       ancestor_mask(i, [&](int j) { return s_par[j]; }, a);
 #pragma unroll
-      for (int w = 0; w < 4; ++w) s_anc[i][w] = a[w];
+      for (int w = 0; w < kAncWords; ++w) s_anc[i - node0][w] = a[w];
     }
     TAPS_LDS_BARRIER();
   }
@@ -710,12 +715,9 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
                         f32x16& sn, int base) __attribute__((always_inline)) {
     const bool need_mask = base + KT > ctx || base + KT > k_end;
     if (need_mask) {
-      uint64_t anc[4] = {0ull, 0ull, 0ull, 0ull};
-      if (base + KT > ctx && qnode < n) {
-#pragma unroll
-        for (int w = 0; w < 4; ++w) anc[w] = s_anc[qnode][w];
-      }
-      uint64_t A = (low_bits(ctx - base) | mask_window(anc, base - ctx)) & low_bits(k_end - base);
+      const uint64_t win =
+          base + KT > ctx && qnode < n ? mask_window(s_anc[qnode - node0], base - ctx) : 0ull;
+      uint64_t A = (low_bits(ctx - base) | win) & low_bits(k_end - base);
       const uint32_t word = (uint32_t)(A >> (4 * hl));   // keys 8*(v/4) + 4*hl + v%4
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
@@ -983,7 +985,7 @@ __global__ __launch_bounds__(kThreads) void attn_f32_kernel(
   __shared__ float s_q[HD];
   __shared__ float s_p[kThreads];
   __shared__ float s_red[kThreads / 64];
-  __shared__ uint64_t s_anc[4];
+  __shared__ uint64_t s_anc[kAncWords];
   __shared__ float s_acc[GROUPS][HD];
   const int i = blockIdx.x, hq = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
@@ -996,10 +998,10 @@ __global__ __launch_bounds__(kThreads) void attn_f32_kernel(
   const size_t rs = (size_t)Hkv * HD;
   if (tid < HD) s_q[tid] = Q[(((size_t)b * N + i) * Hq + hq) * HD + tid];
   if (tid == 0) {
-    uint64_t a[4];
+    uint64_t a[kAncWords];
     const int32_t* pp = parentp + (size_t)b * N;
     ancestor_mask(i, [&](int j) { return pp[j]; }, a);
-    for (int w = 0; w < 4; ++w) s_anc[w] = a[w];
+    for (int w = 0; w < kAncWords; ++w) s_anc[w] = a[w];
   }
   __syncthreads();
   float m_run = -INFINITY, l_run = 0.f, acc = 0.f;
@@ -1010,7 +1012,7 @@ __global__ __launch_bounds__(kThreads) void attn_f32_kernel(
     bool ok = key < R;
     if (ok && key >= ctx) {
       const int t = key - ctx;
-      ok = (s_anc[(t >> 6) & 3] >> (t & 63)) & 1ull;
+      ok = (s_anc[t >> 6] >> (t & 63)) & 1ull;
     }
     if (ok) {
       const float* kr = Kc + (size_t)(kv0 + key) * rs + (size_t)g * HD;

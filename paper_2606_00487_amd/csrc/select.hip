@@ -892,6 +892,12 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
         }
       }
       base += total;
+      // once N-1 nodes are stored, the pruning bin can rise after every chunk, also in
+      // the middle of a level: every node below it is beaten by N-1 stored nodes
+      if (base >= N - 1 && c0 + 4 * kThreads < items) {   // uniform
+        __syncthreads();   // the chunk's histogram counts are complete
+        bstar = find_bstar(L, N);
+      }
     }
     if (fallback) break;
     __syncthreads();   // the level's nodes and histogram counts are complete
@@ -1111,11 +1117,13 @@ hipError_t launch_select(const void* /*marg*/, const taps_select_params& p, cons
         marginal, cand, zpart, spart, mlp, out.parent, out.token, out.depth, out.rank,        \
         out.q_reach, out.n_nodes, out.topk_idx, out.topk_val);                                \
   } while (0)
+  static_assert(TAPS_MAX_BUDGET <= 8 * kWave, "at most eight frontier slots per lane");
   switch (slots) {
     case 1: TAPS_SEL(1); break;
     case 2: TAPS_SEL(2); break;
-    case 3: TAPS_SEL(3); break;
-    default: TAPS_SEL(4); break;
+    case 3:
+    case 4: TAPS_SEL(4); break;
+    default: TAPS_SEL(8); break;
   }
 #undef TAPS_SEL
   return hipGetLastError();

@@ -89,11 +89,13 @@ hipError_t launch_walk(const taps_tree& t, int batch, int budget, int block,
 #define TAPS_WALK(SL)                                                                        \
   walk_kernel<SL><<<grid, blk, 0, s>>>(t.parent, t.token, t.n_nodes, budget, block, target, \
                                        path, path_len, bonus)
+  static_assert(TAPS_MAX_BUDGET <= 8 * kWave, "at most eight node slots per lane");
   switch ((budget + kWave - 1) / kWave) {
     case 1: TAPS_WALK(1); break;
     case 2: TAPS_WALK(2); break;
-    case 3: TAPS_WALK(3); break;
-    default: TAPS_WALK(4); break;
+    case 3:
+    case 4: TAPS_WALK(4); break;
+    default: TAPS_WALK(8); break;
   }
 #undef TAPS_WALK
   return hipGetLastError();

@@ -42,7 +42,8 @@ def params(**kw):
     ({"batch": -1}, _lib.TAPS_ERR_INVALID_ARG),
     ({"K": 17}, _lib.TAPS_ERR_UNSUPPORTED),
     ({"K": 0}, _lib.TAPS_ERR_INVALID_ARG),
-    ({"budget": 257}, _lib.TAPS_ERR_UNSUPPORTED),
+    ({"budget": 513}, _lib.TAPS_ERR_UNSUPPORTED),
+    ({"budget": 512}, _lib.TAPS_OK),
     ({"budget": 0}, _lib.TAPS_ERR_INVALID_ARG),
     ({"block": 33}, _lib.TAPS_ERR_UNSUPPORTED),
     ({"block": 0}, _lib.TAPS_ERR_INVALID_ARG),
@@ -127,7 +128,8 @@ def test_select_rejects_null_buffers_and_small_workspace(lib):
     ((1, 64, 32, 8, 128, 8192, 0, 0.088), _lib.TAPS_OK),
     ((1, 64, 32, 7, 128, 8192, 0, 0.088), _lib.TAPS_ERR_INVALID_ARG),
     ((1, 64, 32, 8, 96, 8192, 0, 0.088), _lib.TAPS_ERR_UNSUPPORTED),
-    ((1, 300, 32, 8, 128, 8192, 0, 0.088), _lib.TAPS_ERR_UNSUPPORTED),
+    ((1, 600, 32, 8, 128, 8192, 0, 0.088), _lib.TAPS_ERR_UNSUPPORTED),
+    ((1, 300, 32, 8, 128, 8192, 0, 0.088), _lib.TAPS_OK),
     ((1, 64, 32, 8, 128, -1, 0, 0.088), _lib.TAPS_ERR_INVALID_ARG),
     ((1, 64, 32, 8, 128, 8192, 3, 0.088), _lib.TAPS_ERR_INVALID_ARG),
     ((1, 64, 32, 8, 128, 8192, 0, math.inf), _lib.TAPS_ERR_INVALID_ARG),
@@ -170,7 +172,7 @@ def test_commit_validation(lib):
 
     assert call(sizes=(0, 64, 16, 8, 128, 8192, 0)) == _lib.TAPS_OK            # nothing to do
     assert call(sizes=(-1, 64, 16, 8, 128, 8192, 0)) == _lib.TAPS_ERR_INVALID_ARG
-    assert call(sizes=(1, 257, 16, 8, 128, 8192, 0)) == _lib.TAPS_ERR_UNSUPPORTED
+    assert call(sizes=(1, 513, 16, 8, 128, 8192, 0)) == _lib.TAPS_ERR_UNSUPPORTED
     assert call(sizes=(1, 64, 33, 8, 128, 8192, 0)) == _lib.TAPS_ERR_UNSUPPORTED
     assert call(sizes=(1, 64, 16, 8, 96, 8192, 0)) == _lib.TAPS_ERR_UNSUPPORTED
     assert call(sizes=(1, 64, 16, 8, 128, 8192, 5)) == _lib.TAPS_ERR_INVALID_ARG
