@@ -37,6 +37,8 @@ if ROOT not in sys.path:
 METRIC = ("verification rounds/sec (select+tree-attn+accept) and achieved HBM GB/s, "
           "Qwen3-8B shape")
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0        # dense bf16 matrix-core peak of MI355X
+RIDGE = MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)   # flop per byte
 MALL_BYTES = 256 << 20
 ATTN_SRC = os.path.join(ROOT, "paper_2606_00487_amd", "csrc", "attn.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_bf16_kernel_qwen3_8b_hbm.txt")
@@ -109,6 +111,21 @@ def algorithmic_bytes(cfg, ctx_len, n_nodes):
     kv = sum(int(c) + int(n) for c, n in zip(ctx_len, n_nodes)) * cfg.Hkv * cfg.head_dim * es * 2
     qo = sum(int(n) for n in n_nodes) * cfg.Hq * cfg.head_dim * es * 2
     return marg, kv, qo
+
+
+def attention_flops(cfg, ctx_len, n_nodes):
+    """Matrix-core work of the tree attention, dense over each request's context and tree
+    rows: Q K^T and P V for every selected node and query head, 4 * n * Hq * (ctx + n) * hd
+    per request."""
+    return sum(4 * int(n) * cfg.Hq * (int(c) + int(n)) * cfg.head_dim
+               for c, n in zip(ctx_len, n_nodes))
+
+
+def spread(us):
+    """Median and 10th / 90th percentiles of per-round times (us)."""
+    a = np.asarray(us, dtype=np.float64)
+    return {"median": round(float(np.median(a)), 3), "p10": round(float(np.percentile(a, 10)), 3),
+            "p90": round(float(np.percentile(a, 90)), 3), "rounds": int(a.size)}
 
 
 def commit_moved_bytes(cfg, path, path_len):
@@ -229,11 +246,14 @@ def main():
                 graphs.append(g)
         torch.cuda.synchronize()
 
-        def step(i):
+        def run_set(k):
             if args.eager:
-                round_(sets[i % nsets])
+                round_(sets[k])
             else:
-                graphs[i % nsets].replay()
+                graphs[k].replay()
+
+        def step(i):
+            run_set(i % nsets)
 
         for i in range(args.warmup):
             step(i)
@@ -244,6 +264,27 @@ def main():
         torch.cuda.synchronize()
         t1 = time.perf_counter()
         elapsed = t1 - t0
+
+        # ---------------- per-round times: events between consecutive rounds, with the input
+        # sets rotating (cold: more than the Infinity Cache holds) and with one set repeated
+        # (warm: its working set stays in the cache)
+        def per_round(order):
+            evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(order) + 1)]
+            for e in evs:                     # materialise the event handles
+                e.record(stream)
+            torch.cuda.synchronize()
+            evs[0].record(stream)
+            for k, si in enumerate(order):
+                run_set(si)
+                evs[k + 1].record(stream)
+            torch.cuda.synchronize()
+            return [evs[k].elapsed_time(evs[k + 1]) * 1e3 for k in range(len(order))]
+
+        R = max(2 * nsets, min(args.steps, 300))
+        for _ in range(2):
+            run_set(0)
+        dist_cold = spread(per_round([i % nsets for i in range(R)]))
+        dist_warm = spread(per_round([0] * R))
 
         # ---------------- per-stage timing pass (eager, same launches, HIP events)
         reps = max(nsets, min(args.steps, 200))
@@ -335,6 +376,7 @@ def main():
     t_attn = float(np.mean([e[2].elapsed_time(e[3]) for e in ev])) * 1e3
     t_attn_call = float(np.mean([e[1].elapsed_time(e[4]) for e in ev])) * 1e3
     t_walk = float(np.mean([e[4].elapsed_time(e[5]) for e in ev])) * 1e3
+    dist_eager = spread([e[0].elapsed_time(e[5]) * 1e3 for e in ev])
 
     # ---------------- bytes and roofline
     per_set = [algorithmic_bytes(cfg, s["inp"].ctx_len, s["n"]) for s in sets]
@@ -343,9 +385,36 @@ def main():
     qo_b = float(np.mean([p[2] for p in per_set]))
     round_bytes = marg_b + kv_b + qo_b
     attn_bytes = kv_b + qo_b
+    attn_fl = float(np.mean([attention_flops(cfg, s["inp"].ctx_len, s["n"]) for s in sets]))
+    intensity = attn_fl / attn_bytes
     ms_per_step = elapsed / args.steps * 1e3
     rounds_per_s = cfg.batch * args.steps / elapsed
     achieved = attn_bytes / (t_attn * 1e-6) / 1e9
+    traffic = measured_traffic(cfg.name)
+    if bf and intensity > RIDGE:
+        # more flops per byte than the machine balance: the matrix cores bound the kernel
+        roofline = {"bound": "mfma", "kernel": "attn_bf16_kernel",
+                    "achieved": round(attn_fl / (t_attn * 1e-6) / 1e12, 1),
+                    "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(attn_fl / (t_attn * 1e-6) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)}
+    else:
+        roofline = {"bound": "hbm", "kernel": "attn_bf16_kernel" if bf else "attn_f32_kernel",
+                    "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    roofline.update({
+        "traffic": traffic,
+        "traffic_source": (os.path.relpath(TRAFFIC_FILE, ROOT) + ": rocprofv3 --pmc FETCH_SIZE, "
+                           "WRITE_SIZE of this kernel source, scaled by a plain copy")
+        if traffic is not None else None,
+        "bytes_per_launch": int(attn_bytes),
+        "flops_per_launch": int(attn_fl),
+        "intensity_flop_per_byte": round(intensity, 1),
+        "ridge_flop_per_byte": round(RIDGE, 1),
+        "hbm_frac": round(achieved / HBM_PEAK_GBS, 4),
+        "mfma_frac": round(attn_fl / (t_attn * 1e-6) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
+        if bf else None,
+        "avg_launch_us": round(t_attn, 3),
+    })
     out = {
         "metric": METRIC,
         "value": round(rounds_per_s, 2),
@@ -372,6 +441,7 @@ def main():
         },
         "hbm_gbs_round": round(round_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "round_bytes": int(round_bytes),
+        "round_us": {"graph_cold": dist_cold, "graph_warm": dist_warm, "eager_cold": dist_eager},
         "stages_us": {"select": round(t_sel, 2), "attn_main_kernel": round(t_attn, 2),
                       "attn_call": round(t_attn_call, 2), "walk": round(t_walk, 2),
                       "kv_commit": round(t_commit, 2)},
@@ -384,17 +454,7 @@ def main():
             "bytes_per_launch": int(np.mean(layer_b)),
             "achieved_gbs": round(float(np.mean(layer_b)) / (float(np.mean(layer_us)) * 1e-6) / 1e9, 1),
             "avg_launch_us": round(float(np.mean(layer_us)), 3)},
-        "roofline": {
-            "bound": "hbm",
-            "kernel": "attn_bf16_kernel" if bf else "attn_f32_kernel",
-            "achieved": round(achieved, 1),
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic(cfg.name),
-            "bytes_per_launch": int(attn_bytes),
-            "avg_launch_us": round(t_attn, 3),
-        },
+        "roofline": roofline,
         "round_roofline_frac": round((round_bytes / HBM_PEAK_GBS / 1e3) / (ms_per_step * 1e3), 4),
     }
     if not args.no_cpu_baseline:
@@ -402,15 +462,30 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(cfg, inp, budget_s, scorer=0, mlp=None):
-    """The oracle as it stands, on this host, over a bounded sample of one round."""
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo) and the cores this process may run on."""
+    import platform
+    model = platform.processor() or "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover - not Linux
+        cores = os.cpu_count() or 1
+    return model, cores
+
+
+def oracle_round(cfg, inp, budget_s, scorer=0, mlp=None):
+    """The oracle as it stands over one round of `inp`: the whole selection, the attention of
+    as many (node, head) rows as fit in budget_s (extrapolated to all rows), the walk.
+    Returns (seconds per round, the sample's description)."""
     import oracle
     from workloads import target_tokens
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover - threadpoolctl missing
-        threads = 1
     x = inp.marginals_f64()
     t0 = time.perf_counter()
     w = None
@@ -438,15 +513,37 @@ def cpu_baseline(cfg, inp, budget_s, scorer=0, mlp=None):
         tgt = target_tokens(cfg, b, t.parent, t.rank, t.n, t.topk_idx[:, 0], inp.p_acc[b])
         oracle.accept_walk(t.parent, t.token, t.n, tgt)
     t_walk = time.perf_counter() - t0
-    per_round = t_sel + t_attn + t_walk
+    desc = (f"selection {t_sel:.2f} s, attention {done}/{len(rows)} (node, head) rows "
+            f"extrapolated to all {t_attn:.1f} s, walk {t_walk:.3f} s")
+    return t_sel + t_attn + t_walk, desc
+
+
+def cpu_baseline(cfg, inp, budget_s, scorer=0, mlp=None):
+    """The oracle as it stands, on this host, over a bounded sample of one round: once with
+    the BLAS pool at its default size (the attention's products use it; selection and walk
+    are single-threaded Python) and once limited to one thread."""
+    model, avail = cpu_model()
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        threads = max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl missing
+        threadpool_limits, threads = None, 1
+    per_round, desc = oracle_round(cfg, inp, budget_s / 2, scorer, mlp)
+    single = None
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            t1, d1 = oracle_round(cfg, inp, budget_s / 2, scorer, mlp)
+        single = {"value": round(cfg.batch / t1, 5), "unit": "rounds/s", "cores": 1,
+                  "sample": d1}
     return {
         "value": round(cfg.batch / per_round, 5),
         "unit": "rounds/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": (f"one round of {cfg.name}: full selection ({t_sel:.2f} s), attention on "
-                   f"{done}/{len(rows)} (node, head) rows extrapolated to all ({t_attn:.1f} s), "
-                   f"walk ({t_walk:.3f} s); fp64 NumPy"),
+        "sample": f"one round of {cfg.name}, fp64 NumPy oracle: {desc}",
+        "cpu_model": model,
+        "cores_available": int(avail),
+        "single_thread": single,
     }
 
 
