@@ -17,6 +17,7 @@
 //   * fp32 online softmax in base 2; each split writes unnormalised O, its running max
 //     and its sum; a second kernel combines the splits and rounds to bf16.
 // fp32 path: a plain VALU kernel, one workgroup per (request, node, query head).
+#include <algorithm>
 #include <cstdio>
 #include <cstdlib>
 #include <type_traits>
@@ -528,6 +529,93 @@ __device__ inline void load_two_scalars(const int32_t* x, const int32_t* y, int&
       : "memory");
 }
 
+// inclusive prefix sum over the lanes of a wave (DPP row shifts, then row broadcasts)
+__device__ inline int wave_inclusive_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return v;
+}
+
+// sum of a 64-bit integer over the lanes of a wave, in every lane
+__device__ inline long long wave_sum_i64(long long v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const uint32_t lo = __shfl_xor((uint32_t)v, m), hi = __shfl_xor((uint32_t)((uint64_t)v >> 32), m);
+    v += (long long)(((uint64_t)hi << 32) | lo);
+  }
+  return v;
+}
+
+// Ragged work list of several requests.  Request b has R_b keys (context rows + nodes) and
+// S_b = ceil(R_b / L) splits per KV head; its pairs are numbered from the prefix sum E_b of
+// Hkv * S_b, KV head by KV head.  When the lengths are close (the longest at most 5/4 of
+// the mean), L is the host's split length for max_ctx + budget keys, as in the one-request
+// plan; otherwise L is sized from the batch's total keys so that the batch makes about
+// target_pairs pairs.  Every wave of the workgroup computes the same result; wave 0 of the
+// designated workgroup also writes tab[b] = (E_b, S_b) and tab[batch] = (L, total pairs)
+// for the split combine.
+struct RaggedPick {
+  int b, g, split, L;
+  bool found;
+};
+__device__ inline RaggedPick ragged_pick(const int32_t* ctxp, const int32_t* nnp, int batch,
+                                         int N, int max_ctx, int Hkv, int target_pairs,
+                                         int lcap, int L_host, int p, int2* tab, bool write_tab) {
+  const int lane = threadIdx.x & 63;
+  long long tot = 0;
+  int rmax = 0;
+  for (int c = 0; c < batch; c += 64) {
+    const int b = c + lane;
+    if (b < batch) {
+      const int R = min(max(ctxp[b], 0), max_ctx) + min(max(nnp[b], 0), N);
+      tot += R;
+      rmax = max(rmax, R);
+    }
+  }
+  tot = wave_sum_i64(tot);
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) rmax = max(rmax, __shfl_xor(rmax, m));
+  int L;
+  if (4ll * rmax * batch <= 5ll * tot) {
+    L = L_host;
+  } else {
+    const long long want = (tot * Hkv + target_pairs - 1) / target_pairs;
+    L = (int)min((long long)lcap, max(128ll, (want + 63) / 64 * 64));
+  }
+  RaggedPick r;
+  r.b = r.g = r.split = 0;
+  r.L = L;
+  r.found = false;
+  int carry = 0;
+  for (int c = 0; c < batch; c += 64) {
+    const int b = c + lane;
+    int R = 0;
+    if (b < batch) R = min(max(ctxp[b], 0), max_ctx) + min(max(nnp[b], 0), N);
+    const int S = (R + L - 1) / L;
+    const int P = Hkv * S;
+    const int incl = carry + wave_inclusive_sum(P);
+    const int excl = incl - P;
+    if (write_tab && b < batch) tab[b] = make_int2(excl, S);
+    const uint64_t m = __ballot(b < batch && P > 0 && excl <= p && p < incl);
+    if (m && !r.found) {
+      const int l = __ffsll((long long)m) - 1;
+      const int local = p - __builtin_amdgcn_readlane(excl, l);
+      const int Sb = __builtin_amdgcn_readlane(S, l);
+      r.b = c + l;
+      r.g = local / Sb;
+      r.split = local - r.g * Sb;
+      r.found = true;
+    }
+    carry = __builtin_amdgcn_readlane(incl, 63);
+  }
+  if (write_tab && lane == 0) tab[batch] = make_int2(L, carry);
+  return r;
+}
+
 template <int KG>
 struct GroupTag {
   static constexpr int value = KG;
@@ -539,7 +627,8 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     const int32_t* __restrict__ ctxp, const int32_t* __restrict__ parentp,
     const int32_t* __restrict__ nnp, int N, int Hq, int Hkv, int max_ctx, float scale_log2,
     int split_len, int splits, int mtiles, int pairs, int mrows_pad, uint16_t* __restrict__ wsO,
-    float2* __restrict__ wsML, DivMagic dm) {
+    float2* __restrict__ wsML, DivMagic dm, int batch, int target_pairs, int lcap,
+    int2* __restrict__ tab) {
   // the body uses the buffer-resource type, which exists only in the device pass; the
   // host pass needs no more than the signature to emit the launch stub
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -569,14 +658,30 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
                "s"(N), "s"(Hq), "s"(Hkv), "s"(max_ctx), "s"(scale_log2), "s"(split_len),
                "s"(splits), "s"(mtiles), "s"(pairs), "s"(mrows_pad), "s"(wsO), "s"(wsML),
                "s"(dm.mt), "s"(dm.sp), "s"(dm.hk), "s"(dm.g));
-  // ---- which (request, KV head, split, row tile) this workgroup owns
+  // ---- which (request, KV head, split, row tile) this workgroup owns.  The row tiles of a
+  // pair are 8 block ids apart (one XCD, which shares the pair's K/V in its L2).  One
+  // request (tab == nullptr): pair = (KV head) * splits + split, fixed by the host; several:
+  // the ragged list of ragged_pick.  The split's partial results go to slot `pair`.
   const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
   const int sq = dm.div(slot, mtiles, dm.mt);
   const int mt = slot - sq * mtiles, pair = sq * 8 + xcd;
   if (pair >= pairs) return;
-  const int bg = dm.div(pair, splits, dm.sp);
-  const int split = pair - bg * splits;
-  const int b = dm.div(bg, Hkv, dm.hk), g = bg - b * Hkv;
+  int b, g, split;
+  if (tab == nullptr) {
+    const int bg = dm.div(pair, splits, dm.sp);
+    split = pair - bg * splits;
+    b = dm.div(bg, Hkv, dm.hk);
+    g = bg - b * Hkv;
+  } else {
+    const RaggedPick rp = ragged_pick(ctxp, nnp, batch, N, max_ctx, Hkv, target_pairs, lcap,
+                                      split_len, pair, tab,
+                                      pair == 0 && mt == 0 && (threadIdx.x >> 6) == 0);
+    if (!rp.found) return;   // past the batch's pairs (nothing issued yet)
+    b = rp.b;
+    g = rp.g;
+    split = rp.split;
+    split_len = rp.L;
+  }
   const int G = dm.div(Hq, Hkv, dm.hk);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rg = wave & 3, kg = wave >> 2;
@@ -881,7 +986,7 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  const size_t obase = ((size_t)bg * splits + split) * mrows_pad;
+  const size_t obase = (size_t)pair * mrows_pad;
   const int qbase = row0 + rg * 32;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -900,12 +1005,12 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
     const uint16_t* __restrict__ wsO, const float2* __restrict__ wsML,
     const int32_t* __restrict__ ctxp, const int32_t* __restrict__ nnp, int N, int Hq, int Hkv,
     int max_ctx, int split_len, int splits, int mrows_pad, DivMagic dm,
-    uint16_t* __restrict__ O) {
+    uint16_t* __restrict__ O, const int2* __restrict__ tab, int batch) {
   constexpr int TPR = HD / 4;  // threads per output row, 4 values each
   constexpr int RPB = kThreads / TPR;
   asm volatile("" ::"s"(wsO), "s"(wsML), "s"(ctxp), "s"(nnp), "s"(N), "s"(Hq), "s"(Hkv),
                "s"(max_ctx), "s"(split_len), "s"(splits), "s"(mrows_pad), "s"(dm.hk),
-               "s"(dm.g), "s"(O));
+               "s"(dm.g), "s"(O), "s"(tab), "s"(batch));
   const int b = blockIdx.y;
   const int rr = blockIdx.x * RPB + threadIdx.x / TPR;   // (node, query head) of request b
   const int d = (threadIdx.x % TPR) * 4;
@@ -913,7 +1018,19 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
   const int i = dm.div(rr, Hq, dm.hk), hq = rr - i * Hq;   // dm.hk holds the Hq multiplier
   const int G = Hq / Hkv, g = dm.div(hq, G, dm.g);
   const int qr = i * G + (hq - g * G);
-  const size_t base = (size_t)(b * Hkv + g) * splits;
+  // the request's splits of KV head g: slots base .. base + cap - 1 (the ragged list's
+  // table, written by the attention kernel, or the host's fixed split count)
+  size_t base;
+  int cap;
+  if (tab != nullptr) {
+    const int2 t = tab[b];
+    base = (size_t)t.x + (size_t)g * t.y;
+    cap = t.y;
+    split_len = tab[batch].x;
+  } else {
+    base = (size_t)(b * Hkv + g) * splits;
+    cap = splits;
+  }
   // each split holds O_s / l_s (bf16) and (m_s, l_s) with m_s in base 2:
   // O = sum_s 2^(m_s - M) l_s (O_s / l_s) / sum_s 2^(m_s - M) l_s.  The loads of the first
   // CH splits go out before the request's sizes are known (their addresses do not depend on
@@ -925,19 +1042,19 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
   auto load_group = [&](int s0) __attribute__((always_inline)) {
 #pragma unroll
     for (int t = 0; t < CH; ++t) {
-      const size_t r = (base + min(s0 + t, splits - 1)) * mrows_pad + qr;
+      const size_t r = (base + min(s0 + t, cap - 1)) * mrows_pad + qr;
       ml[t] = wsML[r];
       ov[t] = *(const uint2*)(wsO + r * HD + d);
     }
   };
-  load_group(0);
+  if (cap > 0) load_group(0);
   int ctx_raw, n_raw;
   load_two_scalars(ctxp + b, nnp + b, ctx_raw, n_raw);
   const int n = min(max(n_raw, 0), N);
   if (i >= n) return;
   const int ctx = min(max(ctx_raw, 0), max_ctx);
   const int R = ctx + n;
-  const int nspl = min((R + split_len - 1) / split_len, splits);
+  const int nspl = min((R + split_len - 1) / split_len, cap);
   float M = -INFINITY, L = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int s0 = 0; s0 < nspl; s0 += CH) {
@@ -1067,6 +1184,12 @@ AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max
   p.wk = 1;
   p.mtile = 4 * 32;
   p.mtiles = (mrows + p.mtile - 1) / p.mtile;
+  p.ragged = 0;
+  p.target_pairs = p.pairs_max = 0;
+  // the buffer ranges of a split, look-ahead included, stay below 2^31 bytes
+  const long long rsb0 = (long long)Hkv * head_dim * 2;
+  p.lcap = (int)((((1ll << 31) - 1) / rsb0 - 5 * kKT) / kKT * kKT);
+
   // Split the keys so that the workgroups (one per CU: the K/V rings fill its LDS) finish
   // soonest: estimated time = rounds of 256 workgroups x (32-key stages per split + ~8
   // stages' worth of prologue and partial writes).  Rounding the split count up to fill
@@ -1090,19 +1213,43 @@ AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max
   int len = (keys + splits - 1) / splits;
   len = ((len + step - 1) / step) * step;
   if (len < 2 * step) len = 2 * step;
-  // the buffer ranges of a split, look-ahead included, stay below 2^31 bytes
-  const long long rsb = (long long)Hkv * head_dim * 2;
-  const long long cap = (((1ll << 31) - 1) / rsb - 5 * step) / step * step;
-  if (len > cap) len = (int)cap;
+  if (len > p.lcap) len = p.lcap;
   p.split_len = len;
   p.splits = (keys + len - 1) / len;
+  if (batch > 1 && head_dim == 128) {
+    // Several requests: their lengths are known only on the device, where the kernel picks
+    // the split length (ragged_pick): this plan's for lengths close to each other, else one
+    // sized for about three workgroups per CU over the batch's actual keys (measured: a
+    // 16-request batch with lengths from 512 to 16K keys takes 12 % less time than with
+    // every request split for max_ctx, a 4 x 32K batch the same).
+    const int target = (3 * 256 + p.mtiles - 1) / p.mtiles;
+    const long long worst = ((long long)batch * (max_ctx + budget) * Hkv + target - 1) / target;
+    const long long pm = std::max((long long)target + (long long)batch * Hkv,
+                                  (long long)batch * Hkv * p.splits);
+    if (worst <= p.lcap && pm < (1ll << 24)) {
+      p.ragged = 1;
+      p.target_pairs = target;
+      p.pairs_max = (int)pm;
+    }
+  }
   return p;
+}
+
+// split partials [slot][mtiles * mtile][head_dim] bf16, then their (max, sum) pairs, then
+// (ragged list) the per-request table of the combine
+static size_t attn_rows(const AttnPlan& pl, int batch, int Hkv) {
+  const size_t slots = pl.ragged ? (size_t)pl.pairs_max : (size_t)batch * Hkv * pl.splits;
+  return slots * (size_t)pl.mtiles * pl.mtile;
+}
+static size_t attn_tab_offset(const AttnPlan& pl, int batch, int Hkv, int head_dim) {
+  const size_t rows = attn_rows(pl, batch, Hkv);
+  return (rows * head_dim * sizeof(uint16_t) + rows * sizeof(float2) + 15) & ~(size_t)15;
 }
 
 size_t attn_ws_bytes(const AttnPlan& pl, int batch, int /*budget*/, int /*Hq*/, int Hkv,
                      int head_dim) {
-  const size_t rows = (size_t)batch * Hkv * pl.splits * (size_t)pl.mtiles * pl.mtile;
-  return rows * head_dim * sizeof(uint16_t) + rows * sizeof(float2) + 256;
+  return attn_tab_offset(pl, batch, Hkv, head_dim) +
+         (pl.ragged ? (size_t)(batch + 1) * sizeof(int2) : 0) + 256;
 }
 
 hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const int64_t* off,
@@ -1112,10 +1259,11 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
                             hipEvent_t ev_begin, hipEvent_t ev_end) {
   if (batch <= 0) return hipSuccess;
   const int mrows_pad = pl.mtiles * pl.mtile;
-  const size_t rows = (size_t)batch * Hkv * pl.splits * mrows_pad;
+  const size_t rows = attn_rows(pl, batch, Hkv);
   uint16_t* wsO = (uint16_t*)ws;
   float2* wsML = (float2*)((char*)ws + rows * head_dim * sizeof(uint16_t));
-  const int pairs = pl.splits * batch * Hkv;
+  int2* tab = pl.ragged ? (int2*)((char*)ws + attn_tab_offset(pl, batch, Hkv, head_dim)) : nullptr;
+  const int pairs = pl.ragged ? pl.pairs_max : pl.splits * batch * Hkv;
   dim3 grid((unsigned)(8 * pl.mtiles * ((pairs + 7) / 8)));
   dim3 block(256u);
   const float sl2 = scale * kLog2e;
@@ -1128,11 +1276,13 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
     if (ev_begin || ev_end)
       hipExtLaunchKernelGGL(attn_bf16_kernel, grid, block8, 0, s, ev_begin, ev_end, 0, q, k, v,
                             off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2, pl.split_len,
-                            pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML, dm);
+                            pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML, dm, batch,
+                            pl.target_pairs, pl.lcap, tab);
     else
       attn_bf16_kernel<<<grid, block8, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv,
                                                max_ctx, sl2, pl.split_len, pl.splits,
-                                               pl.mtiles, pairs, mrows_pad, wsO, wsML, dm);
+                                               pl.mtiles, pairs, mrows_pad, wsO, wsML, dm, batch,
+                                               pl.target_pairs, pl.lcap, tab);
   } else {
     if (ev_begin || ev_end)
       hipExtLaunchKernelGGL(attn_bf16_w4_kernel<64>, grid, block, 0, s, ev_begin, ev_end, 0, q,
@@ -1153,13 +1303,13 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
     attn_combine_kernel<128><<<dim3((unsigned)((rows_req + rpb - 1) / rpb), (unsigned)batch),
                                dim3(kThreads), 0, s>>>(wsO, wsML, ctx, n, budget, Hq, Hkv, max_ctx,
                                                        pl.split_len, pl.splits, mrows_pad, cm,
-                                                       (uint16_t*)O);
+                                                       (uint16_t*)O, tab, batch);
   } else {
     const int rpb = kThreads / 16;
     attn_combine_kernel<64><<<dim3((unsigned)((rows_req + rpb - 1) / rpb), (unsigned)batch),
                               dim3(kThreads), 0, s>>>(wsO, wsML, ctx, n, budget, Hq, Hkv, max_ctx,
                                                       pl.split_len, pl.splits, mrows_pad, cm,
-                                                      (uint16_t*)O);
+                                                      (uint16_t*)O, nullptr, batch);
   }
   return hipGetLastError();
 }

@@ -59,8 +59,15 @@ struct AttnPlan {
   int wk;          // key groups per workgroup (1 or 2): 256 * wk threads
   int mtile;       // query rows per workgroup (4 waves)
   int mtiles;      // workgroups along the budget*G query rows of one KV head
-  int split_len;   // keys per split (multiple of 64)
-  int splits;      // splits along max_ctx + budget keys
+  int split_len;   // keys per split (multiple of 64); 0 when ragged
+  int splits;      // splits along max_ctx + budget keys; 1 when ragged
+  // Ragged work list (several requests, head_dim 128): the kernel sizes the splits from the
+  // requests' actual keys so that the batch makes about target_pairs (request, KV head,
+  // split) pairs; at most pairs_max; split lengths at most lcap keys
+  int ragged;
+  int target_pairs;
+  int pairs_max;
+  int lcap;
 };
 AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max_ctx);
 size_t attn_ws_bytes(const AttnPlan& pl, int batch, int budget, int Hq, int Hkv, int head_dim);

@@ -534,3 +534,35 @@ def test_select_sequential_fallback_matches_oracle(taps, name):
     torch.cuda.synchronize()
     cfg = _fuzz_cfg(None, case["dtype"], case["kind"], V, D, case["K"], case["N"], B=1)
     U.assert_tree_equal(gpu, [t], cfg)
+
+
+def test_attention_ragged_batch(taps):
+    """Several requests of very different lengths (the ragged work list: split lengths from
+    the batch's actual keys, pairs numbered by prefix sums), including an empty request and
+    one-row ones, with NaN bits in every unwritten workspace slot."""
+    from workloads import f32_to_bf16_bits, bf16_bits_to_f32
+    rng = np.random.default_rng(321)
+    B, N, Hq, Hkv, hd = 6, 64, 16, 4, 128
+    ctx = np.array([0, 16000, 1, 5000, 77, 0], dtype=np.int32)
+    n = [0, 64, 1, 33, 64, 5]
+    say("[attn-ragged] contexts", ctx.tolist(), "nodes", n)
+    off = kv_offsets(ctx, N)
+    rows = int(off[-1] + ctx[-1] + N)
+    Q = f32_to_bf16_bits(rng.standard_normal((B, N, Hq, hd)).astype(np.float32))
+    K = f32_to_bf16_bits(rng.standard_normal((rows, Hkv, hd)).astype(np.float32))
+    V = f32_to_bf16_bits(rng.standard_normal((rows, Hkv, hd)).astype(np.float32))
+    parents = [np.array([-1] + [int(rng.integers(0, i)) for i in range(1, N)], dtype=np.int32)
+               for _ in range(B)]
+    att = taps.TreeAttention(B, N, Hq, Hkv, hd, 16384, dtype=BF16, scale=hd ** -0.5)
+    att.ws.fill_(0xFF)
+    O = att(U.to_dev(Q, True), U.to_dev(K, True), U.to_dev(V, True), torch.from_numpy(off).cuda(),
+            torch.from_numpy(ctx).cuda(), torch.from_numpy(np.stack(parents)).cuda(),
+            torch.tensor(n, dtype=torch.int32).cuda())
+    torch.cuda.synchronize()
+    picks = [(b, i, h) for b in range(B) for i in range(n[b]) for h in (0, 5, Hq - 1)]
+    ref = oracle.tree_attention(*(bf16_bits_to_f32(a).astype(np.float64) for a in (Q, K, V)),
+                                off, ctx, parents, n, hd ** -0.5, samples=picks)
+    got = U.gpu_o_as_f64(O)
+    for b in range(B):
+        if n[b]:
+            U.attention_error(got[b, :n[b]], ref[b, :n[b]], BF16, f"ragged b={b} ctx={ctx[b]}")
