@@ -98,8 +98,7 @@ hipError_t launch_commit(void* K, void* V, const int64_t* off, const int32_t* ct
 // epilogue (RMSNorm, rotary positions, bf16 Q and cache rows) and the output reduction
 struct GemmPlan {
   int splits;   // K splits (partials), each a multiple of 64 K values
-  int unroll;   // 16-value MFMA steps per load batch (1, 2 or 4)
-  int cols;     // output columns per workgroup (32 or 64)
+  int cols;     // output columns per workgroup (64, 96 or 128)
 };
 GemmPlan plan_gemm(int M, int N, int K);
 hipError_t launch_gemm_bf16(const void* X, int M, int K, const void* w0, int n0, const void* w1,

@@ -5,15 +5,20 @@
 //
 //   gemm_kernel       Y_part = X W^T for a skinny X (the budget's nodes) and a large
 //                     row-major weight [N][K]: HBM-bound on the weight, which is read once.
-//                     A workgroup owns 32 output columns, 64 rows and one split of K; each
-//                     of its four waves takes a quarter of that split on
-//                     v_mfma_f32_32x32x16_bf16, and the waves' partials are added in LDS
-//                     in a fixed order.  Split partials (fp32) are added by the consumer.
+//                     A workgroup owns 64, 96 or 128 output columns, 64 rows and one split
+//                     of K, planned so that the workgroups fill the 256 CUs in as few rounds
+//                     as possible (one round of exactly 256 at the Qwen3-8B shapes).  The
+//                     weight rows and X stream through a ring of LDS stages by direct loads
+//                     (~60 KB of weight in flight per CU, which HBM's latency asks for);
+//                     each of the four waves takes one 16-value k-step of every 64-value
+//                     stage on v_mfma_f32_32x32x16_bf16, and the waves' partials are added in
+//                     LDS in a fixed order.  Split partials (fp32) are added by the consumer.
 //   qkv_rope_kernel   adds the projection's split partials, applies the per-head RMSNorm
 //                     and the rotary embedding at position ctx + depth, and stores Q and the
 //                     cache rows ctx + i of K and V in bf16.
 //   reduce_kernel     adds the output projection's split partials and rounds to bf16.
 #include "common.h"
+#include "ldsload.h"
 
 namespace taps {
 namespace {
@@ -38,26 +43,89 @@ struct WSeg {
   int end0, end1;
 };
 
-template <int U, int NB>
+// Waits until at most c * PER vector-memory operations of this wave are outstanding, for a
+// uniform c in [0, C] (s_waitcnt takes its count as an immediate).
+template <int PER, int C>
+__device__ inline void wait_later(int c) {
+  if constexpr (C <= 0) {
+    TAPS_WAIT_VMCNT(0);
+  } else {
+    if (c >= C) TAPS_WAIT_VMCNT(C * PER);
+    else wait_later<PER, C - 1>(c);
+  }
+}
+
+// XOR key of the 16-byte chunks of a 128-byte LDS row: 16 lanes reading the same logical
+// chunk of 16 consecutive rows hit 16 distinct chunk positions of the 256-byte bank window
+__device__ inline int row_swz(int r) { return (r >> 1) & 7; }
+
+// Y_part[split] = X W^T over one split of K for 32 * NB output columns and 64 rows.
+// Every global read is a direct load into a ring of D LDS stages; a stage is 64 values of K:
+// the weight rows of the tile (32 * NB x 128 bytes) and the 64 X rows (64 x 128 bytes).
+// Each 128-byte row keeps its 16-byte chunks XOR-permuted by row_swz.  Wave w takes the
+// 16-value k-step w of every stage, so each wave holds a partial sum of the whole tile; the
+// four partials are added in LDS in a fixed order at the end.
+template <int NB, int D>
 __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ X, int M, int K,
                                                    WSeg ws, int N, int splits,
                                                    float* __restrict__ part) {
-  __shared__ float red[4][2][16][kWave];
-  const int c0 = blockIdx.x * 32 * NB, split = blockIdx.y, m0 = blockIdx.z * 64;
-  const uint16_t* W = c0 < ws.end0 ? ws.w0 + (size_t)c0 * K
-                      : c0 < ws.end1 ? ws.w1 + (size_t)(c0 - ws.end0) * K
-                                     : ws.w2 + (size_t)(c0 - ws.end1) * K;
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  constexpr int WROWS = 32 * NB;     // weight rows (output columns) of the tile
+  constexpr int WSLOT = WROWS * 128;
+  constexpr int XSLOT = 64 * 128;
+  constexpr int PER = NB + 2;        // direct loads per wave and stage (NB of W, 2 of X)
+  constexpr int WPART = 2 * 16 * kWave;   // floats of one wave's partial of a column block
+  static_assert(D * (WSLOT + XSLOT) >= NB * 4 * WPART * 4, "the reduction reuses the ring");
+  static_assert((D - 2) * PER <= 63, "vmcnt counts at most 63 operations");
+  __shared__ __attribute__((aligned(16))) unsigned char s_ring[D * (WSLOT + XSLOT)];
+  asm volatile("" ::"s"(X), "s"(M), "s"(K), "s"(N), "s"(splits), "s"(part));
+  const int c0 = blockIdx.x * WROWS, split = blockIdx.y, m0 = blockIdx.z * 64;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int l32 = lane & 31, hl = lane >> 5;
-  const int kper = K / (splits * 4);                 // K values per wave, a multiple of 32 U
-  const int kb = split * (K / splits) + wave * kper + 8 * hl;
-  // MFMA operands: lane (l32, hl) holds 8 consecutive K values at 8 hl of each 16-value
-  // step, of output row l32 (X) and of output column l32 of each 32-column block (W);
-  // rows past M repeat row M-1
-  const uint16_t* wp = W + (size_t)l32 * K + kb;
-  const size_t wnb = (size_t)32 * K;                 // next 32-column block
-  const uint16_t* x0 = X + (size_t)min(m0 + l32, M - 1) * K + kb;
-  const uint16_t* x1 = X + (size_t)min(m0 + 32 + l32, M - 1) * K + kb;
+  const int Ks = K / splits, S = Ks / 64, kb = split * Ks;
+  const uint32_t rowb = (uint32_t)K * 2;
+  const int mrows = min(64, M - m0);
+
+  // direct loads: wave-load g of a stage fills 1 KB = 8 rows (128 bytes each) of a slot;
+  // lane i takes row 8g + i / 8, chunk position i % 8, i.e. global chunk
+  // (i % 8) ^ row_swz(row).  Wave w issues W loads g = NB w .. NB w + NB - 1 (the tile's
+  // weight rows 8g ..) and X loads g = 2w, 2w + 1.
+  i32x4 wrs[NB];
+  uint32_t woff[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int g = NB * wave + j, gc = c0 + 8 * g;   // first output column of the 8 rows
+    // the 8 rows lie in one weight array (its column count is a multiple of 8); the
+    // resource covers exactly them
+    const uint16_t* rows8 = gc < ws.end0   ? ws.w0 + (size_t)gc * K
+                            : gc < ws.end1 ? ws.w1 + (size_t)(gc - ws.end0) * K
+                                           : ws.w2 + (size_t)(gc - ws.end1) * K;
+    wrs[j] = buffer_rsrc(rows8, 8u * rowb);
+    const int r = 8 * g + (lane >> 3);
+    woff[j] = (uint32_t)(lane >> 3) * rowb + (uint32_t)(kb + 8 * ((lane & 7) ^ row_swz(r))) * 2u;
+  }
+  const i32x4 xrs = buffer_rsrc(X + (size_t)m0 * K, (uint32_t)mrows * rowb);
+  uint32_t xoff[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int r = 8 * (2 * wave + j) + (lane >> 3);   // rows past M repeat row M - 1
+    xoff[j] = (uint32_t)min(r, mrows - 1) * rowb +
+              (uint32_t)(kb + 8 * ((lane & 7) ^ row_swz(r))) * 2u;
+  }
+  auto issue = [&](int slot, int st) __attribute__((always_inline)) {
+    unsigned char* sw = s_ring + slot * WSLOT;
+    unsigned char* sx = s_ring + D * WSLOT + slot * XSLOT;
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      load_lds16(wrs[j], sw + (NB * wave + j) * 1024, woff[j] + (uint32_t)st * 128u);
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      load_lds16(xrs, sx + (2 * wave + j) * 1024, xoff[j] + (uint32_t)st * 128u);
+  };
+
+  // MFMA operands: lane (l32, hl) reads 8 K values (chunk 2w + hl of the stage) of X row
+  // l32 (+32) and of weight row l32 (+32 per column block)
+  const int rdo = l32 * 128 + 16 * ((2 * wave + hl) ^ row_swz(l32));
   f32x16 acc[2][NB];
 #pragma unroll
   for (int r = 0; r < 2; ++r)
@@ -65,55 +133,67 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
     for (int c = 0; c < NB; ++c)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[r][c][v] = 0.f;
-  // two register batches of U steps: the next batch's loads are in flight while the
-  // current one feeds the MFMAs
-  bf16x8 wA[NB][U], xA[2][U], wB[NB][U], xB[2][U];
-  auto load = [&](bf16x8 (&w)[NB][U], bf16x8 (&y)[2][U], int k) __attribute__((always_inline)) {
+  auto compute = [&](int slot) __attribute__((always_inline)) {
+    const unsigned char* sw = s_ring + slot * WSLOT + rdo;
+    const unsigned char* sx = s_ring + D * WSLOT + slot * XSLOT + rdo;
+    bf16x8 xa[2], wb[NB];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
+    for (int r = 0; r < 2; ++r) xa[r] = *(const bf16x8*)(sx + r * 32 * 128);
 #pragma unroll
-      for (int c = 0; c < NB; ++c) w[c][u] = *(const bf16x8*)(wp + c * wnb + k + 16 * u);
-      y[0][u] = *(const bf16x8*)(x0 + k + 16 * u);
-      y[1][u] = *(const bf16x8*)(x1 + k + 16 * u);
+    for (int c = 0; c < NB; ++c) wb[c] = *(const bf16x8*)(sw + c * 32 * 128);
+#pragma unroll
+    for (int c = 0; c < NB; ++c)
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+        acc[r][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa[r], wb[c], acc[r][c], 0, 0, 0);
+  };
+
+  // stages 0 .. D - 2 in flight first; at stage s, once its loads have landed (every
+  // wave's: the barrier), slot (s - 1) % D is free and takes stage s + D - 1
+  for (int s = 0; s < D - 1 && s < S; ++s) issue(s, s);
+  for (int s0 = 0; s0 < S; s0 += D) {
+#pragma unroll
+    for (int i = 0; i < D; ++i) {
+      const int s = s0 + i;
+      if (s < S) {   // uniform; a guard, not an early exit, so that the loop unrolls fully
+        // this wave's loads still allowed in flight: stages s + 1 .. min(S, s + D - 1) - 1
+        const int later = min(S - 1 - s, D - 2);
+        if (later == D - 2) TAPS_WAIT_VMCNT((D - 2) * PER);
+        else wait_later<PER, D - 3>(later);
+        TAPS_LDS_BARRIER();   // every wave's loads of stage s landed; slot (s - 1) % D is read
+        if (s + D - 1 < S) issue((i + D - 1) % D, s + D - 1);
+        compute(i);
+      }
     }
-  };
-  auto mma = [&](const bf16x8 (&w)[NB][U], const bf16x8 (&y)[2][U])
-      __attribute__((always_inline)) {
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int c = 0; c < NB; ++c)
-#pragma unroll
-        for (int r = 0; r < 2; ++r)
-          acc[r][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(y[r][u], w[c][u], acc[r][c], 0, 0, 0);
-  };
-  load(wA, xA, 0);
-  for (int k = 0; k < kper; k += 32 * U) {
-    const bool second = k + 16 * U < kper;
-    if (second) load(wB, xB, k + 16 * U);
-    mma(wA, xA);
-    if (k + 32 * U < kper) load(wA, xA, k + 32 * U);
-    if (second) mma(wB, xB);
   }
-  // the four waves' partials are added in LDS in a fixed order, one 32-column block at a
-  // time; accumulator element v of lane l is row 8 (v / 4) + 4 (l / 32) + v % 4, column
-  // l % 32
+  TAPS_WAIT_VMCNT(0);
+  __syncthreads();   // every wave is done with the ring
+
+  // The four waves' partials of every column block go to LDS at once; then each thread
+  // adds the four values of its outputs in a fixed order and stores the sums.  No barrier
+  // follows the stores, so they all stay in flight together.  Accumulator element v of
+  // lane l is row 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32 of its 32 x 32 block.
+  float* red = (float*)s_ring;   // [column block][wave][row block][v][lane]
 #pragma unroll
-  for (int c = 0; c < NB; ++c) {
-    if (c > 0) __syncthreads();
+  for (int c = 0; c < NB; ++c)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      red[wave][0][v][lane] = acc[0][c][v];
-      red[wave][1][v][lane] = acc[1][c][v];
-    }
-    __syncthreads();
-    for (int e = tid; e < 2 * 16 * kWave; e += 256) {
-      const int ln = e & (kWave - 1), v = (e / kWave) & 15, rb = e / (16 * kWave);
-      const float sum = ((red[0][rb][v][ln] + red[1][rb][v][ln]) + red[2][rb][v][ln]) +
-                        red[3][rb][v][ln];
-      const int row = m0 + rb * 32 + 8 * (v >> 2) + 4 * (ln >> 5) + (v & 3);
-      if (row < M) part[((size_t)split * M + row) * N + c0 + 32 * c + (ln & 31)] = sum;
-    }
+    for (int r = 0; r < 2; ++r)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) red[(((c * 4 + wave) * 2 + r) * 16 + v) * kWave + lane] = acc[r][c][v];
+  TAPS_LDS_BARRIER();
+  // four consecutive columns of one row per thread and step: one 16-byte store each
+  constexpr int Q4 = WPART / 4;
+  const float4* red4 = (const float4*)s_ring;
+#pragma unroll
+  for (int k = 0; k < NB * Q4 / 256; ++k) {
+    const int e4 = tid + 256 * k, c = e4 / Q4, w4 = e4 - c * Q4, e = 4 * w4;
+    const int ln = e & (kWave - 1), v = (e / kWave) & 15, rb = e / (16 * kWave);
+    const float4* q = red4 + c * 4 * Q4 + w4;
+    const float4 a = q[0], b = q[Q4], d = q[2 * Q4], f = q[3 * Q4];
+    const float4 sum = make_float4(((a.x + b.x) + d.x) + f.x, ((a.y + b.y) + d.y) + f.y,
+                                   ((a.z + b.z) + d.z) + f.z, ((a.w + b.w) + d.w) + f.w);
+    const int row = m0 + rb * 32 + 8 * (v >> 2) + 4 * (ln >> 5) + (v & 3);
+    if (row < M) *(float4*)(part + ((size_t)split * M + row) * N + c0 + 32 * c + (ln & 31)) = sum;
   }
 }
 
@@ -189,16 +269,33 @@ __global__ __launch_bounds__(256) void reduce_kernel(const float* __restrict__ p
 }  // namespace
 
 GemmPlan plan_gemm(int M, int N, int K) {
-  GemmPlan p;
-  // 64 columns per workgroup halve the re-reads of X against 32; N is a multiple of 64
-  p.cols = N % 64 == 0 ? 64 : 32;
-  const long long tiles = (long long)(N / p.cols) * ((M + 63) / 64);
-  p.splits = 1;
-  while (p.splits < 16 && tiles * p.splits < 256 && K % (2 * p.splits * 64) == 0) p.splits *= 2;
-  const int steps = K / (p.splits * 4 * 16);
-  p.unroll = p.cols == 64 ? 2 : 4;   // two batches in registers keep two waves per SIMD
-  while (steps % p.unroll) p.unroll /= 2;
-  return p;
+  // Candidates (64, 96 or 128 columns per workgroup; K splits 1 .. 16)
+  // are ranked by how full their last round of workgroups leaves the 256 CUs (one
+  // workgroup per CU: the ring takes most of the LDS), then by fewer rounds, then by fewer
+  // splits (less partial traffic).  N is a multiple of 64 and K of 64, so 64 columns and
+  // one split always qualify.
+  const long long mt = (M + 63) / 64;
+  GemmPlan best{1, 64};
+  double best_fill = -1.0;
+  long long best_rounds = 0;
+  for (int nb = 2; nb <= 4; ++nb) {
+    if (N % (32 * nb) != 0) continue;
+    for (int sp = 1; sp <= 16 && K % (64 * sp) == 0; sp *= 2) {
+      const long long wgs = (long long)(N / (32 * nb)) * sp * mt;
+      const long long rounds = (wgs + 255) / 256;
+      const double fill = (double)wgs / (double)(rounds * 256);
+      const bool better =
+          fill > best_fill + 1e-9 ||
+          (fill > best_fill - 1e-9 &&
+           (rounds < best_rounds || (rounds == best_rounds && sp < best.splits)));
+      if (better) {
+        best = GemmPlan{sp, 32 * nb};
+        best_fill = fill;
+        best_rounds = rounds;
+      }
+    }
+  }
+  return best;
 }
 
 hipError_t launch_gemm_bf16(const void* X, int M, int K, const void* w0, int n0, const void* w1,
@@ -206,22 +303,15 @@ hipError_t launch_gemm_bf16(const void* X, int M, int K, const void* w0, int n0,
                             hipStream_t s) {
   const WSeg ws{(const uint16_t*)w0, (const uint16_t*)w1, (const uint16_t*)w2, n0, n0 + n1};
   const int N = n0 + n1 + n2;
+  if (M <= 0) return hipSuccess;
   const dim3 grid((unsigned)(N / p.cols), (unsigned)p.splits, (unsigned)((M + 63) / 64));
   const uint16_t* x = (const uint16_t*)X;
-#define TAPS_GEMM(UU, NBB) gemm_kernel<UU, NBB><<<grid, 256, 0, s>>>(x, M, K, ws, N, p.splits, part)
-  if (p.cols == 64) {
-    switch (p.unroll) {
-      case 2: TAPS_GEMM(2, 2); break;
-      default: TAPS_GEMM(1, 2); break;
-    }
-  } else {
-    switch (p.unroll) {
-      case 4: TAPS_GEMM(4, 1); break;
-      case 2: TAPS_GEMM(2, 1); break;
-      default: TAPS_GEMM(1, 1); break;
-    }
+  switch (p.cols) {   // ring depth: 120-144 KB of LDS
+    case 64: gemm_kernel<2, 8><<<grid, 256, 0, s>>>(x, M, K, ws, N, p.splits, part); break;
+    case 96: gemm_kernel<3, 6><<<grid, 256, 0, s>>>(x, M, K, ws, N, p.splits, part); break;
+    case 128: gemm_kernel<4, 6><<<grid, 256, 0, s>>>(x, M, K, ws, N, p.splits, part); break;
+    default: return hipErrorInvalidValue;
   }
-#undef TAPS_GEMM
   return hipGetLastError();
 }
 
