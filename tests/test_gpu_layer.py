@@ -132,6 +132,14 @@ def test_layer_ragged_rows_span_several_tiles(taps):
          n=[40, 23, 31])
 
 
+def test_layer_many_rows_take_the_widest_gemm_tiles(taps):
+    """M = 8 x 128 = 1024 rows: the Q/K/V projection's plan takes 128 columns per workgroup
+    and one K split (the fewest rounds of workgroups), the output projection 64 columns and
+    eight splits; ragged node counts, empty and short contexts."""
+    _run(taps, np.random.default_rng(6), B=8, N=128, H=128, Hq=8, Hkv=4,
+         ctx=[30, 0, 65, 3, 100, 7, 12, 50], n=[128, 1, 77, 128, 5, 64, 100, 33])
+
+
 def test_layer_qwen3_8b_shape(taps):
     """One Qwen3-8B-shaped layer (hidden 4096, 32/8 heads x 128) over 8192 context rows
     and a 64-node tree; Y on the root, the last node and six random nodes."""
