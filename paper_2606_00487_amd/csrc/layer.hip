@@ -199,67 +199,84 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
 
 // One wave per (tree node, head): blockIdx.x is the node (row = b * budget + i), and
 // wave w of workgroup blockIdx.y takes head 4 blockIdx.y + w of the Hq query, Hkv key and
-// Hkv value heads.  head_dim 128: lane l holds dims l and l + 64, the rotary pair.
+// Hkv value heads.  head_dim 128: lane l holds dims l and l + 64, the rotary pair.  SP =
+// the projection's K splits: every load of the wave (the request's sizes, the node's depth
+// and cache offset, and all SP partials) is issued before any of them is used, so the
+// kernel waits for memory once.
+template <int SP>
 __global__ __launch_bounds__(256) void qkv_rope_kernel(
-    const float* __restrict__ part, int splits, int M, int budget, int Hq, int Hkv,
+    const float* __restrict__ part, int M, int budget, int Hq, int Hkv,
     const uint16_t* __restrict__ q_norm, const uint16_t* __restrict__ k_norm, double theta,
     float eps, const int64_t* __restrict__ off, const int32_t* __restrict__ ctxp,
     const int32_t* __restrict__ depthp, const int32_t* __restrict__ np_, int max_ctx,
     uint16_t* __restrict__ Q, uint16_t* __restrict__ Kc, uint16_t* __restrict__ Vc) {
   constexpr int HD = 128;
   const int row = blockIdx.x, b = row / budget, i = row - b * budget;
-  const int n = min(max(np_[b], 0), budget);
-  if (i >= n) return;
-  const int ctx = min(max(ctxp[b], 0), max_ctx);
-  const int pos = ctx + max(depthp[(size_t)b * budget + i], 0);
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   const int hs = blockIdx.y * 4 + wave;
   if (hs >= Hq + 2 * Hkv) return;
   const int N = (Hq + 2 * Hkv) * HD;
-  const size_t crow = (size_t)(off[b] + ctx + i) * Hkv;   // first head of the node's cache row
+  const int n_raw = np_[b], ctx_raw = ctxp[b], d_raw = depthp[(size_t)b * budget + i];
+  const int64_t kv0 = off[b];
+  float p0[SP], p1[SP];
+#pragma unroll
+  for (int s = 0; s < SP; ++s) {
+    const float* pr = part + ((size_t)s * M + row) * N + (size_t)hs * HD;
+    p0[s] = pr[lane];
+    p1[s] = pr[lane + 64];
+  }
+  const int n = min(max(n_raw, 0), budget);
+  if (i >= n) return;
+  const int ctx = min(max(ctx_raw, 0), max_ctx);
+  const int pos = ctx + max(d_raw, 0);
+  const size_t crow = (size_t)(kv0 + ctx + i) * Hkv;   // first head of the node's cache row
+  float x0 = 0.f, x1 = 0.f;
+#pragma unroll
+  for (int s = 0; s < SP; ++s) {   // the splits in order
+    x0 += p0[s];
+    x1 += p1[s];
+  }
+  if (hs >= Hq + Hkv) {             // value head: stored as projected
+    const size_t o = (crow + (hs - Hq - Hkv)) * HD;
+    Vc[o + lane] = f32_to_bf16(x0);
+    Vc[o + lane + 64] = f32_to_bf16(x1);
+    return;
+  }
   // rotation of the pair (lane, lane + 64) at this position, from fp64 angles
   const double ang = (double)pos * pow(theta, -2.0 * (double)lane / (double)HD);
   double sd, cd;
   sincos(ang, &sd, &cd);
   const float sn = (float)sd, cs = (float)cd;
-  {
-    float x0 = 0.f, x1 = 0.f;
-    for (int s = 0; s < splits; ++s) {
-      const float* pr = part + ((size_t)s * M + row) * N + (size_t)hs * HD;
-      x0 += pr[lane];
-      x1 += pr[lane + 64];
-    }
-    if (hs >= Hq + Hkv) {             // value head: stored as projected
-      const size_t o = (crow + (hs - Hq - Hkv)) * HD;
-      Vc[o + lane] = f32_to_bf16(x0);
-      Vc[o + lane + 64] = f32_to_bf16(x1);
-      return;
-    }
-    float ss = x0 * x0 + x1 * x1;
+  float ss = x0 * x0 + x1 * x1;
 #pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m);
-    const float r = 1.0f / sqrtf(ss * (1.0f / HD) + eps);
-    const uint16_t* w = hs < Hq ? q_norm : k_norm;
-    const float y0 = x0 * r * bf16_to_f32(w[lane]);
-    const float y1 = x1 * r * bf16_to_f32(w[lane + 64]);
-    const float z0 = y0 * cs - y1 * sn, z1 = y1 * cs + y0 * sn;
-    uint16_t* dst = hs < Hq ? Q + ((size_t)row * Hq + hs) * HD : Kc + (crow + (hs - Hq)) * HD;
-    dst[lane] = f32_to_bf16(z0);
-    dst[lane + 64] = f32_to_bf16(z1);
-  }
+  for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m);
+  const float r = 1.0f / sqrtf(ss * (1.0f / HD) + eps);
+  const uint16_t* w = hs < Hq ? q_norm : k_norm;
+  const float y0 = x0 * r * bf16_to_f32(w[lane]);
+  const float y1 = x1 * r * bf16_to_f32(w[lane + 64]);
+  const float z0 = y0 * cs - y1 * sn, z1 = y1 * cs + y0 * sn;
+  uint16_t* dst = hs < Hq ? Q + ((size_t)row * Hq + hs) * HD : Kc + (crow + (hs - Hq)) * HD;
+  dst[lane] = f32_to_bf16(z0);
+  dst[lane + 64] = f32_to_bf16(z1);
 }
 
-__global__ __launch_bounds__(256) void reduce_kernel(const float* __restrict__ part, int splits,
+// Adds the output projection's SP split partials in order and rounds to bf16: four
+// values per thread, all SP loads issued before the first addition.
+template <int SP>
+__global__ __launch_bounds__(256) void reduce_kernel(const float* __restrict__ part,
                                                      size_t total, uint16_t* __restrict__ Y) {
   const size_t e = ((size_t)blockIdx.x * 256 + threadIdx.x) * 4;
   if (e >= total) return;
-  float4 s = *(const float4*)(part + e);
-  for (int k = 1; k < splits; ++k) {
-    const float4 t = *(const float4*)(part + (size_t)k * total + e);
-    s.x += t.x;
-    s.y += t.y;
-    s.z += t.z;
-    s.w += t.w;
+  float4 t[SP];
+#pragma unroll
+  for (int k = 0; k < SP; ++k) t[k] = *(const float4*)(part + (size_t)k * total + e);
+  float4 s = t[0];
+#pragma unroll
+  for (int k = 1; k < SP; ++k) {
+    s.x += t[k].x;
+    s.y += t[k].y;
+    s.z += t[k].z;
+    s.w += t[k].w;
   }
   const uint2 o = make_uint2((uint32_t)f32_to_bf16(s.x) | ((uint32_t)f32_to_bf16(s.y) << 16),
                              (uint32_t)f32_to_bf16(s.z) | ((uint32_t)f32_to_bf16(s.w) << 16));
@@ -322,9 +339,20 @@ hipError_t launch_qkv_rope(const float* part, int splits, int batch, int budget,
                            hipStream_t s) {
   const int M = batch * budget;
   const dim3 grid((unsigned)M, (unsigned)((Hq + 2 * Hkv + 3) / 4));
-  qkv_rope_kernel<<<grid, 256, 0, s>>>(part, splits, M, budget, Hq, Hkv, (const uint16_t*)q_norm,
-                                    (const uint16_t*)k_norm, theta, eps, off, ctx, depth, n,
-                                    max_ctx, (uint16_t*)Q, (uint16_t*)Kc, (uint16_t*)Vc);
+#define TAPS_ROPE(SP)                                                                     \
+  qkv_rope_kernel<SP><<<grid, 256, 0, s>>>(part, M, budget, Hq, Hkv, (const uint16_t*)q_norm, \
+                                           (const uint16_t*)k_norm, theta, eps, off, ctx,     \
+                                           depth, n, max_ctx, (uint16_t*)Q, (uint16_t*)Kc,    \
+                                           (uint16_t*)Vc)
+  switch (splits) {   // the GEMM plan's split counts
+    case 1: TAPS_ROPE(1); break;
+    case 2: TAPS_ROPE(2); break;
+    case 4: TAPS_ROPE(4); break;
+    case 8: TAPS_ROPE(8); break;
+    case 16: TAPS_ROPE(16); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef TAPS_ROPE
   return hipGetLastError();
 }
 
@@ -332,7 +360,14 @@ hipError_t launch_reduce_bf16(const float* part, int splits, int M, int N, void*
                               hipStream_t s) {
   const size_t total = (size_t)M * N;     // a multiple of 4 (N is a multiple of 64)
   const unsigned blocks = (unsigned)((total / 4 + 255) / 256);
-  reduce_kernel<<<blocks, 256, 0, s>>>(part, splits, total, (uint16_t*)Y);
+  switch (splits) {   // the GEMM plan's split counts
+    case 1: reduce_kernel<1><<<blocks, 256, 0, s>>>(part, total, (uint16_t*)Y); break;
+    case 2: reduce_kernel<2><<<blocks, 256, 0, s>>>(part, total, (uint16_t*)Y); break;
+    case 4: reduce_kernel<4><<<blocks, 256, 0, s>>>(part, total, (uint16_t*)Y); break;
+    case 8: reduce_kernel<8><<<blocks, 256, 0, s>>>(part, total, (uint16_t*)Y); break;
+    case 16: reduce_kernel<16><<<blocks, 256, 0, s>>>(part, total, (uint16_t*)Y); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
