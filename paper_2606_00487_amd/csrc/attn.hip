@@ -947,21 +947,23 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
 #endif
 }
 
-// Split combine: grid (row blocks, batch); one thread per 4 head dims of one output row.
-template <int HD>
+// Split combine: grid (row blocks, batch); one thread per 8 head dims of one output row
+// (16-byte loads and stores).  CH = splits merged per group: the plan's split count for one
+// request (up to 16), 4 for the ragged list, whose requests mostly hold a few splits each.
+template <int HD, int CH>
 __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
     const uint16_t* __restrict__ wsO, const float2* __restrict__ wsML,
     const int32_t* __restrict__ ctxp, const int32_t* __restrict__ nnp, int N, int Hq, int Hkv,
     int max_ctx, int split_len, int splits, int mrows_pad, DivMagic dm,
     uint16_t* __restrict__ O, const int2* __restrict__ tab, int batch) {
-  constexpr int TPR = HD / 4;  // threads per output row, 4 values each
+  constexpr int TPR = HD / 8;  // threads per output row, 8 values each
   constexpr int RPB = kThreads / TPR;
   asm volatile("" ::"s"(wsO), "s"(wsML), "s"(ctxp), "s"(nnp), "s"(N), "s"(Hq), "s"(Hkv),
                "s"(max_ctx), "s"(split_len), "s"(splits), "s"(mrows_pad), "s"(dm.hk),
                "s"(dm.g), "s"(O), "s"(tab), "s"(batch));
   const int b = blockIdx.y;
   const int rr = blockIdx.x * RPB + threadIdx.x / TPR;   // (node, query head) of request b
-  const int d = (threadIdx.x % TPR) * 4;
+  const int d = (threadIdx.x % TPR) * 8;
   if (rr >= N * Hq) return;
   const int i = dm.div(rr, Hq, dm.hk), hq = rr - i * Hq;   // dm.hk holds the Hq multiplier
   const int G = Hq / Hkv, g = dm.div(hq, G, dm.g);
@@ -984,15 +986,14 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
   // CH splits go out before the request's sizes are known (their addresses do not depend on
   // them; splits past the request's keys are masked once the sizes have arrived), then
   // groups of up to CH splits are merged with a running maximum.
-  constexpr int CH = 16;
   float2 ml[CH];
-  uint2 ov[CH];
+  uint4 ov[CH];
   auto load_group = [&](int s0) __attribute__((always_inline)) {
 #pragma unroll
     for (int t = 0; t < CH; ++t) {
       const size_t r = (base + min(s0 + t, cap - 1)) * mrows_pad + qr;
       ml[t] = wsML[r];
-      ov[t] = *(const uint2*)(wsO + r * HD + d);
+      ov[t] = *(const uint4*)(wsO + r * HD + d);
     }
   };
   if (cap > 0) load_group(0);
@@ -1004,7 +1005,7 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
   const int R = ctx + n;
   const int nspl = min((R + split_len - 1) / split_len, cap);
   float M = -INFINITY, L = 0.f;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   for (int s0 = 0; s0 < nspl; s0 += CH) {
     if (s0 > 0) load_group(s0);
     // splits past the request's keys were not written by this call: their slots hold
@@ -1014,7 +1015,7 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
     for (int t = 0; t < CH; ++t)
       if (s0 + t >= nspl) {
         ml[t] = make_float2(-INFINITY, 0.f);
-        ov[t] = make_uint2(0u, 0u);
+        ov[t] = make_uint4(0u, 0u, 0u, 0u);
       }
     float Mc = M;
 #pragma unroll
@@ -1022,21 +1023,25 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
     if (Mc == -INFINITY) continue;
     const float a = M == -INFINITY ? 0.f : exp2f(M - Mc);
     L *= a;
-    acc.x *= a; acc.y *= a; acc.z *= a; acc.w *= a;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] *= a;
 #pragma unroll
     for (int t = 0; t < CH; ++t) {
       const float w = ml[t].x == -INFINITY ? 0.f : exp2f(ml[t].x - Mc) * ml[t].y;
       L += w;
-      acc.x += w * __uint_as_float(ov[t].x << 16);
-      acc.y += w * __uint_as_float(ov[t].x & 0xFFFF0000u);
-      acc.z += w * __uint_as_float(ov[t].y << 16);
-      acc.w += w * __uint_as_float(ov[t].y & 0xFFFF0000u);
+      const uint32_t wd[4] = {ov[t].x, ov[t].y, ov[t].z, ov[t].w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        acc[2 * k] += w * __uint_as_float(wd[k] << 16);
+        acc[2 * k + 1] += w * __uint_as_float(wd[k] & 0xFFFF0000u);
+      }
     }
     M = Mc;
   }
   const float inv = 1.f / L;
-  *(uint2*)(O + (((size_t)b * N + i) * Hq + hq) * HD + d) =
-      pack_bf16x4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
+  const uint2 lo = pack_bf16x4(acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+  const uint2 hi = pack_bf16x4(acc[4] * inv, acc[5] * inv, acc[6] * inv, acc[7] * inv);
+  *(uint4*)(O + (((size_t)b * N + i) * Hq + hq) * HD + d) = make_uint4(lo.x, lo.y, hi.x, hi.y);
 }
 
 // ---------------------------------------------------------------- fp32 VALU path
@@ -1246,19 +1251,26 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
   if (e != hipSuccess) return e;
   const int rows_req = budget * Hq;   // output rows of one request
   const DivMagic cm{0u, 0u, DivMagic::make(Hq), DivMagic::make(Hq / Hkv)};
+  // splits per group: the one-request plan's split count (rounded up to 4, 8 or 16), 4
+  // for the ragged list
+  const int ch = tab != nullptr || pl.splits <= 4 ? 4 : pl.splits <= 8 ? 8 : 16;
+  const int2* tb = head_dim == 128 ? tab : nullptr;
+#define TAPS_COMBINE(HDC, CHC)                                                                  \
+  attn_combine_kernel<HDC, CHC>                                                                 \
+      <<<dim3((unsigned)((rows_req + kThreads / (HDC / 8) - 1) / (kThreads / (HDC / 8))),       \
+              (unsigned)batch),                                                                 \
+         dim3(kThreads), 0, s>>>(wsO, wsML, ctx, n, budget, Hq, Hkv, max_ctx, pl.split_len,     \
+                                 pl.splits, mrows_pad, cm, (uint16_t*)O, tb, batch)
   if (head_dim == 128) {
-    const int rpb = kThreads / 32;
-    attn_combine_kernel<128><<<dim3((unsigned)((rows_req + rpb - 1) / rpb), (unsigned)batch),
-                               dim3(kThreads), 0, s>>>(wsO, wsML, ctx, n, budget, Hq, Hkv, max_ctx,
-                                                       pl.split_len, pl.splits, mrows_pad, cm,
-                                                       (uint16_t*)O, tab, batch);
+    if (ch == 4) TAPS_COMBINE(128, 4);
+    else if (ch == 8) TAPS_COMBINE(128, 8);
+    else TAPS_COMBINE(128, 16);
   } else {
-    const int rpb = kThreads / 16;
-    attn_combine_kernel<64><<<dim3((unsigned)((rows_req + rpb - 1) / rpb), (unsigned)batch),
-                              dim3(kThreads), 0, s>>>(wsO, wsML, ctx, n, budget, Hq, Hkv, max_ctx,
-                                                      pl.split_len, pl.splits, mrows_pad, cm,
-                                                      (uint16_t*)O, nullptr, batch);
+    if (ch == 4) TAPS_COMBINE(64, 4);
+    else if (ch == 8) TAPS_COMBINE(64, 8);
+    else TAPS_COMBINE(64, 16);
   }
+#undef TAPS_COMBINE
   return hipGetLastError();
 }
 
