@@ -197,13 +197,14 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
   }
 }
 
-// One wave per (tree node, head): blockIdx.x is the node (row = b * budget + i), and
-// wave w of workgroup blockIdx.y takes head 4 blockIdx.y + w of the Hq query, Hkv key and
-// Hkv value heads.  head_dim 128: lane l holds dims l and l + 64, the rotary pair.  SP =
-// the projection's K splits: every load of the wave (the request's sizes, the node's depth
-// and cache offset, and all SP partials) is issued before any of them is used, so the
-// kernel waits for memory once.
-template <int SP>
+// One wave per (tree node, HPW heads): blockIdx.x is the node (row = b * budget + i), and
+// wave w of workgroup blockIdx.y takes heads (4 blockIdx.y + w) HPW .. + HPW - 1 of the Hq
+// query, Hkv key and Hkv value heads.  head_dim 128: lane l holds dims l and l + 64, the
+// rotary pair; the wave's heads share the node's rotation, computed once.  SP = the
+// projection's K splits: every load of the wave (the request's sizes, the node's depth and
+// cache offset, and all SP partials of its heads) is issued before any of them is used, so
+// the kernel waits for memory once.
+template <int SP, int HPW>
 __global__ __launch_bounds__(256) void qkv_rope_kernel(
     const float* __restrict__ part, int M, int budget, int Hq, int Hkv,
     const uint16_t* __restrict__ q_norm, const uint16_t* __restrict__ k_norm, double theta,
@@ -213,51 +214,64 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(
   constexpr int HD = 128;
   const int row = blockIdx.x, b = row / budget, i = row - b * budget;
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  const int hs = blockIdx.y * 4 + wave;
-  if (hs >= Hq + 2 * Hkv) return;
-  const int N = (Hq + 2 * Hkv) * HD;
+  const int H = Hq + 2 * Hkv;
+  const int h0 = (blockIdx.y * 4 + wave) * HPW;
+  if (h0 >= H) return;
+  const int N = H * HD;
   const int n_raw = np_[b], ctx_raw = ctxp[b], d_raw = depthp[(size_t)b * budget + i];
   const int64_t kv0 = off[b];
-  float p0[SP], p1[SP];
+  float p0[HPW][SP], p1[HPW][SP];
 #pragma unroll
-  for (int s = 0; s < SP; ++s) {
-    const float* pr = part + ((size_t)s * M + row) * N + (size_t)hs * HD;
-    p0[s] = pr[lane];
-    p1[s] = pr[lane + 64];
+  for (int j = 0; j < HPW; ++j) {
+    const int hs = min(h0 + j, H - 1);
+#pragma unroll
+    for (int s = 0; s < SP; ++s) {
+      const float* pr = part + ((size_t)s * M + row) * N + (size_t)hs * HD;
+      p0[j][s] = pr[lane];
+      p1[j][s] = pr[lane + 64];
+    }
   }
   const int n = min(max(n_raw, 0), budget);
   if (i >= n) return;
   const int ctx = min(max(ctx_raw, 0), max_ctx);
   const int pos = ctx + max(d_raw, 0);
   const size_t crow = (size_t)(kv0 + ctx + i) * Hkv;   // first head of the node's cache row
-  float x0 = 0.f, x1 = 0.f;
-#pragma unroll
-  for (int s = 0; s < SP; ++s) {   // the splits in order
-    x0 += p0[s];
-    x1 += p1[s];
-  }
-  if (hs >= Hq + Hkv) {             // value head: stored as projected
-    const size_t o = (crow + (hs - Hq - Hkv)) * HD;
-    Vc[o + lane] = f32_to_bf16(x0);
-    Vc[o + lane + 64] = f32_to_bf16(x1);
-    return;
-  }
   // rotation of the pair (lane, lane + 64) at this position, from fp64 angles
-  const double ang = (double)pos * pow(theta, -2.0 * (double)lane / (double)HD);
-  double sd, cd;
-  sincos(ang, &sd, &cd);
-  const float sn = (float)sd, cs = (float)cd;
-  float ss = x0 * x0 + x1 * x1;
+  float sn = 0.f, cs = 1.f;
+  if (h0 < Hq + Hkv) {   // the wave holds a query or key head
+    const double ang = (double)pos * pow(theta, -2.0 * (double)lane / (double)HD);
+    double sd, cd;
+    sincos(ang, &sd, &cd);
+    sn = (float)sd;
+    cs = (float)cd;
+  }
 #pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m);
-  const float r = 1.0f / sqrtf(ss * (1.0f / HD) + eps);
-  const uint16_t* w = hs < Hq ? q_norm : k_norm;
-  const float y0 = x0 * r * bf16_to_f32(w[lane]);
-  const float y1 = x1 * r * bf16_to_f32(w[lane + 64]);
-  const float z0 = y0 * cs - y1 * sn, z1 = y1 * cs + y0 * sn;
-  uint16_t* dst = hs < Hq ? Q + ((size_t)row * Hq + hs) * HD : Kc + (crow + (hs - Hq)) * HD;
-  dst[lane] = f32_to_bf16(z0);
-  dst[lane + 64] = f32_to_bf16(z1);
+  for (int j = 0; j < HPW; ++j) {
+    const int hs = h0 + j;
+    float x0 = 0.f, x1 = 0.f;
+#pragma unroll
+    for (int s = 0; s < SP; ++s) {   // the splits in order
+      x0 += p0[j][s];
+      x1 += p1[j][s];
+    }
+    if (hs >= Hq + Hkv && hs < H) {   // value head: stored as projected
+      const size_t o = (crow + (hs - Hq - Hkv)) * HD;
+      Vc[o + lane] = f32_to_bf16(x0);
+      Vc[o + lane + 64] = f32_to_bf16(x1);
+    } else if (hs < Hq + Hkv) {        // query or key head: RMSNorm and rotation
+      float ss = x0 * x0 + x1 * x1;
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m);
+      const float r = 1.0f / sqrtf(ss * (1.0f / HD) + eps);
+      const uint16_t* w = hs < Hq ? q_norm : k_norm;
+      const float y0 = x0 * r * bf16_to_f32(w[lane]);
+      const float y1 = x1 * r * bf16_to_f32(w[lane + 64]);
+      const float z0 = y0 * cs - y1 * sn, z1 = y1 * cs + y0 * sn;
+      uint16_t* dst = hs < Hq ? Q + ((size_t)row * Hq + hs) * HD : Kc + (crow + (hs - Hq)) * HD;
+      dst[lane] = f32_to_bf16(z0);
+      dst[lane + 64] = f32_to_bf16(z1);
+    }
+  }
 }
 
 // Adds the output projection's SP split partials in order and rounds to bf16: four
@@ -337,21 +351,28 @@ hipError_t launch_qkv_rope(const float* part, int splits, int batch, int budget,
                            const int64_t* off, const int32_t* ctx, const int32_t* depth,
                            const int32_t* n, int max_ctx, void* Q, void* Kc, void* Vc,
                            hipStream_t s) {
-  const int M = batch * budget;
-  const dim3 grid((unsigned)M, (unsigned)((Hq + 2 * Hkv + 3) / 4));
-#define TAPS_ROPE(SP)                                                                     \
-  qkv_rope_kernel<SP><<<grid, 256, 0, s>>>(part, M, budget, Hq, Hkv, (const uint16_t*)q_norm, \
-                                           (const uint16_t*)k_norm, theta, eps, off, ctx,     \
-                                           depth, n, max_ctx, (uint16_t*)Q, (uint16_t*)Kc,    \
-                                           (uint16_t*)Vc)
+  const int M = batch * budget, H = Hq + 2 * Hkv;
+  // four heads per wave once there are many (node, head) pairs: the fp64 rotation is then
+  // computed once per four heads, and the grid still holds thousands of waves
+  const int hpw = (long long)M * H > 8192 ? 4 : 1;
+  const dim3 grid((unsigned)M, (unsigned)((H + 4 * hpw - 1) / (4 * hpw)));
+#define TAPS_ROPE(SP, HPW)                                                                    \
+  qkv_rope_kernel<SP, HPW><<<grid, 256, 0, s>>>(part, M, budget, Hq, Hkv,                     \
+                                                (const uint16_t*)q_norm, (const uint16_t*)k_norm, \
+                                                theta, eps, off, ctx, depth, n, max_ctx,        \
+                                                (uint16_t*)Q, (uint16_t*)Kc, (uint16_t*)Vc)
+#define TAPS_ROPE_SP(SP)                \
+  if (hpw == 4) TAPS_ROPE(SP, 4);       \
+  else TAPS_ROPE(SP, 1)
   switch (splits) {   // the GEMM plan's split counts
-    case 1: TAPS_ROPE(1); break;
-    case 2: TAPS_ROPE(2); break;
-    case 4: TAPS_ROPE(4); break;
-    case 8: TAPS_ROPE(8); break;
-    case 16: TAPS_ROPE(16); break;
+    case 1: TAPS_ROPE_SP(1); break;
+    case 2: TAPS_ROPE_SP(2); break;
+    case 4: TAPS_ROPE_SP(4); break;
+    case 8: TAPS_ROPE_SP(8); break;
+    case 16: TAPS_ROPE_SP(16); break;
     default: return hipErrorInvalidValue;
   }
+#undef TAPS_ROPE_SP
 #undef TAPS_ROPE
   return hipGetLastError();
 }

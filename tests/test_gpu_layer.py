@@ -140,6 +140,14 @@ def test_layer_many_rows_take_the_widest_gemm_tiles(taps):
          ctx=[30, 0, 65, 3, 100, 7, 12, 50], n=[128, 1, 77, 128, 5, 64, 100, 33])
 
 
+def test_layer_many_pairs_take_four_heads_per_wave(taps):
+    """M = 8 x 128 rows and 12 heads per node (8 query, 2 key, 2 value): the rotary pass
+    gives each wave four heads of a node (the last group of the node's three partly
+    filled: heads 8-11 of one workgroup of 16)."""
+    _run(taps, np.random.default_rng(7), B=8, N=128, H=128, Hq=8, Hkv=2,
+         ctx=[0, 41, 9, 130, 1, 64, 7, 20], n=[128, 128, 3, 90, 1, 60, 128, 17])
+
+
 def test_layer_qwen3_8b_shape(taps):
     """One Qwen3-8B-shaped layer (hidden 4096, 32/8 heads x 128) over 8192 context rows
     and a 64-node tree; Y on the root, the last node and six random nodes."""
