@@ -407,6 +407,34 @@ def test_attention_multi_split_other_head_sizes(taps, dtype, hd):
         U.attention_error(got[b, :n[b]], ref[b, :n[b]], dtype, f"split dtype={dtype} hd={hd} b={b}")
 
 
+@pytest.mark.parametrize("hd,ctx", [(128, 100), (128, 600), (128, 2000), (64, 700), (64, 1100)])
+def test_attention_one_request_split_groups(taps, hd, ctx):
+    """One request (the host's split plan): contexts whose plans take a few, six to eight,
+    and more than eight key splits, so the split combine merges them in groups of 4, 8 and
+    16; every (node, head) row against the oracle."""
+    rng = np.random.default_rng(60 + hd + ctx)
+    B, N, Hq, Hkv = 1, 64, 32, 8
+    ctxs = np.array([ctx], dtype=np.int32)
+    say(f"[attn-groups] hd={hd} ctx={ctx}")
+    off = kv_offsets(ctxs, N)
+    rows = int(off[-1] + ctxs[-1] + N)
+    from workloads import f32_to_bf16_bits, bf16_bits_to_f32
+    Q, K, V = (f32_to_bf16_bits(rng.standard_normal(sh).astype(np.float32))
+               for sh in ((B, N, Hq, hd), (rows, Hkv, hd), (rows, Hkv, hd)))
+    Qd, Kd, Vd = (bf16_bits_to_f32(a).astype(np.float64) for a in (Q, K, V))
+    parents = [np.array([-1] + [int(rng.integers(0, i)) for i in range(1, N)], dtype=np.int32)]
+    n = [N]
+    import paper_2606_00487_amd as taps_mod
+    att = taps_mod.TreeAttention(B, N, Hq, Hkv, hd, ctx, dtype=BF16, scale=hd ** -0.5)
+    att.ws.fill_(0xFF)            # NaN bits in every unwritten partial slot
+    O = att(U.to_dev(Q, True), U.to_dev(K, True), U.to_dev(V, True), torch.from_numpy(off).cuda(),
+            torch.from_numpy(ctxs).cuda(), torch.from_numpy(np.stack(parents)).cuda(),
+            torch.tensor(n, dtype=torch.int32).cuda())
+    torch.cuda.synchronize()
+    ref = oracle.tree_attention(Qd, Kd, Vd, off, ctxs, parents, n, hd ** -0.5)
+    U.attention_error(U.gpu_o_as_f64(O)[0], ref[0], BF16, f"groups hd={hd} ctx={ctx}")
+
+
 def test_attention_tree_rows_dominate_at_full_size(taps):
     """The Qwen3-8B round shape (context 8192, 64 nodes, 32/8 heads, head_dim 128, the
     bench's key splits) with a common direction added to every query and to the tree rows'
