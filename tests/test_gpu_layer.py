@@ -148,6 +148,23 @@ def test_layer_many_pairs_take_four_heads_per_wave(taps):
          ctx=[0, 41, 9, 130, 1, 64, 7, 20], n=[128, 128, 3, 90, 1, 60, 128, 17])
 
 
+@pytest.mark.parametrize("seed", range(10))
+def test_layer_fuzz_shapes(taps, seed):
+    """Seeded random shapes: 1-4 requests of 1-70 nodes, hidden 64-1024, 1-16 query heads
+    over 1-4 KV heads, ragged contexts up to 400 rows and node counts down to none; the
+    GEMM plans they reach vary in columns per workgroup (64, 96) and K splits (1-16)."""
+    rng = np.random.default_rng(1000 + seed)
+    B = int(rng.integers(1, 5))
+    N = int(rng.integers(1, 71))
+    H = 64 * int(rng.integers(1, 17))
+    Hkv = int(rng.choice([1, 2, 4]))
+    Hq = Hkv * int(rng.choice([1, 2, 4]))
+    ctx = [int(x) for x in rng.integers(0, 401, B)]
+    n = [int(x) for x in rng.integers(0, N + 1, B)]
+    n[int(rng.integers(0, B))] = N                  # one request with a full tree
+    _run(taps, rng, B=B, N=N, H=H, Hq=Hq, Hkv=Hkv, ctx=ctx, n=n)
+
+
 def test_layer_qwen3_8b_shape(taps):
     """One Qwen3-8B-shaped layer (hidden 4096, 32/8 heads x 128) over 8192 context rows
     and a 64-node tree; Y on the root, the last node and six random nodes."""
