@@ -564,6 +564,49 @@ def test_select_sequential_fallback_matches_oracle(taps, name):
     U.assert_tree_equal(gpu, [t], cfg)
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_attention_fuzz_batches(taps, seed):
+    """Seeded random batches for the ragged work list and the grouped split combine: 2-6
+    requests, contexts from empty to 6000 rows (max_ctx above every one of them), 1-100
+    nodes with random parents, 1-4 KV heads of 1-4 query heads each; sampled (node, head)
+    rows of every request against the oracle."""
+    from workloads import f32_to_bf16_bits, bf16_bits_to_f32
+    rng = np.random.default_rng(500 + seed)
+    B = int(rng.integers(2, 7))
+    N = int(rng.integers(1, 101))
+    Hkv = int(rng.choice([1, 2, 4]))
+    Hq = Hkv * int(rng.choice([1, 2, 4]))
+    hd = 128
+    ctx = rng.integers(0, 6001, B).astype(np.int32)
+    ctx[int(rng.integers(0, B))] = int(rng.integers(0, 3))      # a (nearly) empty context
+    n = [int(x) for x in rng.integers(0, N + 1, B)]
+    n[int(rng.integers(0, B))] = N
+    max_ctx = int(ctx.max()) + int(rng.integers(0, 500))
+    say(f"[attn-fuzz] seed={seed} B={B} N={N} Hq={Hq} Hkv={Hkv} ctx={ctx.tolist()} n={n} max_ctx={max_ctx}")
+    off = kv_offsets(ctx, N)
+    rows = int(off[-1] + ctx[-1] + N)
+    Q = f32_to_bf16_bits(rng.standard_normal((B, N, Hq, hd)).astype(np.float32))
+    K = f32_to_bf16_bits(rng.standard_normal((rows, Hkv, hd)).astype(np.float32))
+    V = f32_to_bf16_bits(rng.standard_normal((rows, Hkv, hd)).astype(np.float32))
+    parents = [np.array([-1] + [int(rng.integers(0, i)) for i in range(1, N)], dtype=np.int32)
+               for _ in range(B)]
+    att = taps.TreeAttention(B, N, Hq, Hkv, hd, max_ctx, dtype=BF16, scale=hd ** -0.5)
+    att.ws.fill_(0xFF)
+    O = att(U.to_dev(Q, True), U.to_dev(K, True), U.to_dev(V, True), torch.from_numpy(off).cuda(),
+            torch.from_numpy(ctx).cuda(), torch.from_numpy(np.stack(parents)).cuda(),
+            torch.tensor(n, dtype=torch.int32).cuda())
+    torch.cuda.synchronize()
+    picks = [(b, int(i), int(h)) for b in range(B) if n[b]
+             for i in sorted({0, n[b] - 1, *rng.integers(0, n[b], 6).tolist()})
+             for h in sorted({0, Hq - 1, int(rng.integers(0, Hq))})]
+    ref = oracle.tree_attention(*(bf16_bits_to_f32(a).astype(np.float64) for a in (Q, K, V)),
+                                off, ctx, parents, n, hd ** -0.5, samples=picks)
+    got = U.gpu_o_as_f64(O)
+    for b in range(B):
+        if n[b]:
+            U.attention_error(got[b, :n[b]], ref[b, :n[b]], BF16, f"fuzz b={b} ctx={ctx[b]}")
+
+
 def test_attention_ragged_batch(taps):
     """Several requests of very different lengths (the ragged work list: split lengths from
     the batch's actual keys, pairs numbered by prefix sums), including an empty request and
