@@ -18,6 +18,9 @@ round's state update (kv_commit of the accepted path) is not part of the step;
 ``stages_us.kv_commit`` and ``kv_commit`` report it from its own timed pass.  ``layer``
 reports one attention layer of the target over the tree (verify_layer, hidden = Hq x
 head_dim, seeded random bf16 weights), also timed on its own and not part of the step.
+``stages_us`` times the round's three calls with events between eager launches;
+``stages_graph_us`` times each call from HIP graphs of ten back-to-back calls per input
+set (the graph-launched cost of its kernels, next to the round's own graph time).
 """
 from __future__ import annotations
 
@@ -293,6 +296,10 @@ def main():
             for x in e:
                 x.record(stream)
         torch.cuda.synchronize()
+        # a head start for the host: while the GPU sleeps, the timed launches queue up, so
+        # that they run back to back as in the graphs (an idle GPU between launches would
+        # add its wake-up to every kernel's time)
+        torch.cuda._sleep(int(2e7))
         for r in range(reps):
             s = sets[r % nsets]
             e = ev[r]
@@ -305,6 +312,39 @@ def main():
             walk(s["tree"], s["tgt"])
             e[5].record(stream)
         torch.cuda.synchronize()
+
+        # ---------------- per-stage times from HIP graphs: for each stage one graph of GR
+        # back-to-back calls per input set, replayed over the rotating sets, so that each
+        # figure carries the graph-launched start-up of the round's own kernels
+        stage_graph = {}
+        if not args.eager:
+            GR = 10
+            stage_calls = {
+                "select": lambda s: sel(s["marg"], s["tree"]),
+                "attn_call": lambda s: att(s["Q"], s["K"], s["V"], s["off"], s["ctx"],
+                                           s["tree"].parent, s["tree"].n_nodes, out=s["O"]),
+                "walk": lambda s: walk(s["tree"], s["tgt"]),
+            }
+            for name, fn in stage_calls.items():
+                gs = []
+                for s in sets:
+                    g = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(g, stream=stream):
+                        for _ in range(GR):
+                            fn(s)
+                    gs.append(g)
+                for g in gs:                      # warm
+                    g.replay()
+                g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                g0.record(stream)
+                for _ in range(2):
+                    for g in gs:
+                        g.replay()
+                g1.record(stream)
+                torch.cuda.synchronize()
+                stage_graph[name] = round(g0.elapsed_time(g1) * 1e3 / (2 * len(gs) * GR), 2)
+                del gs
+            stage_graph["sum"] = round(sum(stage_graph.values()), 2)
 
         # ---------------- the round's state update (kv_commit), timed on its own from a HIP
         # graph of back-to-back calls per input set (eager events would include the host's
@@ -445,6 +485,7 @@ def main():
         "stages_us": {"select": round(t_sel, 2), "attn_main_kernel": round(t_attn, 2),
                       "attn_call": round(t_attn_call, 2), "walk": round(t_walk, 2),
                       "kv_commit": round(t_commit, 2)},
+        "stages_graph_us": stage_graph or None,
         "kv_commit": {"bytes_per_launch": int(commit_b),
                       "achieved_gbs": round(commit_b / (t_commit * 1e-6) / 1e9, 1),
                       "avg_launch_us": round(t_commit, 3)},
