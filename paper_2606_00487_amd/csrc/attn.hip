@@ -33,6 +33,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 256;
 constexpr int kWavesA = 4;
@@ -905,7 +906,10 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
 
   // ---- write this split's partial: O / sum in bf16 for this group's 64 head dims of the
   // wave's 32 rows, max and sum.  The tile goes through LDS (this wave's V slot, free
-  // now) so that each store instruction writes whole 128-byte row segments.
+  // now) so that each store instruction writes whole 128-byte row segments.  The stores
+  // are non-temporal: only the combine, a later launch, reads the partials, and streaming
+  // them out of the L2 leaves less to write back when the kernel ends (measured: the
+  // kernel took 0.5 us less at the Qwen3-8B shape).
   constexpr int TROW = 144;            // bytes per staged row (128 + 16: fewer bank conflicts)
   unsigned char* stage;
   switch (wave) {
@@ -939,11 +943,16 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int r = 8 * i + (lane >> 3), c = (lane & 7) * 16;   // row in the tile, byte in the half
-    const uint4 v = *(const uint4*)(stage + r * TROW + c);
-    *(uint4*)((unsigned char*)(wsO + (obase + qbase + r) * HD) + kg * 128 + c) = v;
+    const i32x4 v = *(const i32x4*)(stage + r * TROW + c);
+    __builtin_nontemporal_store(v, (i32x4*)((unsigned char*)(wsO + (obase + qbase + r) * HD) + kg * 128 + c));
   }
   const int qr = qbase + l32;
-  if (kg == 0 && hl == 0) wsML[obase + qr] = make_float2(M, Ls);
+  if (kg == 0 && hl == 0) {
+    f32x2 ml2;
+    ml2.x = M;
+    ml2.y = Ls;
+    __builtin_nontemporal_store(ml2, (f32x2*)(wsML + obase + qr));
+  }
 #endif
 }
 
