@@ -8,6 +8,7 @@
  *   tree_verify_attn  tree-masked verification attention: every selected node attends
  *                     to the cached context and to its own ancestors (Sec. 4.1 Stage 3,
  *                     Sec. 4.3: verification needs a connected subtree at the root).
+ *                     tree_verify_attn_paged: the same over a paged KV cache.
  *   accept_walk       greedy (temperature 0) acceptance of the longest matching root
  *                     path (Sec. 1: one prefix path is committed per round; Limitations).
  *   kv_commit         the round's state update: the accepted path's tree K/V rows move
@@ -227,6 +228,38 @@ taps_status tree_verify_attn_timed(const void *Q_tree, const void *K_cache, cons
                                    int32_t head_dim, int32_t max_ctx, int32_t dtype,
                                    float scale, void *O, void *ws, size_t ws_bytes,
                                    hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_end);
+
+/* Bytes of scratch tree_verify_attn_paged needs for these sizes and page size (0 when
+ * they are not supported). */
+size_t tree_verify_attn_paged_workspace_bytes(int32_t batch, int32_t budget, int32_t Hq,
+                                              int32_t Hkv, int32_t head_dim, int32_t max_ctx,
+                                              int32_t page_rows);
+
+/* tree_verify_attn over a paged KV cache, for batched serving (the Limitations leave the
+ * cache layout to the serving system; pages let requests grow without moving rows).  Same
+ * result as tree_verify_attn with request b's logical cache row r (its context rows
+ * 0 .. ctx-1, then node i at row ctx + i) stored at
+ *   K_pages[block_table[b][r / page_rows]][r % page_rows] (and V_pages alike).
+ *   K_pages,
+ *   V_pages      [num_pages][page_rows][Hkv][head_dim] bf16 pools, 16-byte aligned
+ *   num_pages    pages in each pool (>= 1)
+ *   page_rows    rows per page: a power of two from 32 to 4096
+ *   block_table  [batch][max_pages] int32 page ids, row b covering request b's rows in
+ *                order; max_pages * page_rows must be at least max_ctx + budget.  Entries
+ *                the request's rows do not reach are not read for keys; ids outside
+ *                [0, num_pages) are clamped into it (never a read outside the pools; the
+ *                result is then meaningless)
+ *   the other arguments as for tree_verify_attn (no kv_offset); head_dim 128 and TAPS_BF16
+ *   only (other sizes and types: TAPS_ERR_UNSUPPORTED)
+ *   ws           tree_verify_attn_paged_workspace_bytes(...) bytes, 16-byte aligned */
+taps_status tree_verify_attn_paged(const void *Q_tree, const void *K_pages, const void *V_pages,
+                                   int32_t num_pages, int32_t page_rows,
+                                   const int32_t *block_table, int32_t max_pages,
+                                   const int32_t *ctx_len, const int32_t *tree_parent,
+                                   const int32_t *n_nodes, int32_t batch, int32_t budget,
+                                   int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t max_ctx,
+                                   int32_t dtype, float scale, void *O, void *ws,
+                                   size_t ws_bytes, hipStream_t stream);
 
 /* Greedy acceptance walk (temperature 0).
  *   tree           [host] struct; parent, token and n_nodes are read

@@ -25,6 +25,6 @@ from .select import (  # noqa: F401
     topk_row, edge_factors, denominators, select_request, select_batch,
     select_literal_alg1, brute_force_best_set, Tree,
 )
-from .attention import ancestor_sets, tree_attention  # noqa: F401
+from .attention import ancestor_sets, tree_attention, tree_attention_paged  # noqa: F401
 from .walk import accept_walk  # noqa: F401
 from .commit import committed_path, kv_commit  # noqa: F401

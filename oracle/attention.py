@@ -70,3 +70,34 @@ def tree_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, kv_offset: np.nd
                 g = h // G
                 O[b, i, h] = attend_one(Q[b, i, h], Kr[:, g, :], Vr[:, g, :], scale)
     return O
+
+
+def tree_attention_paged(Q: np.ndarray, K_pages: np.ndarray, V_pages: np.ndarray,
+                         block_table: np.ndarray, page_rows: int, ctx_len: np.ndarray,
+                         parents: list[np.ndarray], n_nodes: list[int], scale: float,
+                         samples=None) -> np.ndarray:
+    """tree_attention over a paged cache.
+
+    Reading (the cache layout is the serving system's; the paper's Limitations name batched
+    serving): request b's logical cache row r -- its context rows 0 .. ctx-1, then tree
+    node i at row ctx + i, as in the contiguous layout -- is stored at
+    K_pages[block_table[b][r // page_rows], r % page_rows] (V_pages alike).  The rows are
+    gathered into a contiguous cache, then the plain definition above applies.
+
+    K_pages/V_pages: [pages][page_rows][Hkv][hd] float64; block_table: [B][max_pages].
+    """
+    B, N = Q.shape[0], Q.shape[1]
+    Ks, Vs, offs = [], [], []
+    base = 0
+    for b in range(B):
+        rows = np.arange(int(ctx_len[b]) + N)
+        page = np.asarray(block_table[b])[rows // page_rows]
+        slot = rows % page_rows
+        Ks.append(K_pages[page, slot])
+        Vs.append(V_pages[page, slot])
+        offs.append(base)
+        base += len(rows)
+    K = np.concatenate(Ks) if Ks else np.zeros((0,) + K_pages.shape[2:])
+    V = np.concatenate(Vs) if Vs else np.zeros((0,) + V_pages.shape[2:])
+    return tree_attention(Q, K, V, np.asarray(offs, dtype=np.int64), ctx_len, parents, n_nodes,
+                          scale, samples)

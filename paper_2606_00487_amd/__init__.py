@@ -185,6 +185,47 @@ class TreeAttention:
         return O
 
 
+class PagedTreeAttention:
+    """tree_verify_attn_paged: tree_verify_attn over a paged KV cache (bf16, head_dim 128)."""
+
+    def __init__(self, batch, budget, Hq, Hkv, max_ctx, page_rows, scale=None, device="cuda"):
+        self.lib = load()
+        hd = 128
+        self.shape = (batch, budget, Hq, Hkv, hd, max_ctx)
+        self.page_rows = int(page_rows)
+        self.scale = float(scale if scale is not None else hd ** -0.5)
+        self.ws_bytes = self.lib.tree_verify_attn_paged_workspace_bytes(
+            batch, budget, Hq, Hkv, hd, max_ctx, self.page_rows)
+        self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device=device)
+
+    def __call__(self, Q, K_pages, V_pages, block_table, ctx_len, parent, n_nodes, out=None):
+        """K_pages, V_pages: [num_pages, page_rows, Hkv, 128] bf16; block_table: [batch,
+        max_pages] int32 page ids (request b's logical row r at page block_table[b, r //
+        page_rows], slot r % page_rows)."""
+        batch, budget, Hq, Hkv, hd, max_ctx = self.shape
+        _need(Q, "Q_tree", torch.bfloat16, (batch, budget, Hq, hd))
+        _need(K_pages, "K_pages", torch.bfloat16)
+        if K_pages.dim() != 4 or K_pages.shape[1:] != (self.page_rows, Hkv, hd):
+            raise ValueError(f"K_pages: expected [pages, {self.page_rows}, {Hkv}, {hd}], "
+                             f"got {tuple(K_pages.shape)}")
+        _need(V_pages, "V_pages", torch.bfloat16, tuple(K_pages.shape))
+        _need(block_table, "block_table", torch.int32)
+        if block_table.dim() != 2 or block_table.shape[0] != batch:
+            raise ValueError(f"block_table: expected [{batch}, max_pages], "
+                             f"got {tuple(block_table.shape)}")
+        _need(ctx_len, "ctx_len", torch.int32, (batch,))
+        _need(parent, "tree_parent", torch.int32, (batch, budget))
+        _need(n_nodes, "n_nodes", torch.int32, (batch,))
+        O = out if out is not None else torch.empty_like(Q)
+        _need(O, "O", torch.bfloat16, (batch, budget, Hq, hd))
+        _lib.check(self.lib, "tree_verify_attn_paged", self.lib.tree_verify_attn_paged(
+            _ptr(Q), _ptr(K_pages), _ptr(V_pages), K_pages.shape[0], self.page_rows,
+            _ptr(block_table), block_table.shape[1], _ptr(ctx_len), _ptr(parent), _ptr(n_nodes),
+            batch, budget, Hq, Hkv, hd, max_ctx, BF16, self.scale, _ptr(O), _ptr(self.ws),
+            self.ws_bytes, _stream()))
+        return O
+
+
 class AcceptWalk:
     """accept_walk: greedy acceptance of the longest matching root path."""
 

@@ -216,6 +216,67 @@ taps_status tree_verify_attn(const void* Q_tree, const void* K_cache, const void
                                 O, ws, ws_bytes, stream, nullptr, nullptr);
 }
 
+// log2 of a page size that is a power of two in [32, 4096], else -1
+static int page_shift_of(int32_t page_rows) {
+  if (page_rows < 32 || page_rows > 4096 || (page_rows & (page_rows - 1)) != 0) return -1;
+  return __builtin_ctz((unsigned)page_rows);
+}
+
+static taps_status paged_check(int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv,
+                               int32_t head_dim, int32_t max_ctx, int32_t dtype, float scale,
+                               int32_t page_rows) {
+  const taps_status st = attn_check(batch, budget, Hq, Hkv, head_dim, max_ctx, dtype, scale);
+  if (st != TAPS_OK) return st;
+  if (page_shift_of(page_rows) < 0) return TAPS_ERR_INVALID_ARG;
+  if (dtype != TAPS_BF16 || head_dim != 128) return TAPS_ERR_UNSUPPORTED;
+  return TAPS_OK;
+}
+
+size_t tree_verify_attn_paged_workspace_bytes(int32_t batch, int32_t budget, int32_t Hq,
+                                              int32_t Hkv, int32_t head_dim, int32_t max_ctx,
+                                              int32_t page_rows) {
+  if (paged_check(batch, budget, Hq, Hkv, head_dim, max_ctx, TAPS_BF16, 1.0f, page_rows) !=
+          TAPS_OK ||
+      batch == 0)
+    return 0;
+  const AttnPlan pl = plan_attn(batch, budget, Hq, Hkv, head_dim, max_ctx,
+                                paged_max_split(page_shift_of(page_rows)));
+  return attn_ws_bytes(pl, batch, budget, Hq, Hkv, head_dim);
+}
+
+taps_status tree_verify_attn_paged(const void* Q_tree, const void* K_pages, const void* V_pages,
+                                   int32_t num_pages, int32_t page_rows,
+                                   const int32_t* block_table, int32_t max_pages,
+                                   const int32_t* ctx_len, const int32_t* tree_parent,
+                                   const int32_t* n_nodes, int32_t batch, int32_t budget,
+                                   int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t max_ctx,
+                                   int32_t dtype, float scale, void* O, void* ws,
+                                   size_t ws_bytes, hipStream_t stream) {
+  const taps_status st =
+      paged_check(batch, budget, Hq, Hkv, head_dim, max_ctx, dtype, scale, page_rows);
+  if (st != TAPS_OK) return st;
+  if (num_pages < 1 || max_pages < 1) return TAPS_ERR_INVALID_ARG;
+  // every logical row a request may own (its context and its nodes) has a table entry
+  if ((int64_t)max_pages * page_rows < (int64_t)max_ctx + budget) return TAPS_ERR_INVALID_ARG;
+  if (batch == 0) return TAPS_OK;
+  if (!Q_tree || !K_pages || !V_pages || !block_table || !ctx_len || !tree_parent || !n_nodes ||
+      !O)
+    return TAPS_ERR_INVALID_ARG;
+  const uintptr_t align_or =
+      (uintptr_t)Q_tree | (uintptr_t)K_pages | (uintptr_t)V_pages | (uintptr_t)O;
+  if ((align_or & 15) != 0 || ((uintptr_t)block_table & 3) != 0) return TAPS_ERR_INVALID_ARG;
+  const size_t need = tree_verify_attn_paged_workspace_bytes(batch, budget, Hq, Hkv, head_dim,
+                                                             max_ctx, page_rows);
+  if (!ws || ws_bytes < need || ((uintptr_t)ws & 15) != 0) return TAPS_ERR_WORKSPACE;
+  const int shift = page_shift_of(page_rows);
+  const AttnPlan pl = plan_attn(batch, budget, Hq, Hkv, head_dim, max_ctx, paged_max_split(shift));
+  return launch_attn_bf16_paged(Q_tree, K_pages, V_pages, block_table, max_pages, num_pages,
+                                shift, ctx_len, tree_parent, n_nodes, batch, budget, Hq, Hkv,
+                                max_ctx, scale, pl, O, ws, stream) == hipSuccess
+             ? TAPS_OK
+             : TAPS_ERR_HIP;
+}
+
 taps_status accept_walk(const taps_tree* tree, int32_t batch, int32_t budget, int32_t block,
                         const int32_t* target_tokens, int32_t* path, int32_t* path_len,
                         int32_t* bonus, hipStream_t stream) {

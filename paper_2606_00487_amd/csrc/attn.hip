@@ -453,6 +453,17 @@ struct DivMagic {
   }
 };
 
+// Paged KV cache: block table [batch][max_pages] of page ids into pools of num_pages pages
+// of 2^page_shift rows (32 .. 4096, so a 32-key stage never straddles two pages)
+struct PagedKV {
+  const int32_t* btab;
+  int max_pages, num_pages, page_shift;
+};
+// page ids of one split held in LDS (they share the (max, sum) exchange buffer, which is
+// used only after the key loop); split lengths are capped so that a split spans at most
+// this many pages
+constexpr int kPageSlots = 1024;
+
 // The request's context length, node count and KV offset in one scalar-memory round
 // trip (issued together, then one wait)
 __device__ inline void load_request_scalars(const int32_t* c, const int32_t* nn,
@@ -464,6 +475,25 @@ __device__ inline void load_request_scalars(const int32_t* c, const int32_t* nn,
       "s_waitcnt lgkmcnt(0)"
       : "=&s"(cv), "=&s"(nv), "=&s"(ov)
       : "s"(c), "s"(nn), "s"(o)
+      : "memory");
+}
+
+// the request's context length and node count plus four ints of its block-table row (the
+// pages of the split's first four stages) in one scalar-memory round trip
+__device__ inline void load_request_pages(const int32_t* c, const int32_t* nn,
+                                          const int32_t* p0, const int32_t* p1,
+                                          const int32_t* p2, const int32_t* p3, int& cv,
+                                          int& nv, int& v0, int& v1, int& v2, int& v3) {
+  asm volatile(
+      "s_load_dword %0, %6, 0x0\n\t"
+      "s_load_dword %1, %7, 0x0\n\t"
+      "s_load_dword %2, %8, 0x0\n\t"
+      "s_load_dword %3, %9, 0x0\n\t"
+      "s_load_dword %4, %10, 0x0\n\t"
+      "s_load_dword %5, %11, 0x0\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&s"(cv), "=&s"(nv), "=&s"(v0), "=&s"(v1), "=&s"(v2), "=&s"(v3)
+      : "s"(c), "s"(nn), "s"(p0), "s"(p1), "s"(p2), "s"(p3)
       : "memory");
 }
 
@@ -570,6 +600,10 @@ struct GroupTag {
   static constexpr int value = KG;
 };
 
+// PAGED: K and V are page pools [num_pages][page_rows][Hkv][HD] and request b's logical
+// row r sits at page btab[b][r >> page_shift], slot r & (page_rows - 1) (offp unused);
+// otherwise Kc and Vc are the contiguous cache and request b starts at row offp[b].
+template <bool PAGED>
 __global__ __launch_bounds__(512) void attn_bf16_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc,
     const uint16_t* __restrict__ Vc, const int64_t* __restrict__ offp,
@@ -577,7 +611,7 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     const int32_t* __restrict__ nnp, int N, int Hq, int Hkv, int max_ctx, float scale_log2,
     int split_len, int splits, int mtiles, int pairs, int mrows_pad, uint16_t* __restrict__ wsO,
     float2* __restrict__ wsML, DivMagic dm, int batch, int target_pairs, int lcap,
-    int2* __restrict__ tab) {
+    int2* __restrict__ tab, PagedKV pk) {
   // the body uses the buffer-resource type, which exists only in the device pass; the
   // host pass needs no more than the signature to emit the launch stub
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -607,6 +641,8 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
                "s"(N), "s"(Hq), "s"(Hkv), "s"(max_ctx), "s"(scale_log2), "s"(split_len),
                "s"(splits), "s"(mtiles), "s"(pairs), "s"(mrows_pad), "s"(wsO), "s"(wsML),
                "s"(dm.mt), "s"(dm.sp), "s"(dm.hk), "s"(dm.g));
+  if constexpr (PAGED)
+    asm volatile("" ::"s"(pk.btab), "s"(pk.max_pages), "s"(pk.num_pages), "s"(pk.page_shift));
   // ---- which (request, KV head, split, row tile) this workgroup owns.  The row tiles of a
   // pair are 8 block ids apart (one XCD, which shares the pair's K/V in its L2).  One
   // request (tab == nullptr): pair = (KV head) * splits + split, fixed by the host; several:
@@ -662,6 +698,18 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
       load_lds4(buffer_rsrc(parentp + (size_t)b * N, (uint32_t)N * 4),
                 (unsigned char*)s_par + 256 * wave_u, (uint32_t)(64 * wave_u + lane) * 4);
   }
+  // paged: the block-table entries of this split's pages (entries past the row read 0)
+  int* const s_pg = (int*)s_ml;
+  static_assert(sizeof(s_ml) >= kPageSlots * sizeof(int), "page ids fit the exchange buffer");
+  int pi0 = 0;
+  if constexpr (PAGED) {
+    pi0 = (split * split_len) >> pk.page_shift;
+    const i32x4 prs = buffer_rsrc(pk.btab + (size_t)b * pk.max_pages, (uint32_t)pk.max_pages * 4);
+#pragma unroll
+    for (int j = 0; j < kPageSlots / 512; ++j)
+      load_lds4(prs, (unsigned char*)s_pg + 256 * (wave_u + 8 * j),
+                (uint32_t)(pi0 + 64 * (wave_u + 8 * j) + lane) * 4);
+  }
   int qnode;
   {
     const int qr = min(row0 + rg * 32 + l32, N * G - 1);
@@ -671,8 +719,22 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
   const int node0 = dm.div(row0, G, dm.g);
 
   int ctx_raw, n_raw;
-  int64_t kv0;
-  load_request_scalars(ctxp + b, nnp + b, offp + b, ctx_raw, n_raw, kv0);
+  int64_t kv0 = 0;
+  int fpg[4] = {0, 0, 0, 0};   // paged: the pages of the split's first four stages
+  if constexpr (PAGED) {
+    // the entries' addresses are uniform; readfirstlane puts them in scalar registers
+    auto entry = [&](int j) {
+      const uint64_t a = (uint64_t)(pk.btab + (size_t)b * pk.max_pages +
+                                    min(pi0 + j, pk.max_pages - 1));
+      return (const int32_t*)(((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32))
+                               << 32) |
+                              (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a));
+    };
+    load_request_pages(ctxp + b, nnp + b, entry(0), entry(1), entry(2), entry(3), ctx_raw,
+                       n_raw, fpg[0], fpg[1], fpg[2], fpg[3]);
+  } else {
+    load_request_scalars(ctxp + b, nnp + b, offp + b, ctx_raw, n_raw, kv0);
+  }
   const int ctx = min(max(ctx_raw, 0), max_ctx);
   const int n = min(max(n_raw, 0), N);
   const int R = ctx + n;
@@ -688,9 +750,18 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
   const int steps = (nst + 1) / 2;                    // each step: one stage per group
   // buffer resources over this split's K and V rows of head g: rows past the split's end
   // read as zeros without touching memory (the host keeps the range below 2^31 bytes)
-  const size_t seg = ((size_t)kv0 + k_begin) * row_stride + (size_t)g * HD;
-  const i32x4 krs = buffer_rsrc(Kc + seg, (uint32_t)(k_end - k_begin) * rsb);
-  const i32x4 vrs = buffer_rsrc(Vc + seg, (uint32_t)(k_end - k_begin) * rsb);
+  // contiguous: one resource per operand over the split's rows; paged: the pool's head-g
+  // column, with a resource per stage (issue below)
+  const auto krs = [&] {
+    if constexpr (PAGED) return Kc + (size_t)g * HD;
+    else return buffer_rsrc(Kc + ((size_t)kv0 + k_begin) * row_stride + (size_t)g * HD,
+                            (uint32_t)(k_end - k_begin) * rsb);
+  }();
+  const auto vrs = [&] {
+    if constexpr (PAGED) return Vc + (size_t)g * HD;
+    else return buffer_rsrc(Vc + ((size_t)kv0 + k_begin) * row_stride + (size_t)g * HD,
+                            (uint32_t)(k_end - k_begin) * rsb);
+  }();
 
   // ---- direct loads: wave w fills block w (rows 4w .. 4w + 3) of every slot
   uint32_t ld_off;
@@ -700,9 +771,25 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     const int pc = (rb - kr * ROWB) / 16;
     ld_off = (uint32_t)kr * rsb + (uint32_t)((pc ^ kswz(kr)) * 16);
   }
-  // the stage's offset goes into the per-lane offset, which the buffer range check covers
-  auto issue = [&](const i32x4& rs, unsigned char* buf, int s) __attribute__((always_inline)) {
-    load_lds16(rs, buf + wave_u * BLK, ld_off + (uint32_t)(s * KT) * rsb);
+  // contiguous: the stage's offset goes into the per-lane offset, which the buffer range
+  // check covers.  Paged: a resource over the stage's rows in its page, cut at the split's
+  // end (rows past it, and whole stages past it, read as zeros without touching memory);
+  // page ids outside the pool are clamped into it, so no id reads outside the pool.
+  auto issue = [&](const auto& src, unsigned char* buf, int s) __attribute__((always_inline)) {
+    if constexpr (!PAGED) {
+      load_lds16(src, buf + wave_u * BLK, ld_off + (uint32_t)(s * KT) * rsb);
+    } else {
+      const int r0 = k_begin + s * KT;               // logical row of the stage's first key
+      const int rows = min(max(k_end - r0, 0), KT);
+      const int j = (r0 >> pk.page_shift) - pi0;    // the page's entry in this split
+      int pg = 0;
+      if (s < 4) pg = fpg[min(j, 3)];
+      else if (rows > 0) pg = s_pg[min(j, kPageSlots - 1)];
+      pg = min(max(pg, 0), pk.num_pages - 1);
+      const size_t prow = ((size_t)pg << pk.page_shift) + (size_t)(r0 & ((1 << pk.page_shift) - 1));
+      load_lds16(buffer_rsrc(src + prow * row_stride, (uint32_t)rows * rsb), buf + wave_u * BLK,
+                 ld_off);
+    }
   };
 
   const bool tree_split = k_end > ctx;
@@ -1142,7 +1229,8 @@ __global__ __launch_bounds__(kThreads) void attn_f32_kernel(
 
 }  // namespace
 
-AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max_ctx) {
+AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max_ctx,
+                   int max_len) {
   AttnPlan p;
   const int G = Hq / Hkv;
   const int mrows = budget * G;
@@ -1155,6 +1243,7 @@ AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max
   // the buffer ranges of a split, look-ahead included, stay below 2^31 bytes
   const long long rsb0 = (long long)Hkv * head_dim * 2;
   p.lcap = (int)((((1ll << 31) - 1) / rsb0 - 5 * kKT) / kKT * kKT);
+  if (max_len > 0 && max_len < p.lcap) p.lcap = max_len / kKT * kKT;
 
   // Split the keys so that the workgroups (one per CU: the K/V rings fill its LDS) finish
   // soonest: estimated time = rounds of 256 workgroups x (32-key stages per split + ~8
@@ -1218,11 +1307,16 @@ size_t attn_ws_bytes(const AttnPlan& pl, int batch, int /*budget*/, int /*Hq*/, 
          (pl.ragged ? (size_t)(batch + 1) * sizeof(int2) : 0) + 256;
 }
 
-hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const int64_t* off,
-                            const int32_t* ctx, const int32_t* parent, const int32_t* n,
-                            int batch, int budget, int Hq, int Hkv, int head_dim, int max_ctx,
-                            float scale, const AttnPlan& pl, void* O, void* ws, hipStream_t s,
-                            hipEvent_t ev_begin, hipEvent_t ev_end) {
+// The bf16 attention and its split combine; PAGED takes K and V from page pools through
+// the block table of pk (head_dim 128 only), else from the contiguous cache at off[b]
+template <bool PAGED>
+static hipError_t launch_attn_bf16_impl(const void* Q, const void* K, const void* V,
+                                        const int64_t* off, const PagedKV& pk,
+                                        const int32_t* ctx, const int32_t* parent,
+                                        const int32_t* n, int batch, int budget, int Hq, int Hkv,
+                                        int head_dim, int max_ctx, float scale,
+                                        const AttnPlan& pl, void* O, void* ws, hipStream_t s,
+                                        hipEvent_t ev_begin, hipEvent_t ev_end) {
   if (batch <= 0) return hipSuccess;
   const int mrows_pad = pl.mtiles * pl.mtile;
   const size_t rows = attn_rows(pl, batch, Hkv);
@@ -1240,16 +1334,17 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
     const DivMagic dm{DivMagic::make(pl.mtiles), DivMagic::make(pl.splits), DivMagic::make(Hkv),
                       DivMagic::make(Hq / Hkv)};
     if (ev_begin || ev_end)
-      hipExtLaunchKernelGGL(attn_bf16_kernel, grid, block8, 0, s, ev_begin, ev_end, 0, q, k, v,
-                            off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2, pl.split_len,
-                            pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML, dm, batch,
-                            pl.target_pairs, pl.lcap, tab);
+      hipExtLaunchKernelGGL(attn_bf16_kernel<PAGED>, grid, block8, 0, s, ev_begin, ev_end, 0, q,
+                            k, v, off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2,
+                            pl.split_len, pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML, dm,
+                            batch, pl.target_pairs, pl.lcap, tab, pk);
     else
-      attn_bf16_kernel<<<grid, block8, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv,
-                                               max_ctx, sl2, pl.split_len, pl.splits,
-                                               pl.mtiles, pairs, mrows_pad, wsO, wsML, dm, batch,
-                                               pl.target_pairs, pl.lcap, tab);
-  } else {
+      attn_bf16_kernel<PAGED><<<grid, block8, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq,
+                                                      Hkv, max_ctx, sl2, pl.split_len,
+                                                      pl.splits, pl.mtiles, pairs, mrows_pad,
+                                                      wsO, wsML, dm, batch, pl.target_pairs,
+                                                      pl.lcap, tab, pk);
+  } else if constexpr (!PAGED) {
     if (ev_begin || ev_end)
       hipExtLaunchKernelGGL(attn_bf16_w4_kernel<64>, grid, block, 0, s, ev_begin, ev_end, 0, q,
                             k, v, off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2,
@@ -1288,6 +1383,30 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
 #undef TAPS_COMBINE
   return hipGetLastError();
 }
+
+hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const int64_t* off,
+                            const int32_t* ctx, const int32_t* parent, const int32_t* n,
+                            int batch, int budget, int Hq, int Hkv, int head_dim, int max_ctx,
+                            float scale, const AttnPlan& pl, void* O, void* ws, hipStream_t s,
+                            hipEvent_t ev_begin, hipEvent_t ev_end) {
+  return launch_attn_bf16_impl<false>(Q, K, V, off, PagedKV{nullptr, 0, 1, 5}, ctx, parent, n,
+                                      batch, budget, Hq, Hkv, head_dim, max_ctx, scale, pl, O,
+                                      ws, s, ev_begin, ev_end);
+}
+
+hipError_t launch_attn_bf16_paged(const void* Q, const void* K_pages, const void* V_pages,
+                                  const int32_t* block_table, int max_pages, int num_pages,
+                                  int page_shift, const int32_t* ctx, const int32_t* parent,
+                                  const int32_t* n, int batch, int budget, int Hq, int Hkv,
+                                  int max_ctx, float scale, const AttnPlan& pl, void* O,
+                                  void* ws, hipStream_t s) {
+  return launch_attn_bf16_impl<true>(Q, K_pages, V_pages, nullptr,
+                                     PagedKV{block_table, max_pages, num_pages, page_shift}, ctx,
+                                     parent, n, batch, budget, Hq, Hkv, 128, max_ctx, scale, pl,
+                                     O, ws, s, nullptr, nullptr);
+}
+
+int paged_max_split(int page_shift) { return (kPageSlots - 1) << page_shift; }
 
 hipError_t launch_attn_f32(const float* Q, const float* K, const float* V, const int64_t* off,
                            const int32_t* ctx, const int32_t* parent, const int32_t* n,

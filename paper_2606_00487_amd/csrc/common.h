@@ -69,7 +69,10 @@ struct AttnPlan {
   int pairs_max;
   int lcap;
 };
-AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max_ctx);
+// max_len > 0 caps the split length (a multiple of 32): paged calls, whose splits may span
+// at most a fixed number of pages
+AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max_ctx,
+                   int max_len = 0);
 size_t attn_ws_bytes(const AttnPlan& pl, int batch, int budget, int Hq, int Hkv, int head_dim);
 
 hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const int64_t* off,
@@ -77,6 +80,17 @@ hipError_t launch_attn_bf16(const void* Q, const void* K, const void* V, const i
                             int batch, int budget, int Hq, int Hkv, int head_dim, int max_ctx,
                             float scale, const AttnPlan& pl, void* O, void* ws, hipStream_t s,
                             hipEvent_t ev_begin = nullptr, hipEvent_t ev_end = nullptr);
+
+// Paged K/V (head_dim 128, bf16): pools [num_pages][2^page_shift][Hkv][128], request b's
+// logical row r at page block_table[b * max_pages + (r >> page_shift)]
+hipError_t launch_attn_bf16_paged(const void* Q, const void* K_pages, const void* V_pages,
+                                  const int32_t* block_table, int max_pages, int num_pages,
+                                  int page_shift, const int32_t* ctx, const int32_t* parent,
+                                  const int32_t* n, int batch, int budget, int Hq, int Hkv,
+                                  int max_ctx, float scale, const AttnPlan& pl, void* O,
+                                  void* ws, hipStream_t s);
+// longest split a paged call may take: its page ids must fit the kernel's table
+int paged_max_split(int page_shift);
 
 hipError_t launch_attn_f32(const float* Q, const float* K, const float* V, const int64_t* off,
                            const int32_t* ctx, const int32_t* parent, const int32_t* n,

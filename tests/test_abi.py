@@ -155,6 +155,43 @@ def test_attention_workspace_is_a_pure_function(lib):
                                 0, 0.088, fake, fake, a - 1, None) == _lib.TAPS_ERR_WORKSPACE
 
 
+@pytest.mark.parametrize("page_rows,hd,dtype,max_pages,num_pages,status", [
+    (64, 128, 0, 130, 200, _lib.TAPS_OK),
+    (32, 128, 0, 260, 1, _lib.TAPS_OK),
+    (4096, 128, 0, 3, 1, _lib.TAPS_OK),
+    (48, 128, 0, 200, 200, _lib.TAPS_ERR_INVALID_ARG),       # not a power of two
+    (16, 128, 0, 600, 600, _lib.TAPS_ERR_INVALID_ARG),       # below 32 rows
+    (8192, 128, 0, 2, 2, _lib.TAPS_ERR_INVALID_ARG),         # above 4096 rows
+    (64, 64, 0, 130, 200, _lib.TAPS_ERR_UNSUPPORTED),        # head_dim 64
+    (64, 128, 1, 130, 200, _lib.TAPS_ERR_UNSUPPORTED),       # fp32
+    (64, 128, 0, 128, 200, _lib.TAPS_ERR_INVALID_ARG),       # 128 * 64 < 8192 + 64 rows
+    (64, 128, 0, 129, 200, _lib.TAPS_OK),                    # 129 * 64 = 8192 + 64 rows
+    (64, 128, 0, 130, 0, _lib.TAPS_ERR_INVALID_ARG),         # no pages
+])
+def test_paged_attention_validation(lib, page_rows, hd, dtype, max_pages, num_pages, status):
+    """tree_verify_attn_paged checks its page geometry on the host; every case stops
+    before a launch (the pointers are never dereferenced)."""
+    fake = 1 << 20
+    need = lib.tree_verify_attn_paged_workspace_bytes(1, 64, 32, 8, hd, 8192, page_rows)
+    args = (fake, fake, fake, num_pages, page_rows, fake, max_pages, fake, fake, fake, 1, 64,
+            32, 8, hd, 8192, dtype, 0.088, fake, fake)
+    if status == _lib.TAPS_OK:
+        assert need > 0
+        # a valid geometry gets as far as the workspace check
+        assert lib.tree_verify_attn_paged(*args, need - 1, None) == _lib.TAPS_ERR_WORKSPACE
+    else:
+        assert lib.tree_verify_attn_paged(*args, 1 << 30, None) == status
+
+
+def test_paged_attention_workspace_matches_contiguous_plan(lib):
+    """Below the paged split cap the paged plan is the contiguous one, so the workspaces
+    agree; without a valid page size there is none."""
+    a = lib.tree_verify_attn_workspace_bytes(1, 64, 32, 8, 128, 8192, 0)
+    assert lib.tree_verify_attn_paged_workspace_bytes(1, 64, 32, 8, 128, 8192, 64) == a
+    assert lib.tree_verify_attn_paged_workspace_bytes(1, 64, 32, 8, 128, 8192, 48) == 0
+    assert lib.tree_verify_attn_paged_workspace_bytes(0, 64, 32, 8, 128, 8192, 64) == 0
+
+
 def test_walk_validation(lib):
     assert lib.accept_walk(None, 1, 64, 16, None, None, None, None, None) == _lib.TAPS_ERR_INVALID_ARG
     assert lib.accept_walk(None, 1, 64, 33, None, None, None, None, None) == _lib.TAPS_ERR_UNSUPPORTED

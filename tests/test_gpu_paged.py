@@ -1,0 +1,202 @@
+"""GPU parity of the paged tree attention (tree_verify_attn_paged) through the C ABI.
+
+Each request's logical cache rows (its context, then one row per tree node) are scattered
+page by page into random distinct pages of pools whose other pages hold NaN bits, and the
+block-table entries past a request's pages hold junk ids (negative, or past the pool), so
+a wrong page or slot, or a read of an entry the request does not reach, shows up.  The
+result is compared with the oracle's paged form (bf16 bounds as for the contiguous call),
+and, for the identity layout, bit for bit with the contiguous call."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests import _util as U
+from workloads import BF16, bf16_bits_to_f32, f32_to_bf16_bits, gen_round, kv_offsets
+
+pytestmark = pytest.mark.gpu
+
+NAN_BF16 = np.uint16(0x7FC0)
+
+
+@pytest.fixture(scope="module")
+def taps():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_00487_amd as taps
+    taps.load()
+    return taps
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def to_pages(K, V, off, ctx, N, page_rows, rng, spare=7):
+    """Scatter request b's ctx[b] + N logical rows (from row off[b] of the contiguous bf16
+    caches K, V) page by page into random distinct pages of NaN-filled pools; `spare` pages
+    stay unused.  Returns the pools [pages][page_rows][Hkv][hd] and the block table."""
+    B = len(ctx)
+    need = [-(-(int(ctx[b]) + N) // page_rows) for b in range(B)]
+    num_pages = sum(need) + spare
+    ids = rng.permutation(num_pages)[:sum(need)]
+    max_pages = max(need) + 3
+    table = np.where(rng.random((B, max_pages)) < 0.5, -5, num_pages + 1000).astype(np.int32)
+    Kp = np.full((num_pages, page_rows) + K.shape[1:], NAN_BF16, dtype=np.uint16)
+    Vp = np.full_like(Kp, NAN_BF16)
+    k = 0
+    for b in range(B):
+        rows = int(ctx[b]) + N
+        for p in range(need[b]):
+            table[b, p] = ids[k]
+            lo, hi = p * page_rows, min(rows, (p + 1) * page_rows)
+            Kp[ids[k], :hi - lo] = K[int(off[b]) + lo:int(off[b]) + hi]
+            Vp[ids[k], :hi - lo] = V[int(off[b]) + lo:int(off[b]) + hi]
+            k += 1
+    return Kp, Vp, table
+
+
+def run_paged(taps, Q, Kp, Vp, table, page_rows, ctx, parents, n, Hq, Hkv, max_ctx):
+    B, N = Q.shape[0], Q.shape[1]
+    att = taps.PagedTreeAttention(B, N, Hq, Hkv, max_ctx, page_rows, scale=128 ** -0.5)
+    att.ws.fill_(0xFF)            # NaN bits in every unwritten partial slot
+    O = att(U.to_dev(Q, True), U.to_dev(Kp, True), U.to_dev(Vp, True),
+            torch.from_numpy(table).cuda(), torch.from_numpy(ctx).cuda(),
+            torch.from_numpy(np.stack(parents)).cuda(), torch.tensor(n, dtype=torch.int32).cuda())
+    torch.cuda.synchronize()
+    return O
+
+
+def paged_ref(Q, Kp, Vp, table, page_rows, ctx, parents, n, samples=None):
+    f = lambda a: bf16_bits_to_f32(a).astype(np.float64)   # noqa: E731
+    return oracle.tree_attention_paged(f(Q), f(Kp), f(Vp), table, page_rows, ctx, parents, n,
+                                       128 ** -0.5, samples=samples)
+
+
+def random_inputs(rng, B, N, Hq, Hkv, ctx):
+    hd = 128
+    off = kv_offsets(ctx, N)
+    rows = int(off[-1] + ctx[-1] + N)
+    Q = f32_to_bf16_bits(rng.standard_normal((B, N, Hq, hd)).astype(np.float32))
+    K = f32_to_bf16_bits(rng.standard_normal((rows, Hkv, hd)).astype(np.float32))
+    V = f32_to_bf16_bits(rng.standard_normal((rows, Hkv, hd)).astype(np.float32))
+    return Q, K, V, off
+
+
+@pytest.mark.parametrize("page_rows,ctx,N,Hq,Hkv", [
+    (32, [0, 1, 77, 300], 130, 8, 2),        # one-stage pages; a 130-node chain, a star
+    (64, [3001, 1777], 64, 16, 4),           # several key splits, a ragged last one
+    (256, [5000, 20, 2047], 64, 32, 8),      # the ragged work list over pages
+    (4096, [700], 33, 8, 8),                 # one page holds the whole request
+])
+def test_paged_attention_matches_oracle(taps, page_rows, ctx, N, Hq, Hkv):
+    rng = np.random.default_rng(page_rows + N)
+    ctx = np.array(ctx, dtype=np.int32)
+    B = len(ctx)
+    say(f"[paged] page_rows={page_rows} ctx={ctx.tolist()} N={N} Hq={Hq} Hkv={Hkv}")
+    Q, K, V, off = random_inputs(rng, B, N, Hq, Hkv, ctx)
+    kinds = [np.array([-1] + list(range(N - 1)), dtype=np.int32),            # chain
+             np.array([-1] + [0] * (N - 1), dtype=np.int32)]                 # star
+    parents = [kinds[b] if b < 2 and page_rows == 32 else
+               np.array([-1] + [int(rng.integers(0, i)) for i in range(1, N)], dtype=np.int32)
+               for b in range(B)]
+    n = [N if b != 1 else max(1, N // 3) for b in range(B)]
+    Kp, Vp, table = to_pages(K, V, off, ctx, N, page_rows, rng)
+    O = run_paged(taps, Q, Kp, Vp, table, page_rows, ctx, parents, n, Hq, Hkv, int(ctx.max()))
+    ref = paged_ref(Q, Kp, Vp, table, page_rows, ctx, parents, n)
+    got = U.gpu_o_as_f64(O)
+    for b in range(B):
+        U.attention_error(got[b, :n[b]], ref[b, :n[b]], BF16,
+                          f"paged page_rows={page_rows} b={b} ctx={ctx[b]} n={n[b]}")
+
+
+def test_paged_identity_layout_equals_contiguous(taps):
+    """The Qwen3-8B round's cache cut into 64-row pages in order (block table 0, 1, 2, ...)
+    gives exactly the contiguous call's output: the same plan, loads and arithmetic."""
+    inp = gen_round("qwen3_8b")
+    c = inp.cfg
+    trees = U.oracle_trees(inp)
+    parent, _, n = U.tree_device(trees)
+    rows = int(inp.ctx_len[0]) + c.budget
+    assert rows % 64 == 0 and inp.K.shape[0] == rows
+    say(f"[paged-identity] qwen3_8b rows={rows}")
+    Q, K, V = (U.to_dev(a, True) for a in (inp.Q, inp.K, inp.V))
+    att = taps.TreeAttention(c.batch, c.budget, c.Hq, c.Hkv, c.head_dim, int(inp.ctx_len[0]),
+                             dtype=c.dtype, scale=c.scale)
+    O_c = att(Q, K, V, torch.from_numpy(inp.kv_offset).cuda(), torch.from_numpy(inp.ctx_len).cuda(),
+              parent, n)
+    patt = taps.PagedTreeAttention(c.batch, c.budget, c.Hq, c.Hkv, int(inp.ctx_len[0]), 64,
+                                   scale=c.scale)
+    table = torch.arange(rows // 64, dtype=torch.int32).reshape(1, -1).cuda()
+    O_p = patt(Q, K.reshape(rows // 64, 64, c.Hkv, c.head_dim),
+               V.reshape(rows // 64, 64, c.Hkv, c.head_dim), table,
+               torch.from_numpy(inp.ctx_len).cuda(), parent, n)
+    torch.cuda.synchronize()
+    nn = int(trees[0].n)
+    assert torch.equal(O_p[:, :nn], O_c[:, :nn])
+
+
+def test_paged_tree_rows_dominate_at_full_size(taps):
+    """The Qwen3-8B shape (context 8192, 64 nodes, the bench's key splits) over 128-row pages
+    in random order, with a common direction in every query and in the tree rows' keys so
+    that each node's ancestors carry almost all of its softmax mass: a wrong page of the
+    tree rows, or a wrong mask bit in the last split, moves O by O(1).  Every row."""
+    inp = gen_round("qwen3_8b")
+    c = inp.cfg
+    trees = U.oracle_trees(inp)
+    rng = np.random.default_rng(78)
+    w = rng.standard_normal((c.Hkv, c.head_dim))
+    w /= np.linalg.norm(w, axis=1, keepdims=True)
+    G = c.Hq // c.Hkv
+    Qf = bf16_bits_to_f32(inp.Q).astype(np.float64) + 16.0 * np.repeat(w, G, axis=0)[None, None]
+    Kf = bf16_bits_to_f32(inp.K).astype(np.float64)
+    ctx = int(inp.ctx_len[0])
+    Kf[ctx:ctx + c.budget] += 16.0 * w[None]
+    Q, K = f32_to_bf16_bits(Qf.astype(np.float32)), f32_to_bf16_bits(Kf.astype(np.float32))
+    say("[paged-tree-dominant] qwen3_8b shape, 128-row pages")
+    Kp, Vp, table = to_pages(K, inp.V, inp.kv_offset, inp.ctx_len, c.budget, 128, rng)
+    parents = [t.parent for t in trees]
+    n = [t.n for t in trees]
+    O = run_paged(taps, Q, Kp, Vp, table, 128, inp.ctx_len, parents, n, c.Hq, c.Hkv, ctx)
+    ref = paged_ref(Q, Kp, Vp, table, 128, inp.ctx_len, parents, n)
+    U.attention_error(U.gpu_o_as_f64(O), ref, BF16, "paged tree-dominant qwen3_8b")
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_paged_attention_fuzz(taps, seed):
+    """Seeded batches: 1-4 requests, contexts from empty to 4000 rows (max_ctx above them
+    all), 1-80 nodes with random parents, 1-4 KV heads of 1-4 query heads, pages of 32 to
+    1024 rows; sampled (node, head) rows of every request."""
+    rng = np.random.default_rng(700 + seed)
+    B = int(rng.integers(1, 5))
+    N = int(rng.integers(1, 81))
+    Hkv = int(rng.choice([1, 2, 4]))
+    Hq = Hkv * int(rng.choice([1, 2, 4]))
+    page_rows = int(rng.choice([32, 64, 128, 256, 1024]))
+    ctx = rng.integers(0, 4001, B).astype(np.int32)
+    n = [int(x) for x in rng.integers(0, N + 1, B)]
+    n[int(rng.integers(0, B))] = N
+    max_ctx = int(ctx.max()) + int(rng.integers(0, 300))
+    say(f"[paged-fuzz] seed={seed} B={B} N={N} Hq={Hq} Hkv={Hkv} page_rows={page_rows} "
+        f"ctx={ctx.tolist()} n={n} max_ctx={max_ctx}")
+    Q, K, V, off = random_inputs(rng, B, N, Hq, Hkv, ctx)
+    parents = [np.array([-1] + [int(rng.integers(0, i)) for i in range(1, N)], dtype=np.int32)
+               for _ in range(B)]
+    Kp, Vp, table = to_pages(K, V, off, ctx, N, page_rows, rng)
+    # the table must cover max_ctx + N rows for every request: widen it with junk entries
+    wide = -(-(max_ctx + N) // page_rows)
+    if table.shape[1] < wide:
+        table = np.concatenate([table, np.full((B, wide - table.shape[1]), -3, np.int32)], 1)
+    O = run_paged(taps, Q, Kp, Vp, table, page_rows, ctx, parents, n, Hq, Hkv, max_ctx)
+    picks = [(b, int(i), int(h)) for b in range(B) if n[b]
+             for i in sorted({0, n[b] - 1, *rng.integers(0, n[b], 6).tolist()})
+             for h in sorted({0, Hq - 1, int(rng.integers(0, Hq))})]
+    ref = paged_ref(Q, Kp, Vp, table, page_rows, ctx, parents, n, samples=picks)
+    got = U.gpu_o_as_f64(O)
+    for b in range(B):
+        if n[b]:
+            U.attention_error(got[b, :n[b]], ref[b, :n[b]], BF16,
+                              f"paged fuzz b={b} ctx={ctx[b]} page_rows={page_rows}")

@@ -106,3 +106,50 @@ def test_single_node_is_decode_attention():
         s = 0.25 * K[:ctx + 1, h] @ Q[0, 0, h]
         p = np.exp(s - s.max())
         np.testing.assert_allclose(O[0, 0, h], (p / p.sum()) @ V[:ctx + 1, h], rtol=1e-13)
+
+
+def _scatter_to_pages(K, V, off, ctx, N, page_rows, pool_pages, rng):
+    """Write each request's logical rows (ctx + N of them, from row off[b] of the contiguous
+    caches K and V) page by page into randomly chosen distinct pages of NaN-filled pools."""
+    B = len(ctx)
+    need = [-(-(int(ctx[b]) + N) // page_rows) for b in range(B)]
+    ids = rng.permutation(pool_pages)[:sum(need)]
+    table = np.full((B, max(need) + 2), -7, dtype=np.int32)   # entries past a request: junk
+    Kp = np.full((pool_pages, page_rows) + K.shape[1:], np.nan)
+    Vp = np.full_like(Kp, np.nan)
+    k = 0
+    for b in range(B):
+        rows = int(ctx[b]) + N
+        for p in range(need[b]):
+            table[b, p] = ids[k]
+            lo, hi = p * page_rows, min(rows, (p + 1) * page_rows)
+            Kp[ids[k], :hi - lo] = K[int(off[b]) + lo:int(off[b]) + hi]
+            Vp[ids[k], :hi - lo] = V[int(off[b]) + lo:int(off[b]) + hi]
+            k += 1
+    return Kp, Vp, table
+
+
+@pytest.mark.parametrize("page_rows", [1, 4, 32])
+def test_paged_oracle_equals_contiguous(page_rows):
+    """The paged form gathers exactly the rows of the contiguous layout: pages scattered at
+    random over NaN-filled pools, with junk table entries past each request, give the same
+    O as the contiguous cache, bit for bit, for two different page assignments."""
+    from oracle.attention import tree_attention_paged
+    rng = np.random.default_rng(91 + page_rows)
+    B, N, Hq, Hkv, hd = 3, 9, 4, 2, 8
+    ctx = np.array([0, 5, 37], dtype=np.int32)
+    off = np.concatenate([[0], np.cumsum(ctx + N)[:-1]]).astype(np.int64)
+    rows = int(off[-1] + ctx[-1] + N)
+    Q = rng.standard_normal((B, N, Hq, hd))
+    K = rng.standard_normal((rows, Hkv, hd))
+    V = rng.standard_normal((rows, Hkv, hd))
+    parents = [np.array([-1] + [int(rng.integers(0, i)) for i in range(1, N)], dtype=np.int32)
+               for _ in range(B)]
+    n = [N, 4, 7]
+    ref = tree_attention(Q, K, V, off, ctx, parents, n, 0.3)
+    for trial in range(2):
+        pool_pages = 3 * (rows // page_rows + B + 1)
+        Kp, Vp, table = _scatter_to_pages(K, V, off, ctx, N, page_rows, pool_pages, rng)
+        got = tree_attention_paged(Q, Kp, Vp, table, page_rows, ctx, parents, n, 0.3)
+        for b in range(B):
+            assert np.array_equal(got[b, :n[b]], ref[b, :n[b]]), (page_rows, trial, b)
