@@ -63,12 +63,42 @@ def parse():
                          "learned: the learned-scorer hook with seeded random weights "
                          "(embedding 16, hidden 32)")
     ap.add_argument("--sets", type=int, default=0, help="input sets to rotate (0: enough to exceed the MALL)")
+    ap.add_argument("--paged", type=int, default=0,
+                    help="the round's attention reads a paged KV cache with pages of this many "
+                         "rows (a power of two, 32..4096; pages in random order); 0: contiguous")
     ap.add_argument("--eager", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy (reference for the HBM byte counters)")
     return ap.parse_args()
+
+
+def paged_copy(torch, K, V, kv_offset, ctx_len, budget, max_ctx, page_rows, rng, dev):
+    """Request b's cache rows (its context, then its budget tree rows) copied page by page
+    into pools, the pages in random order; returns the pools and the block table."""
+    B = len(ctx_len)
+    need = [-(-(int(ctx_len[b]) + budget) // page_rows) for b in range(B)]
+    ids = rng.permutation(sum(need))
+    table = np.zeros((B, -(-(max_ctx + budget) // page_rows)), dtype=np.int32)
+    src, dst = [], []
+    k = 0
+    for b in range(B):
+        rows = int(ctx_len[b]) + budget
+        for p in range(need[b]):
+            lo, hi = p * page_rows, min(rows, (p + 1) * page_rows)
+            table[b, p] = ids[k]
+            src.append(np.arange(lo, hi) + int(kv_offset[b]))
+            dst.append(np.arange(hi - lo) + int(ids[k]) * page_rows)
+            k += 1
+    src = torch.from_numpy(np.concatenate(src)).to(dev)
+    dst = torch.from_numpy(np.concatenate(dst)).to(dev)
+    pools = []
+    for X in (K, V):
+        P = torch.zeros((sum(need) * page_rows,) + tuple(X.shape[1:]), dtype=X.dtype, device=dev)
+        P[dst] = X[src]
+        pools.append(P.view((sum(need), page_rows) + tuple(X.shape[1:])))
+    return pools[0], pools[1], torch.from_numpy(table).to(dev)
 
 
 def copy_calibration():
@@ -201,6 +231,12 @@ def main():
                         beta=cfg.beta, scorer=scorer, mlp=mlp_dev)
     att = taps.TreeAttention(cfg.batch, cfg.budget, cfg.Hq, cfg.Hkv, cfg.head_dim, max_ctx,
                              dtype=cfg.dtype, scale=cfg.scale)
+    patt = None
+    if args.paged:
+        if not bf or cfg.head_dim != 128:
+            sys.exit("--paged needs bf16 and head_dim 128")
+        patt = taps.PagedTreeAttention(cfg.batch, cfg.budget, cfg.Hq, cfg.Hkv, max_ctx,
+                                       args.paged, scale=cfg.scale)
     walk = taps.AcceptWalk(cfg.batch, cfg.budget, cfg.block)
     commit = taps.KVCommit(cfg.batch, cfg.budget, cfg.block, cfg.Hkv, cfg.head_dim, max_ctx,
                            dtype=cfg.dtype)
@@ -225,14 +261,25 @@ def main():
                                       seed=inp.seed, token=tok[b]) for b in range(cfg.batch)])
         s["tgt"] = torch.from_numpy(tgt.astype(np.int32)).to(dev)
         s["n"] = nn.copy()
+        if patt is not None:
+            s["Kp"], s["Vp"], s["tab"] = paged_copy(
+                torch, s["K"], s["V"], inp.kv_offset, inp.ctx_len, cfg.budget, max_ctx,
+                args.paged, np.random.default_rng(inp.seed + 17), dev)
         sets.append(s)
         print(f"[bench] input set {k + 1}/{nsets} ready (n_nodes {nn.tolist()[:4]}...)",
               file=sys.stderr, flush=True)
 
+    def attn_call(s, events=None):
+        if patt is not None:
+            patt(s["Q"], s["Kp"], s["Vp"], s["tab"], s["ctx"], s["tree"].parent,
+                 s["tree"].n_nodes, out=s["O"], events=events)
+        else:
+            att(s["Q"], s["K"], s["V"], s["off"], s["ctx"], s["tree"].parent, s["tree"].n_nodes,
+                out=s["O"], events=events)
+
     def round_(s, events=None):
         sel(s["marg"], s["tree"])
-        att(s["Q"], s["K"], s["V"], s["off"], s["ctx"], s["tree"].parent, s["tree"].n_nodes,
-            out=s["O"], events=events)
+        attn_call(s, events)
         walk(s["tree"], s["tgt"])
 
     stream = torch.cuda.Stream()
@@ -306,8 +353,7 @@ def main():
             e[0].record(stream)
             sel(s["marg"], s["tree"])
             e[1].record(stream)
-            att(s["Q"], s["K"], s["V"], s["off"], s["ctx"], s["tree"].parent, s["tree"].n_nodes,
-                out=s["O"], events=(e[2], e[3]))
+            attn_call(s, (e[2], e[3]))
             e[4].record(stream)
             walk(s["tree"], s["tgt"])
             e[5].record(stream)
@@ -321,8 +367,7 @@ def main():
             GR = 10
             stage_calls = {
                 "select": lambda s: sel(s["marg"], s["tree"]),
-                "attn_call": lambda s: att(s["Q"], s["K"], s["V"], s["off"], s["ctx"],
-                                           s["tree"].parent, s["tree"].n_nodes, out=s["O"]),
+                "attn_call": lambda s: attn_call(s),
                 "walk": lambda s: walk(s["tree"], s["tgt"]),
             }
             for name, fn in stage_calls.items():
@@ -430,7 +475,7 @@ def main():
     ms_per_step = elapsed / args.steps * 1e3
     rounds_per_s = cfg.batch * args.steps / elapsed
     achieved = attn_bytes / (t_attn * 1e-6) / 1e9
-    traffic = measured_traffic(cfg.name)
+    traffic = None if args.paged else measured_traffic(cfg.name)   # counters: contiguous only
     if bf and intensity > RIDGE:
         # more flops per byte than the machine balance: the matrix cores bound the kernel
         roofline = {"bound": "mfma", "kernel": "attn_bf16_kernel",
@@ -473,7 +518,8 @@ def main():
                         f"{'bf16 logits' if bf else 'fp32 probs'}, top-{cfg.K}, budget {cfg.budget}, "
                         f"{cfg.Hq}/{cfg.Hkv} heads x {cfg.head_dim}, context {int(s['inp'].ctx_len.max())}"
                         + (f", lambda2 {cfg.lambda2}, tau {cfg.tau}" if over else "")
-                        + (f", {args.scorer} scorer" if scorer else ""),
+                        + (f", {args.scorer} scorer" if scorer else "")
+                        + (f", paged KV ({args.paged}-row pages)" if args.paged else ""),
             "global_batch": cfg.batch,
             "budget": cfg.budget,
             "input_sets": nsets,

@@ -242,7 +242,8 @@ size_t tree_verify_attn_paged_workspace_bytes(int32_t batch, int32_t budget, int
  *   K_pages[block_table[b][r / page_rows]][r % page_rows] (and V_pages alike).
  *   K_pages,
  *   V_pages      [num_pages][page_rows][Hkv][head_dim] bf16 pools, 16-byte aligned
- *   num_pages    pages in each pool (>= 1)
+ *   num_pages    pages in each pool (>= 1; num_pages * page_rows below 2^32, else
+ *                TAPS_ERR_UNSUPPORTED)
  *   page_rows    rows per page: a power of two from 32 to 4096
  *   block_table  [batch][max_pages] int32 page ids, row b covering request b's rows in
  *                order; max_pages * page_rows must be at least max_ctx + budget.  Entries
@@ -260,6 +261,19 @@ taps_status tree_verify_attn_paged(const void *Q_tree, const void *K_pages, cons
                                    int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t max_ctx,
                                    int32_t dtype, float scale, void *O, void *ws,
                                    size_t ws_bytes, hipStream_t stream);
+
+/* tree_verify_attn_paged that also times its main attention kernel, as
+ * tree_verify_attn_timed does.  For profiling callers. */
+taps_status tree_verify_attn_paged_timed(const void *Q_tree, const void *K_pages,
+                                         const void *V_pages, int32_t num_pages,
+                                         int32_t page_rows, const int32_t *block_table,
+                                         int32_t max_pages, const int32_t *ctx_len,
+                                         const int32_t *tree_parent, const int32_t *n_nodes,
+                                         int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv,
+                                         int32_t head_dim, int32_t max_ctx, int32_t dtype,
+                                         float scale, void *O, void *ws, size_t ws_bytes,
+                                         hipStream_t stream, hipEvent_t ev_begin,
+                                         hipEvent_t ev_end);
 
 /* Greedy acceptance walk (temperature 0).
  *   tree           [host] struct; parent, token and n_nodes are read

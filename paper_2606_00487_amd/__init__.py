@@ -198,10 +198,12 @@ class PagedTreeAttention:
             batch, budget, Hq, Hkv, hd, max_ctx, self.page_rows)
         self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device=device)
 
-    def __call__(self, Q, K_pages, V_pages, block_table, ctx_len, parent, n_nodes, out=None):
+    def __call__(self, Q, K_pages, V_pages, block_table, ctx_len, parent, n_nodes, out=None,
+                 events=None):
         """K_pages, V_pages: [num_pages, page_rows, Hkv, 128] bf16; block_table: [batch,
         max_pages] int32 page ids (request b's logical row r at page block_table[b, r //
-        page_rows], slot r % page_rows)."""
+        page_rows], slot r % page_rows).  events: optional (begin, end) pair recorded around
+        the main attention kernel only (tree_verify_attn_paged_timed)."""
         batch, budget, Hq, Hkv, hd, max_ctx = self.shape
         _need(Q, "Q_tree", torch.bfloat16, (batch, budget, Hq, hd))
         _need(K_pages, "K_pages", torch.bfloat16)
@@ -218,11 +220,16 @@ class PagedTreeAttention:
         _need(n_nodes, "n_nodes", torch.int32, (batch,))
         O = out if out is not None else torch.empty_like(Q)
         _need(O, "O", torch.bfloat16, (batch, budget, Hq, hd))
-        _lib.check(self.lib, "tree_verify_attn_paged", self.lib.tree_verify_attn_paged(
-            _ptr(Q), _ptr(K_pages), _ptr(V_pages), K_pages.shape[0], self.page_rows,
-            _ptr(block_table), block_table.shape[1], _ptr(ctx_len), _ptr(parent), _ptr(n_nodes),
-            batch, budget, Hq, Hkv, hd, max_ctx, BF16, self.scale, _ptr(O), _ptr(self.ws),
-            self.ws_bytes, _stream()))
+        args = (_ptr(Q), _ptr(K_pages), _ptr(V_pages), K_pages.shape[0], self.page_rows,
+                _ptr(block_table), block_table.shape[1], _ptr(ctx_len), _ptr(parent),
+                _ptr(n_nodes), batch, budget, Hq, Hkv, hd, max_ctx, BF16, self.scale, _ptr(O),
+                _ptr(self.ws), self.ws_bytes, _stream())
+        if events is None:
+            _lib.check(self.lib, "tree_verify_attn_paged", self.lib.tree_verify_attn_paged(*args))
+        else:
+            _lib.check(self.lib, "tree_verify_attn_paged_timed",
+                       self.lib.tree_verify_attn_paged_timed(*args, events[0].cuda_event,
+                                                             events[1].cuda_event))
         return O
 
 

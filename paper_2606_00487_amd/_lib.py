@@ -33,6 +33,7 @@ EXPORTED = [
     "tree_verify_attn_timed", "accept_walk", "kv_commit", "taps_status_string",
     "taps_spec_exp_host", "verify_layer_workspace_bytes", "verify_layer", "taps_select_noalloc",
     "tree_verify_attn_paged_workspace_bytes", "tree_verify_attn_paged",
+    "tree_verify_attn_paged_timed",
 ]
 SELECT_SCRATCH_BYTES = 8 << 20   # TAPS_SELECT_SCRATCH_BYTES
 
@@ -109,6 +110,8 @@ def load(path: str = LIB_PATH):
     lib.tree_verify_attn_paged.argtypes = [vp, vp, vp, i32, i32, vp, i32, vp, vp, vp, i32, i32,
                                            i32, i32, i32, i32, i32, f32, vp, vp, sz, vp]
     lib.tree_verify_attn_paged.restype = i32
+    lib.tree_verify_attn_paged_timed.argtypes = lib.tree_verify_attn_paged.argtypes + [vp, vp]
+    lib.tree_verify_attn_paged_timed.restype = i32
     lib.accept_walk.argtypes = [P(Tree), i32, i32, i32, vp, vp, vp, vp, vp]
     lib.accept_walk.restype = i32
     lib.kv_commit.argtypes = [vp, vp, vp, vp, P(Tree), vp, vp, vp, i32, i32, i32, i32, i32, i32,

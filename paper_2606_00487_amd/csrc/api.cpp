@@ -244,18 +244,22 @@ size_t tree_verify_attn_paged_workspace_bytes(int32_t batch, int32_t budget, int
   return attn_ws_bytes(pl, batch, budget, Hq, Hkv, head_dim);
 }
 
-taps_status tree_verify_attn_paged(const void* Q_tree, const void* K_pages, const void* V_pages,
-                                   int32_t num_pages, int32_t page_rows,
-                                   const int32_t* block_table, int32_t max_pages,
-                                   const int32_t* ctx_len, const int32_t* tree_parent,
-                                   const int32_t* n_nodes, int32_t batch, int32_t budget,
-                                   int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t max_ctx,
-                                   int32_t dtype, float scale, void* O, void* ws,
-                                   size_t ws_bytes, hipStream_t stream) {
+taps_status tree_verify_attn_paged_timed(const void* Q_tree, const void* K_pages,
+                                         const void* V_pages, int32_t num_pages,
+                                         int32_t page_rows, const int32_t* block_table,
+                                         int32_t max_pages, const int32_t* ctx_len,
+                                         const int32_t* tree_parent, const int32_t* n_nodes,
+                                         int32_t batch, int32_t budget, int32_t Hq, int32_t Hkv,
+                                         int32_t head_dim, int32_t max_ctx, int32_t dtype,
+                                         float scale, void* O, void* ws, size_t ws_bytes,
+                                         hipStream_t stream, hipEvent_t ev_begin,
+                                         hipEvent_t ev_end) {
   const taps_status st =
       paged_check(batch, budget, Hq, Hkv, head_dim, max_ctx, dtype, scale, page_rows);
   if (st != TAPS_OK) return st;
   if (num_pages < 1 || max_pages < 1) return TAPS_ERR_INVALID_ARG;
+  // pool rows are addressed with 32-bit indices
+  if ((int64_t)num_pages * page_rows > (int64_t)UINT32_MAX) return TAPS_ERR_UNSUPPORTED;
   // every logical row a request may own (its context and its nodes) has a table entry
   if ((int64_t)max_pages * page_rows < (int64_t)max_ctx + budget) return TAPS_ERR_INVALID_ARG;
   if (batch == 0) return TAPS_OK;
@@ -272,9 +276,24 @@ taps_status tree_verify_attn_paged(const void* Q_tree, const void* K_pages, cons
   const AttnPlan pl = plan_attn(batch, budget, Hq, Hkv, head_dim, max_ctx, paged_max_split(shift));
   return launch_attn_bf16_paged(Q_tree, K_pages, V_pages, block_table, max_pages, num_pages,
                                 shift, ctx_len, tree_parent, n_nodes, batch, budget, Hq, Hkv,
-                                max_ctx, scale, pl, O, ws, stream) == hipSuccess
+                                max_ctx, scale, pl, O, ws, stream, ev_begin,
+                                ev_end) == hipSuccess
              ? TAPS_OK
              : TAPS_ERR_HIP;
+}
+
+taps_status tree_verify_attn_paged(const void* Q_tree, const void* K_pages, const void* V_pages,
+                                   int32_t num_pages, int32_t page_rows,
+                                   const int32_t* block_table, int32_t max_pages,
+                                   const int32_t* ctx_len, const int32_t* tree_parent,
+                                   const int32_t* n_nodes, int32_t batch, int32_t budget,
+                                   int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t max_ctx,
+                                   int32_t dtype, float scale, void* O, void* ws,
+                                   size_t ws_bytes, hipStream_t stream) {
+  return tree_verify_attn_paged_timed(Q_tree, K_pages, V_pages, num_pages, page_rows,
+                                      block_table, max_pages, ctx_len, tree_parent, n_nodes,
+                                      batch, budget, Hq, Hkv, head_dim, max_ctx, dtype, scale, O,
+                                      ws, ws_bytes, stream, nullptr, nullptr);
 }
 
 taps_status accept_walk(const taps_tree* tree, int32_t batch, int32_t budget, int32_t block,

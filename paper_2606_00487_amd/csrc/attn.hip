@@ -752,13 +752,19 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
   // read as zeros without touching memory (the host keeps the range below 2^31 bytes)
   // contiguous: one resource per operand over the split's rows; paged: the pool's head-g
   // column, with a resource per stage (issue below)
+  // (paged: as 64-bit integers held in scalar registers)
+  auto uniform_ptr = [](const uint16_t* p) -> uint64_t {
+    const uint64_t a = (uint64_t)p;
+    return ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)) << 32) |
+           (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a);
+  };
   const auto krs = [&] {
-    if constexpr (PAGED) return Kc + (size_t)g * HD;
+    if constexpr (PAGED) return uniform_ptr(Kc + (size_t)g * HD);
     else return buffer_rsrc(Kc + ((size_t)kv0 + k_begin) * row_stride + (size_t)g * HD,
                             (uint32_t)(k_end - k_begin) * rsb);
   }();
   const auto vrs = [&] {
-    if constexpr (PAGED) return Vc + (size_t)g * HD;
+    if constexpr (PAGED) return uniform_ptr(Vc + (size_t)g * HD);
     else return buffer_rsrc(Vc + ((size_t)kv0 + k_begin) * row_stride + (size_t)g * HD,
                             (uint32_t)(k_end - k_begin) * rsb);
   }();
@@ -771,25 +777,81 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     const int pc = (rb - kr * ROWB) / 16;
     ld_off = (uint32_t)kr * rsb + (uint32_t)((pc ^ kswz(kr)) * 16);
   }
+  // paged steps: waves 2q and 2q + 1 load all of the step's q-th stage, blocks 4 (w & 1) ..
+  // 4 (w & 1) + 3 each, so that a wave builds one resource per step instead of four
+  uint32_t pg_off[4] = {0u, 0u, 0u, 0u};
+  if constexpr (PAGED) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int rb = (4 * (wave_u & 1) + b) * BLK + lane * 16;
+      const int kr = rb / ROWB;
+      const int pc = (rb - kr * ROWB) / 16;
+      pg_off[b] = (uint32_t)kr * rsb + (uint32_t)((pc ^ kswz(kr)) * 16);
+    }
+  }
   // contiguous: the stage's offset goes into the per-lane offset, which the buffer range
-  // check covers.  Paged: a resource over the stage's rows in its page, cut at the split's
-  // end (rows past it, and whole stages past it, read as zeros without touching memory);
-  // page ids outside the pool are clamped into it, so no id reads outside the pool.
-  auto issue = [&](const auto& src, unsigned char* buf, int s) __attribute__((always_inline)) {
+  // check covers.  Paged: a resource over the stage's rows in page pg, cut at the split's end
+  // (rows past it, and whole stages past it, read as zeros without touching memory); page
+  // ids outside the pool are clamped into it, so no id reads outside the pool.  Everything
+  // here is uniform over the workgroup and kept in scalar registers.
+  const int kb_u = __builtin_amdgcn_readfirstlane(k_begin);
+  const int ke_u = __builtin_amdgcn_readfirstlane(k_end);
+  auto issue_at = [&](const auto& src, unsigned char* buf, int s, int pg)
+                      __attribute__((always_inline)) {
     if constexpr (!PAGED) {
       load_lds16(src, buf + wave_u * BLK, ld_off + (uint32_t)(s * KT) * rsb);
     } else {
-      const int r0 = k_begin + s * KT;               // logical row of the stage's first key
-      const int rows = min(max(k_end - r0, 0), KT);
-      const int j = (r0 >> pk.page_shift) - pi0;    // the page's entry in this split
-      int pg = 0;
-      if (s < 4) pg = fpg[min(j, 3)];
-      else if (rows > 0) pg = s_pg[min(j, kPageSlots - 1)];
-      pg = min(max(pg, 0), pk.num_pages - 1);
-      const size_t prow = ((size_t)pg << pk.page_shift) + (size_t)(r0 & ((1 << pk.page_shift) - 1));
-      load_lds16(buffer_rsrc(src + prow * row_stride, (uint32_t)rows * rsb), buf + wave_u * BLK,
-                 ld_off);
+      // a stage with no rows left gets an empty resource and touches no memory, whatever
+      // its page; the host keeps num_pages * page_rows below 2^32 (prow fits 32 bits)
+      const int r0 = kb_u + s * KT;                 // logical row of the stage's first key
+      const int rows = min(max(ke_u - r0, 0), KT);
+      const uint32_t prow = ((uint32_t)min(max(pg, 0), pk.num_pages - 1) << pk.page_shift) |
+                            (uint32_t)(r0 & ((1 << pk.page_shift) - 1));
+      const uint64_t a = src + (uint64_t)prow * rsb;
+      i32x4 r;                          // (readfirstlane: the words stay scalar)
+      r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+      r[1] = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+      r[2] = __builtin_amdgcn_readfirstlane((int)((uint32_t)rows * rsb));
+      r[3] = 0x00020000;
+      load_lds16(r, buf + wave_u * BLK, ld_off);
     }
+  };
+  // paged: the page of stage s < 4 (taken with the request's sizes) ...
+  auto first_page = [&](int s) -> int {
+    const int j = ((kb_u + s * KT) >> pk.page_shift) - pi0;
+    return j <= 0 ? fpg[0] : j == 1 ? fpg[1] : j == 2 ? fpg[2] : fpg[3];
+  };
+  // ... and of the four stages s0 .. s0 + 3, read from the LDS table (the step reads the
+  // next step's pages, so their latency is hidden behind its compute)
+  auto read_pages4 = [&](int s0, int (&v)[4]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r0 = kb_u + (s0 + q) * KT;
+      v[q] = s_pg[min((r0 >> pk.page_shift) - pi0, kPageSlots - 1)];
+    }
+  };
+  auto issue = [&](const auto& src, unsigned char* buf, int s) __attribute__((always_inline)) {
+    issue_at(src, buf, s, PAGED ? first_page(s) : 0);
+  };
+  auto page_of_stage = [&](int st) -> int {
+    return s_pg[min(((kb_u + st * KT) >> pk.page_shift) - pi0, kPageSlots - 1)];
+  };
+  // paged: this wave's four blocks of stage st (page pg) into slot buf
+  auto issue4_paged = [&](uint64_t src, unsigned char* buf, int st, int pg)
+                          __attribute__((always_inline)) {
+    const int r0 = kb_u + st * KT;
+    const int rows = min(max(ke_u - r0, 0), KT);
+    const uint32_t prow = ((uint32_t)min(max(pg, 0), pk.num_pages - 1) << pk.page_shift) |
+                          (uint32_t)(r0 & ((1 << pk.page_shift) - 1));
+    const uint64_t a = src + (uint64_t)prow * rsb;
+    i32x4 r;
+    r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    r[1] = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+    r[2] = __builtin_amdgcn_readfirstlane((int)((uint32_t)rows * rsb));
+    r[3] = 0x00020000;
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+      load_lds16(r, buf + (4 * (wave_u & 1) + b) * BLK, pg_off[b]);
   };
 
   const bool tree_split = k_end > ctx;
@@ -916,15 +978,25 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     constexpr int KGc = decltype(tag)::value;
     unsigned char* const ks[8] = {s_k0, s_k1, s_k2, s_k3, s_k4, s_k5, s_k6, s_k7};
     unsigned char* const vs[8] = {s_v0, s_v1, s_v2, s_v3, s_v4, s_v5, s_v6, s_v7};
+    int pnext1 = 0;                   // paged: the page id of this wave's next stage
     auto step = [&](auto pt, f32x16& sc, f32x16& sn, int t) __attribute__((always_inline)) {
       constexpr int P = decltype(pt)::value;   // t % 4
       TAPS_WAIT_VMCNT(8);             // V(2t), V(2t+1), K(2t+2), K(2t+3): this wave's part
       TAPS_STAGE_BARRIER();           // ... and every other wave's part; and every wave is
                                       // done with the slots of step t - 1, refilled here
-      issue(vrs, vs[(2 * P + 6) & 7], 2 * t + 6);
-      issue(vrs, vs[(2 * P + 7) & 7], 2 * t + 7);
-      issue(krs, ks[(2 * P + 8) & 7], 2 * t + 8);
-      issue(krs, ks[(2 * P + 9) & 7], 2 * t + 9);
+      if constexpr (PAGED) {
+        const int qw = wave_u >> 1;                 // stage 2t + 6 + qw: V, V, K, K
+        unsigned char* const dst = qw == 0 ? vs[(2 * P + 6) & 7] : qw == 1 ? vs[(2 * P + 7) & 7]
+                                 : qw == 2 ? ks[(2 * P + 8) & 7] : ks[(2 * P + 9) & 7];
+        issue4_paged(qw < 2 ? vrs : krs, dst, 2 * t + 6 + qw,
+                     __builtin_amdgcn_readfirstlane(pnext1));
+        pnext1 = page_of_stage(2 * t + 8 + qw);      // the next step's stage of this wave
+      } else {
+        issue_at(vrs, vs[(2 * P + 6) & 7], 2 * t + 6, 0);
+        issue_at(vrs, vs[(2 * P + 7) & 7], 2 * t + 7, 0);
+        issue_at(krs, ks[(2 * P + 8) & 7], 2 * t + 8, 0);
+        issue_at(krs, ks[(2 * P + 9) & 7], 2 * t + 9, 0);
+      }
       softmax_pv(sc, vs[(2 * P + KGc) & 7], ks[(2 * P + 2 + KGc) & 7], sn,
                  k_begin + (2 * t + KGc) * KT);
     };
@@ -932,8 +1004,17 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     TAPS_LDS_BARRIER();               // every wave has its queries: V slots 4-7 refill below
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) s_mfma(ks[KGc], kk, sA);
-    issue(vrs, s_v2, 2); issue(vrs, s_v3, 3); issue(krs, s_k4, 4); issue(krs, s_k5, 5);
-    issue(vrs, s_v4, 4); issue(vrs, s_v5, 5); issue(krs, s_k6, 6); issue(krs, s_k7, 7);
+    int pg[4] = {0, 0, 0, 0};         // paged: the pages of stages 4 .. 7
+    if constexpr (PAGED) {
+      read_pages4(4, pg);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) pg[q] = __builtin_amdgcn_readfirstlane(pg[q]);
+      pnext1 = page_of_stage(6 + (wave_u >> 1));   // this wave's stage of the first step
+    }
+    issue(vrs, s_v2, 2); issue(vrs, s_v3, 3);
+    issue_at(krs, s_k4, 4, pg[0]); issue_at(krs, s_k5, 5, pg[1]);
+    issue_at(vrs, s_v4, 4, pg[0]); issue_at(vrs, s_v5, 5, pg[1]);
+    issue_at(krs, s_k6, 6, pg[2]); issue_at(krs, s_k7, 7, pg[3]);
     for (int t = 0;;) {
       step(GroupTag<0>(), sA, sB, t);
       if (++t >= steps) break;
@@ -1399,11 +1480,12 @@ hipError_t launch_attn_bf16_paged(const void* Q, const void* K_pages, const void
                                   int page_shift, const int32_t* ctx, const int32_t* parent,
                                   const int32_t* n, int batch, int budget, int Hq, int Hkv,
                                   int max_ctx, float scale, const AttnPlan& pl, void* O,
-                                  void* ws, hipStream_t s) {
+                                  void* ws, hipStream_t s, hipEvent_t ev_begin,
+                                  hipEvent_t ev_end) {
   return launch_attn_bf16_impl<true>(Q, K_pages, V_pages, nullptr,
                                      PagedKV{block_table, max_pages, num_pages, page_shift}, ctx,
                                      parent, n, batch, budget, Hq, Hkv, 128, max_ctx, scale, pl,
-                                     O, ws, s, nullptr, nullptr);
+                                     O, ws, s, ev_begin, ev_end);
 }
 
 int paged_max_split(int page_shift) { return (kPageSlots - 1) << page_shift; }

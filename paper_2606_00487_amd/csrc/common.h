@@ -88,7 +88,8 @@ hipError_t launch_attn_bf16_paged(const void* Q, const void* K_pages, const void
                                   int page_shift, const int32_t* ctx, const int32_t* parent,
                                   const int32_t* n, int batch, int budget, int Hq, int Hkv,
                                   int max_ctx, float scale, const AttnPlan& pl, void* O,
-                                  void* ws, hipStream_t s);
+                                  void* ws, hipStream_t s, hipEvent_t ev_begin = nullptr,
+                                  hipEvent_t ev_end = nullptr);
 // longest split a paged call may take: its page ids must fit the kernel's table
 int paged_max_split(int page_shift);
 

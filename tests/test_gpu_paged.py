@@ -200,3 +200,30 @@ def test_paged_attention_fuzz(taps, seed):
         if n[b]:
             U.attention_error(got[b, :n[b]], ref[b, :n[b]], BF16,
                               f"paged fuzz b={b} ctx={ctx[b]} page_rows={page_rows}")
+
+
+def test_paged_timed_call_matches_and_times(taps):
+    """tree_verify_attn_paged_timed gives the untimed call's output bit for bit, and its
+    events bracket the main kernel (a positive duration)."""
+    rng = np.random.default_rng(9)
+    ctx = np.array([1500, 300], dtype=np.int32)
+    N, Hq, Hkv = 48, 16, 4
+    Q, K, V, off = random_inputs(rng, 2, N, Hq, Hkv, ctx)
+    parents = [np.array([-1] + [int(rng.integers(0, i)) for i in range(1, N)], dtype=np.int32)
+               for _ in range(2)]
+    n = [N, 20]
+    Kp, Vp, table = to_pages(K, V, off, ctx, N, 64, rng)
+    O1 = run_paged(taps, Q, Kp, Vp, table, 64, ctx, parents, n, Hq, Hkv, int(ctx.max()))
+    att = taps.PagedTreeAttention(2, N, Hq, Hkv, int(ctx.max()), 64, scale=128 ** -0.5)
+    ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    for e in ev:                  # materialise the handles; the library records them again
+        e.record()
+    torch.cuda.synchronize()
+    O2 = att(U.to_dev(Q, True), U.to_dev(Kp, True), U.to_dev(Vp, True),
+             torch.from_numpy(table).cuda(), torch.from_numpy(ctx).cuda(),
+             torch.from_numpy(np.stack(parents)).cuda(), torch.tensor(n, dtype=torch.int32).cuda(),
+             events=ev)
+    torch.cuda.synchronize()
+    for b in range(2):
+        assert torch.equal(O1[b, :n[b]], O2[b, :n[b]])
+    assert ev[0].elapsed_time(ev[1]) > 0
