@@ -12,7 +12,8 @@
  *   accept_walk       greedy (temperature 0) acceptance of the longest matching root
  *                     path (Sec. 1: one prefix path is committed per round; Limitations).
  *   kv_commit         the round's state update: the accepted path's tree K/V rows move
- *                     to the rows right after the context, and the emitted tokens.
+ *                     to the rows right after the context, and the emitted tokens
+ *                     (kv_commit_paged: the same on a paged cache).
  *   verify_layer      one attention layer of the target over the tree: projections,
  *                     per-head RMSNorm, rotary positions by tree depth, tree attention,
  *                     output projection (the verification forward's layer slice).
@@ -319,6 +320,23 @@ taps_status kv_commit(void *K_cache, void *V_cache, const int64_t *kv_offset,
                       int32_t budget, int32_t block, int32_t Hkv, int32_t head_dim,
                       int32_t max_ctx, int32_t dtype, int32_t *new_ctx_len,
                       int32_t *committed, int32_t *n_committed, hipStream_t stream);
+
+/* kv_commit for a paged KV cache (the layout of tree_verify_attn_paged): the same update
+ * in logical rows, request b's logical row r being row r % page_rows of page
+ * block_table[b][r / page_rows] of K_pages and V_pages ([num_pages][page_rows][Hkv]
+ * [head_dim], 16-byte aligned).  The rows of the m committed path nodes, logical rows
+ * ctx + path[b][j], move to logical rows ctx + j; no other row is written.  page_rows is a
+ * power of two from 32 to 4096 and max_pages * page_rows >= max_ctx + budget; page ids
+ * outside [0, num_pages) are clamped into it.  A request's rows must sit in pages of its
+ * own (pages shared with another request of the same call race).  The other arguments and
+ * outputs as for kv_commit. */
+taps_status kv_commit_paged(void *K_pages, void *V_pages, int32_t num_pages, int32_t page_rows,
+                            const int32_t *block_table, int32_t max_pages,
+                            const int32_t *ctx_len, const taps_tree *tree, const int32_t *path,
+                            const int32_t *path_len, const int32_t *bonus, int32_t batch,
+                            int32_t budget, int32_t block, int32_t Hkv, int32_t head_dim,
+                            int32_t max_ctx, int32_t dtype, int32_t *new_ctx_len,
+                            int32_t *committed, int32_t *n_committed, hipStream_t stream);
 
 /* [host] Weights of one attention layer of the target, a Qwen3-style block.  DEVICE bf16
  * arrays owned by the caller, row-major [out][in], 16-byte aligned:

@@ -27,4 +27,4 @@ from .select import (  # noqa: F401
 )
 from .attention import ancestor_sets, tree_attention, tree_attention_paged  # noqa: F401
 from .walk import accept_walk  # noqa: F401
-from .commit import committed_path, kv_commit  # noqa: F401
+from .commit import committed_path, kv_commit, kv_commit_paged  # noqa: F401

@@ -284,6 +284,46 @@ class KVCommit:
         return self.new_ctx, self.committed, self.n_committed
 
 
+class PagedKVCommit:
+    """kv_commit_paged: kv_commit on a paged cache (pools [num_pages, page_rows, Hkv,
+    head_dim] and a block table [batch, max_pages], as for PagedTreeAttention)."""
+
+    def __init__(self, batch, budget, block, Hkv, head_dim, max_ctx, page_rows, dtype=BF16,
+                 device="cuda"):
+        self.lib = load()
+        self.shape = (batch, budget, block, Hkv, head_dim, max_ctx, dtype)
+        self.page_rows = int(page_rows)
+        self.new_ctx = torch.empty(batch, dtype=torch.int32, device=device)
+        self.committed = torch.empty(batch, block + 1, dtype=torch.int32, device=device)
+        self.n_committed = torch.empty(batch, dtype=torch.int32, device=device)
+
+    def __call__(self, K_pages, V_pages, block_table, ctx_len, tree: TreeBuffers, path, path_len,
+                 bonus):
+        batch, budget, block, Hkv, hd, max_ctx, dtype = self.shape
+        tdt = _TORCH_DT[dtype]
+        _need(K_pages, "K_pages", tdt)
+        _need(V_pages, "V_pages", tdt, tuple(K_pages.shape))
+        if K_pages.dim() != 4 or K_pages.shape[1:] != (self.page_rows, Hkv, hd):
+            raise ValueError(f"K_pages: expected [pages, {self.page_rows}, {Hkv}, {hd}], "
+                             f"got {tuple(K_pages.shape)}")
+        _need(block_table, "block_table", torch.int32)
+        if block_table.dim() != 2 or block_table.shape[0] != batch:
+            raise ValueError(f"block_table: expected [{batch}, max_pages], "
+                             f"got {tuple(block_table.shape)}")
+        _need(ctx_len, "ctx_len", torch.int32, (batch,))
+        _need(tree.token, "tree.token", torch.int32, (batch, budget))
+        _need(path, "path", torch.int32, (batch, block + 1))
+        _need(path_len, "path_len", torch.int32, (batch,))
+        _need(bonus, "bonus", torch.int32, (batch,))
+        st = tree.struct()
+        _lib.check(self.lib, "kv_commit_paged", self.lib.kv_commit_paged(
+            _ptr(K_pages), _ptr(V_pages), K_pages.shape[0], self.page_rows, _ptr(block_table),
+            block_table.shape[1], _ptr(ctx_len), ctypes.byref(st), _ptr(path), _ptr(path_len),
+            _ptr(bonus), batch, budget, block, Hkv, hd, max_ctx, dtype, _ptr(self.new_ctx),
+            _ptr(self.committed), _ptr(self.n_committed), _stream()))
+        return self.new_ctx, self.committed, self.n_committed
+
+
 @dataclasses.dataclass
 class LayerWeights:
     """Device bf16 weights of one attention layer (taps_layer_weights), row-major [out][in]:

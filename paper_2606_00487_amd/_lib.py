@@ -33,7 +33,7 @@ EXPORTED = [
     "tree_verify_attn_timed", "accept_walk", "kv_commit", "taps_status_string",
     "taps_spec_exp_host", "verify_layer_workspace_bytes", "verify_layer", "taps_select_noalloc",
     "tree_verify_attn_paged_workspace_bytes", "tree_verify_attn_paged",
-    "tree_verify_attn_paged_timed",
+    "tree_verify_attn_paged_timed", "kv_commit_paged",
 ]
 SELECT_SCRATCH_BYTES = 8 << 20   # TAPS_SELECT_SCRATCH_BYTES
 
@@ -117,6 +117,9 @@ def load(path: str = LIB_PATH):
     lib.kv_commit.argtypes = [vp, vp, vp, vp, P(Tree), vp, vp, vp, i32, i32, i32, i32, i32, i32,
                               i32, vp, vp, vp, vp]
     lib.kv_commit.restype = i32
+    lib.kv_commit_paged.argtypes = [vp, vp, i32, i32, vp, i32, vp, P(Tree), vp, vp, vp, i32, i32,
+                                    i32, i32, i32, i32, i32, vp, vp, vp, vp]
+    lib.kv_commit_paged.restype = i32
     lib.verify_layer_workspace_bytes.argtypes = [i32] * 7
     lib.verify_layer_workspace_bytes.restype = ctypes.c_size_t
     lib.verify_layer.argtypes = [vp, P(LayerWeights), vp, vp, vp, vp, P(Tree), i32, i32, i32, i32,

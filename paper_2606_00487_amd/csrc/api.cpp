@@ -311,6 +311,46 @@ taps_status accept_walk(const taps_tree* tree, int32_t batch, int32_t budget, in
              : TAPS_ERR_HIP;
 }
 
+static taps_status commit_check(int32_t batch, int32_t budget, int32_t block, int32_t Hkv,
+                                int32_t head_dim, int32_t max_ctx, int32_t dtype) {
+  if (batch < 0 || budget < 1 || block < 1 || Hkv < 1 || max_ctx < 0)
+    return TAPS_ERR_INVALID_ARG;
+  if (budget > TAPS_MAX_BUDGET || block > TAPS_MAX_BLOCK) return TAPS_ERR_UNSUPPORTED;
+  if (head_dim != 64 && head_dim != 128) return TAPS_ERR_UNSUPPORTED;
+  if (dtype != TAPS_BF16 && dtype != TAPS_FP32) return TAPS_ERR_INVALID_ARG;
+  if ((int64_t)Hkv * head_dim * 4 > ((int64_t)1 << 24)) return TAPS_ERR_UNSUPPORTED;
+  if ((int64_t)max_ctx + budget > (int64_t)1 << 30) return TAPS_ERR_UNSUPPORTED;
+  if (batch > 65535) return TAPS_ERR_UNSUPPORTED;
+  return TAPS_OK;
+}
+
+taps_status kv_commit_paged(void* K_pages, void* V_pages, int32_t num_pages, int32_t page_rows,
+                            const int32_t* block_table, int32_t max_pages,
+                            const int32_t* ctx_len, const taps_tree* tree, const int32_t* path,
+                            const int32_t* path_len, const int32_t* bonus, int32_t batch,
+                            int32_t budget, int32_t block, int32_t Hkv, int32_t head_dim,
+                            int32_t max_ctx, int32_t dtype, int32_t* new_ctx_len,
+                            int32_t* committed, int32_t* n_committed, hipStream_t stream) {
+  const taps_status st = commit_check(batch, budget, block, Hkv, head_dim, max_ctx, dtype);
+  if (st != TAPS_OK) return st;
+  const int shift = page_shift_of(page_rows);
+  if (shift < 0 || num_pages < 1 || max_pages < 1) return TAPS_ERR_INVALID_ARG;
+  if ((int64_t)max_pages * page_rows < (int64_t)max_ctx + budget) return TAPS_ERR_INVALID_ARG;
+  if (batch == 0) return TAPS_OK;
+  if (!K_pages || !V_pages || !block_table || !ctx_len || !tree || !tree->token || !path ||
+      !path_len || !bonus || !new_ctx_len || !committed || !n_committed)
+    return TAPS_ERR_INVALID_ARG;
+  if ((((uintptr_t)K_pages | (uintptr_t)V_pages) & 15) != 0 || ((uintptr_t)block_table & 3) != 0)
+    return TAPS_ERR_INVALID_ARG;
+  if ((const void*)new_ctx_len == (const void*)ctx_len) return TAPS_ERR_INVALID_ARG;
+  const PagedKV pk{block_table, max_pages, num_pages, shift};
+  return launch_commit(K_pages, V_pages, nullptr, ctx_len, tree->token, path, path_len, bonus,
+                       batch, budget, block, Hkv, head_dim, dtype == TAPS_BF16 ? 2 : 4, max_ctx,
+                       new_ctx_len, committed, n_committed, stream, &pk) == hipSuccess
+             ? TAPS_OK
+             : TAPS_ERR_HIP;
+}
+
 taps_status kv_commit(void* K_cache, void* V_cache, const int64_t* kv_offset,
                       const int32_t* ctx_len, const taps_tree* tree, const int32_t* path,
                       const int32_t* path_len, const int32_t* bonus, int32_t batch,

@@ -453,12 +453,7 @@ struct DivMagic {
   }
 };
 
-// Paged KV cache: block table [batch][max_pages] of page ids into pools of num_pages pages
-// of 2^page_shift rows (32 .. 4096, so a 32-key stage never straddles two pages)
-struct PagedKV {
-  const int32_t* btab;
-  int max_pages, num_pages, page_shift;
-};
+// (Paged KV: pages of 32 .. 4096 rows, so a 32-key stage never straddles two pages.)
 // page ids of one split held in LDS (they share the (max, sum) exchange buffer, which is
 // used only after the key loop); split lengths are capped so that a split spans at most
 // this many pages

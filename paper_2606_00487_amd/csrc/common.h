@@ -69,6 +69,13 @@ struct AttnPlan {
   int pairs_max;
   int lcap;
 };
+// Paged KV cache: block table [batch][max_pages] of page ids into pools of num_pages pages
+// of 2^page_shift rows
+struct PagedKV {
+  const int32_t* btab;
+  int max_pages, num_pages, page_shift;
+};
+
 // max_len > 0 caps the split length (a multiple of 32): paged calls, whose splits may span
 // at most a fixed number of pages
 AttnPlan plan_attn(int batch, int budget, int Hq, int Hkv, int head_dim, int max_ctx,
@@ -103,11 +110,13 @@ hipError_t launch_walk(const taps_tree& t, int batch, int budget, int block,
                        const int32_t* target, int32_t* path, int32_t* path_len, int32_t* bonus,
                        hipStream_t s);
 
+// pk != nullptr: K and V are page pools addressed through pk's block table (off unused)
 hipError_t launch_commit(void* K, void* V, const int64_t* off, const int32_t* ctx,
                          const int32_t* token, const int32_t* path, const int32_t* path_len,
                          const int32_t* bonus, int batch, int budget, int block, int Hkv,
                          int head_dim, int elem_bytes, int max_ctx, int32_t* new_ctx,
-                         int32_t* committed, int32_t* n_committed, hipStream_t s);
+                         int32_t* committed, int32_t* n_committed, hipStream_t s,
+                         const PagedKV* pk = nullptr);
 
 // Layer slice: split-K skinny GEMM (fp32 partials [splits][M][N]), the projection
 // epilogue (RMSNorm, rotary positions, bf16 Q and cache rows) and the output reduction

@@ -192,6 +192,26 @@ def test_paged_attention_workspace_matches_contiguous_plan(lib):
     assert lib.tree_verify_attn_paged_workspace_bytes(0, 64, 32, 8, 128, 8192, 64) == 0
 
 
+def test_paged_commit_validation(lib):
+    fake = 1 << 20          # aligned, never dereferenced: every case stops before a launch
+    t = _lib.Tree(fake, fake, fake, fake, fake, fake, fake, fake)
+
+    def call(num_pages=100, page_rows=64, max_pages=129, sizes=(1, 64, 16, 8, 128, 8192, 0),
+             new_ctx=fake + 64):
+        return lib.kv_commit_paged(fake, fake, num_pages, page_rows, fake, max_pages, fake,
+                                   ctypes.byref(t), fake, fake, fake, *sizes, new_ctx,
+                                   fake + 128, fake + 192, None)
+
+    assert call(sizes=(0, 64, 16, 8, 128, 8192, 0)) == _lib.TAPS_OK            # nothing to do
+    assert call(page_rows=48) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(page_rows=16) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(max_pages=128) == _lib.TAPS_ERR_INVALID_ARG    # 128 * 64 < 8192 + 64 rows
+    assert call(num_pages=0) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(new_ctx=fake) == _lib.TAPS_ERR_INVALID_ARG      # new_ctx_len is ctx_len
+    assert call(sizes=(1, 513, 16, 8, 128, 8192, 0)) == _lib.TAPS_ERR_UNSUPPORTED
+    assert call(sizes=(1, 64, 16, 8, 96, 8192, 0)) == _lib.TAPS_ERR_UNSUPPORTED
+
+
 def test_walk_validation(lib):
     assert lib.accept_walk(None, 1, 64, 16, None, None, None, None, None) == _lib.TAPS_ERR_INVALID_ARG
     assert lib.accept_walk(None, 1, 64, 33, None, None, None, None, None) == _lib.TAPS_ERR_UNSUPPORTED

@@ -227,3 +227,107 @@ def test_paged_timed_call_matches_and_times(taps):
     for b in range(2):
         assert torch.equal(O1[b, :n[b]], O2[b, :n[b]])
     assert ev[0].elapsed_time(ev[1]) > 0
+
+
+# ------------------------------------------------------------------ paged KV commit
+def run_commit_paged(taps, Kp, Vp, table, page_rows, ctx, token, path, plen, bonus, budget,
+                     block, Hkv, hd, max_ctx, dtype):
+    bf = dtype == BF16
+    Kd, Vd = U.to_dev(Kp, bf), U.to_dev(Vp, bf)
+    batch = len(ctx)
+    tb = taps.TreeBuffers.empty(batch, block, 1, budget)
+    tb.token.copy_(torch.from_numpy(token.astype(np.int32)).cuda())
+    com = taps.PagedKVCommit(batch, budget, block, Hkv, hd, max_ctx, page_rows, dtype=dtype)
+    nc, cm, n = com(Kd, Vd, torch.from_numpy(table).cuda(),
+                    torch.from_numpy(ctx.astype(np.int32)).cuda(), tb,
+                    torch.from_numpy(path.astype(np.int32)).cuda(),
+                    torch.from_numpy(plen.astype(np.int32)).cuda(),
+                    torch.from_numpy(bonus.astype(np.int32)).cuda())
+    torch.cuda.synchronize()
+    bits = (lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)) if bf else \
+        (lambda t: t.cpu().numpy())
+    return bits(Kd), bits(Vd), nc.cpu().numpy(), cm.cpu().numpy(), n.cpu().numpy()
+
+
+@pytest.mark.parametrize("name,page_rows", [("qwen3_8b", 64), ("serve16", 32), ("stress", 256)])
+def test_paged_commit_matches_oracle_after_walk(taps, name, page_rows):
+    """kv_commit_paged after the oracle's walk (branching targets) on pools scattered at
+    random: pools, new context lengths and emitted tokens equal the oracle's byte for byte
+    (untouched pages included)."""
+    say(f"[paged-commit] {name} page_rows={page_rows}")
+    inp = gen_round(name)
+    c = inp.cfg
+    trees = U.oracle_trees(inp)
+    tgt = U.targets_for(inp, trees, branch=True)
+    from oracle.walk import walk_arrays
+    path = np.full((c.batch, c.block + 1), -1, np.int32)
+    plen = np.zeros(c.batch, np.int32)
+    bonus = np.zeros(c.batch, np.int32)
+    for b, t in enumerate(trees):
+        p, bo = oracle.accept_walk(t.parent, t.token, t.n, tgt[b])
+        path[b], plen[b], bonus[b] = walk_arrays(p, bo, c.block)
+    token = np.stack([t.token for t in trees])
+    max_ctx = int(inp.ctx_len.max())
+    rng = np.random.default_rng(page_rows)
+    Kp, Vp, table = to_pages(inp.K, inp.V, inp.kv_offset, inp.ctx_len, c.budget, page_rows, rng)
+    wide = -(-(max_ctx + c.budget) // page_rows)
+    if table.shape[1] < wide:
+        table = np.concatenate([table, np.full((c.batch, wide - table.shape[1]), -3, np.int32)], 1)
+    got = run_commit_paged(taps, Kp, Vp, table, page_rows, inp.ctx_len, token, path, plen, bonus,
+                           c.budget, c.block, c.Hkv, c.head_dim, max_ctx, BF16)
+    want = oracle.kv_commit_paged(Kp, Vp, table, page_rows, inp.ctx_len, token, path, plen,
+                                  bonus, c.budget, c.block, max_ctx)
+    for nm, g, w in zip(("K", "V", "new_ctx", "committed", "n"), got, want):
+        assert g.shape == w.shape and np.array_equal(g, w), nm
+    assert int(want[4].max()) > 1                     # some request accepted drafted nodes
+
+
+def test_paged_commit_edge_paths(taps):
+    """Root only, the longest chain, malformed and clamped paths, a context clamped to
+    max_ctx, over 32-row pages (a path crosses pages), fp32 and head_dim 64."""
+    from workloads import FP32
+    rng = np.random.default_rng(6)
+    budget, block, Hkv, hd = 40, 12, 2, 64
+    ctx = np.array([0, 7, 33, 100, 5, 64, 9], dtype=np.int32)
+    max_ctx = 64
+    B = len(ctx)
+    off = np.concatenate([[0], np.cumsum(ctx.astype(np.int64) + budget)[:-1]])
+    rows = int(off[-1] + ctx[-1] + budget)
+    K = rng.standard_normal((rows, Hkv, hd)).astype(np.float32)
+    V = rng.standard_normal((rows, Hkv, hd)).astype(np.float32)
+    # pools hold each request's rows for its clamped context
+    ctx_c = np.minimum(ctx, max_ctx)
+    off_c = off + (ctx - ctx_c)            # the clamped request's rows start later in K
+    need = [-(-(int(ctx_c[b]) + budget) // 32) for b in range(B)]
+    npages = sum(need) + 5
+    ids = rng.permutation(npages)
+    table = np.full((B, -(-(max_ctx + budget) // 32)), -9, np.int32)
+    Kp = rng.standard_normal((npages, 32, Hkv, hd)).astype(np.float32)
+    Vp = rng.standard_normal((npages, 32, Hkv, hd)).astype(np.float32)
+    k = 0
+    for b in range(B):
+        for p in range(need[b]):
+            table[b, p] = ids[k]
+            lo, hi = p * 32, min(int(ctx_c[b]) + budget, (p + 1) * 32)
+            Kp[ids[k], :hi - lo] = K[int(off_c[b]) + lo:int(off_c[b]) + hi]
+            Vp[ids[k], :hi - lo] = V[int(off_c[b]) + lo:int(off_c[b]) + hi]
+            k += 1
+    token = rng.integers(0, 1000, size=(B, budget)).astype(np.int32)
+    path = np.full((B, block + 1), -1, np.int32)
+    plen = np.zeros(B, np.int32)
+    path[0, 0] = 0; plen[0] = 1                                       # root only
+    path[1] = np.arange(block + 1); plen[1] = block + 1               # chain, identity moves
+    path[2] = [0] + sorted(rng.choice(np.arange(1, budget), size=block, replace=False).tolist())
+    plen[2] = block + 1                                               # longest scattered path
+    path[3, :5] = [0, 3, 9, 9, 20]; plen[3] = 5                       # repeat: cut after 9
+    path[4, :4] = [0, 2, 45, 46]; plen[4] = 4                         # beyond the budget: cut
+    path[5, :3] = [0, 1, 39]; plen[5] = 99                            # length clamped
+    path[6, :3] = [0, 4, 8]; plen[6] = 0                              # length clamped to 1
+    bonus = rng.integers(0, 1000, size=B).astype(np.int32)
+    got = run_commit_paged(taps, Kp, Vp, table, 32, ctx, token, path, plen, bonus, budget, block,
+                           Hkv, hd, max_ctx, FP32)
+    want = oracle.kv_commit_paged(Kp, Vp, table, 32, ctx, token, path, plen, bonus, budget,
+                                  block, max_ctx)
+    for nm, g, w in zip(("K", "V", "new_ctx", "committed", "n"), got, want):
+        assert g.shape == w.shape and np.array_equal(g, w), nm
+    assert list(want[4]) == [1, 13, 13, 3, 2, 3, 1]

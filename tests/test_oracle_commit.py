@@ -101,3 +101,49 @@ def test_commit_after_walk_keeps_the_accepted_rows(seed):
     assert m[0] == len(p) and newctx[0] == ctx + len(p)
     assert list(K2[ctx:ctx + len(p), 0, 0]) == [ctx + s for s in p]
     assert list(com[0][:len(p)]) == [int(token[s]) for s in p[1:]] + [bonus]
+
+
+@pytest.mark.parametrize("page_rows", [1, 4, 16])
+def test_paged_commit_equals_contiguous(page_rows):
+    """The paged commit is the contiguous one seen through the block table: pools scattered
+    from a contiguous cache at random, committed, and gathered back give the contiguous
+    commit's cache, row for row; pages of no request keep their contents."""
+    from oracle.commit import kv_commit, kv_commit_paged
+    rng = np.random.default_rng(60 + page_rows)
+    B, N, D, Hkv, hd = 3, 12, 5, 2, 4
+    ctx = np.array([0, 7, 29], dtype=np.int32)
+    off = np.concatenate([[0], np.cumsum(ctx + N)[:-1]]).astype(np.int64)
+    rows = int(off[-1] + ctx[-1] + N)
+    K = rng.standard_normal((rows, Hkv, hd))
+    V = rng.standard_normal((rows, Hkv, hd))
+    token = rng.integers(0, 1000, (B, N)).astype(np.int32)
+    path = np.array([[0, 1, 3, 7, 11, -1], [0, 2, 2, 5, -1, -1], [0, 4, 9, 10, 11, 12]],
+                    dtype=np.int32)
+    plen = np.array([5, 4, 6], dtype=np.int32)
+    bonus = np.array([5, 6, 7], dtype=np.int32)
+    want = kv_commit(K, V, off, ctx, token, path, plen, bonus, N, D, int(ctx.max()))
+    need = [-(-(int(ctx[b]) + N) // page_rows) for b in range(B)]
+    pool = sum(need) + 4
+    ids = rng.permutation(pool)
+    table = np.zeros((B, max(need)), dtype=np.int32)
+    Kp = rng.standard_normal((pool, page_rows, Hkv, hd))
+    Vp = rng.standard_normal((pool, page_rows, Hkv, hd))
+    k = 0
+    for b in range(B):
+        for p in range(need[b]):
+            table[b, p] = ids[k]
+            for r in range(p * page_rows, min(int(ctx[b]) + N, (p + 1) * page_rows)):
+                Kp[ids[k], r - p * page_rows] = K[int(off[b]) + r]
+                Vp[ids[k], r - p * page_rows] = V[int(off[b]) + r]
+            k += 1
+    got = kv_commit_paged(Kp, Vp, table, page_rows, ctx, token, path, plen, bonus, N, D,
+                          int(ctx.max()))
+    for b in range(B):
+        for r in range(int(ctx[b]) + N):
+            pg, sl = table[b, r // page_rows], r % page_rows
+            assert np.array_equal(got[0][pg, sl], want[0][int(off[b]) + r])
+            assert np.array_equal(got[1][pg, sl], want[1][int(off[b]) + r])
+    for x in ids[k:]:                        # pages no request owns
+        assert np.array_equal(got[0][x], Kp[x]) and np.array_equal(got[1][x], Vp[x])
+    for g, w in zip(got[2:], want[2:]):
+        assert np.array_equal(g, w)
