@@ -476,14 +476,16 @@ def main():
     rounds_per_s = cfg.batch * args.steps / elapsed
     achieved = attn_bytes / (t_attn * 1e-6) / 1e9
     traffic = None if args.paged else measured_traffic(cfg.name)   # counters: contiguous only
+    attn_kernel = (f"attn_bf16_kernel<{'true' if args.paged else 'false'}>" if bf
+                   else "attn_f32_kernel")
     if bf and intensity > RIDGE:
         # more flops per byte than the machine balance: the matrix cores bound the kernel
-        roofline = {"bound": "mfma", "kernel": "attn_bf16_kernel",
+        roofline = {"bound": "mfma", "kernel": attn_kernel,
                     "achieved": round(attn_fl / (t_attn * 1e-6) / 1e12, 1),
                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(attn_fl / (t_attn * 1e-6) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)}
     else:
-        roofline = {"bound": "hbm", "kernel": "attn_bf16_kernel" if bf else "attn_f32_kernel",
+        roofline = {"bound": "hbm", "kernel": attn_kernel,
                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4)}
     roofline.update({
