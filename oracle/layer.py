@@ -78,3 +78,34 @@ def verify_layer(X, Wq, Wk, Wv, Wo, q_norm, k_norm, Kc, Vc, kv_offset, ctx_len, 
     O = bf16_round(O)
     Y = O.reshape(B, N, Hq * hd) @ np.asarray(Wo, np.float64).T
     return Y, Kc, Vc, q, O
+
+
+def verify_layer_paged(X, Wq, Wk, Wv, Wo, q_norm, k_norm, K_pages, V_pages, block_table,
+                       page_rows, ctx_len, depth, parent, n_nodes, Hq, Hkv, hd, theta, eps,
+                       scale, samples=None):
+    """verify_layer over a paged cache (reading C20 of the layout: request b's logical row r
+    is row r % page_rows of page block_table[b][r // page_rows]): the logical rows are
+    gathered into a contiguous cache, the layer runs as defined above, and the rows are put
+    back.  Returns (Y, K_pages', V_pages', Q, O)."""
+    B, N = np.asarray(X).shape[:2]
+    where, offs, Ks, Vs = [], [], [], []
+    base = 0
+    for b in range(B):
+        rows = np.arange(int(ctx_len[b]) + N)
+        pg = np.asarray(block_table[b])[rows // page_rows]
+        sl = rows % page_rows
+        where.append((pg, sl))
+        Ks.append(np.asarray(K_pages)[pg, sl])
+        Vs.append(np.asarray(V_pages)[pg, sl])
+        offs.append(base)
+        base += len(rows)
+    Y, Kc, Vc, q, O = verify_layer(X, Wq, Wk, Wv, Wo, q_norm, k_norm, np.concatenate(Ks),
+                                   np.concatenate(Vs), np.asarray(offs, np.int64), ctx_len, depth,
+                                   parent, n_nodes, Hq, Hkv, hd, theta, eps, scale, samples)
+    Kp = np.array(K_pages, dtype=np.float64)
+    Vp = np.array(V_pages, dtype=np.float64)
+    for b in range(B):
+        pg, sl = where[b]
+        Kp[pg, sl] = Kc[offs[b]:offs[b] + len(pg)]
+        Vp[pg, sl] = Vc[offs[b]:offs[b] + len(pg)]
+    return Y, Kp, Vp, q, O

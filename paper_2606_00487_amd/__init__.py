@@ -381,3 +381,46 @@ class VerifyLayer:
             ctypes.byref(st), batch, budget, Hq, Hkv, hd, max_ctx, self.scale, _ptr(self.Y),
             _ptr(self.ws), self.ws.numel(), _stream()))
         return self.Y
+
+
+class PagedVerifyLayer:
+    """verify_layer_paged: verify_layer over a paged KV cache (pools [num_pages, page_rows,
+    Hkv, head_dim] and a block table [batch, max_pages], as for PagedTreeAttention)."""
+
+    def __init__(self, batch, budget, Hq, Hkv, head_dim, hidden, max_ctx, page_rows, scale=None,
+                 device="cuda"):
+        self.lib = load()
+        self.scale = float(scale if scale is not None else head_dim ** -0.5)
+        self.shape = (batch, budget, Hq, Hkv, head_dim, hidden, max_ctx)
+        self.page_rows = int(page_rows)
+        nbytes = self.lib.verify_layer_paged_workspace_bytes(batch, budget, Hq, Hkv, head_dim,
+                                                             hidden, max_ctx, self.page_rows)
+        if batch > 0 and nbytes == 0:
+            raise TapsError("verify_layer_paged_workspace_bytes", _lib.TAPS_ERR_UNSUPPORTED)
+        self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        self.Y = torch.empty((batch, budget, hidden), dtype=torch.bfloat16, device=device)
+
+    def __call__(self, X, w: LayerWeights, K_pages, V_pages, block_table, ctx_len,
+                 tree: TreeBuffers):
+        batch, budget, Hq, Hkv, hd, hidden, max_ctx = self.shape
+        _need(X, "X", torch.bfloat16, (batch, budget, hidden))
+        _need(K_pages, "K_pages", torch.bfloat16)
+        if K_pages.dim() != 4 or K_pages.shape[1:] != (self.page_rows, Hkv, hd):
+            raise ValueError(f"K_pages: expected [pages, {self.page_rows}, {Hkv}, {hd}], "
+                             f"got {tuple(K_pages.shape)}")
+        _need(V_pages, "V_pages", torch.bfloat16, tuple(K_pages.shape))
+        _need(block_table, "block_table", torch.int32)
+        if block_table.dim() != 2 or block_table.shape[0] != batch:
+            raise ValueError(f"block_table: expected [{batch}, max_pages], "
+                             f"got {tuple(block_table.shape)}")
+        _need(ctx_len, "ctx_len", torch.int32, (batch,))
+        ws = w.struct()
+        if ws.hidden != hidden:
+            raise ValueError(f"weights: hidden {ws.hidden}, expected {hidden}")
+        st = tree.struct()
+        _lib.check(self.lib, "verify_layer_paged", self.lib.verify_layer_paged(
+            _ptr(X), ctypes.byref(ws), _ptr(K_pages), _ptr(V_pages), K_pages.shape[0],
+            self.page_rows, _ptr(block_table), block_table.shape[1], _ptr(ctx_len),
+            ctypes.byref(st), batch, budget, Hq, Hkv, hd, max_ctx, self.scale, _ptr(self.Y),
+            _ptr(self.ws), self.ws.numel(), _stream()))
+        return self.Y

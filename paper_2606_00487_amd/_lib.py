@@ -33,7 +33,8 @@ EXPORTED = [
     "tree_verify_attn_timed", "accept_walk", "kv_commit", "taps_status_string",
     "taps_spec_exp_host", "verify_layer_workspace_bytes", "verify_layer", "taps_select_noalloc",
     "tree_verify_attn_paged_workspace_bytes", "tree_verify_attn_paged",
-    "tree_verify_attn_paged_timed", "kv_commit_paged",
+    "tree_verify_attn_paged_timed", "kv_commit_paged", "verify_layer_paged_workspace_bytes",
+    "verify_layer_paged",
 ]
 SELECT_SCRATCH_BYTES = 8 << 20   # TAPS_SELECT_SCRATCH_BYTES
 
@@ -125,6 +126,12 @@ def load(path: str = LIB_PATH):
     lib.verify_layer.argtypes = [vp, P(LayerWeights), vp, vp, vp, vp, P(Tree), i32, i32, i32, i32,
                                  i32, i32, ctypes.c_float, vp, vp, ctypes.c_size_t, vp]
     lib.verify_layer.restype = i32
+    lib.verify_layer_paged_workspace_bytes.argtypes = [i32] * 8
+    lib.verify_layer_paged_workspace_bytes.restype = ctypes.c_size_t
+    lib.verify_layer_paged.argtypes = [vp, P(LayerWeights), vp, vp, i32, i32, vp, i32, vp,
+                                       P(Tree), i32, i32, i32, i32, i32, i32, f32, vp, vp, sz,
+                                       vp]
+    lib.verify_layer_paged.restype = i32
     lib.taps_status_string.argtypes = [i32]
     lib.taps_status_string.restype = ctypes.c_char_p
     lib.taps_spec_exp_host.argtypes = [f64]

@@ -77,7 +77,8 @@ struct LayerWs {
   size_t part, q, o, attn, total;
 };
 
-LayerWs layer_ws(int batch, int budget, int Hq, int Hkv, int hd, int hidden, int max_ctx) {
+LayerWs layer_ws(int batch, int budget, int Hq, int Hkv, int hd, int hidden, int max_ctx,
+                 int page_rows = 0) {
   const int M = batch * budget, Nqkv = (Hq + 2 * Hkv) * hd;
   const GemmPlan a = plan_gemm(M, Nqkv, hidden), o = plan_gemm(M, hidden, Hq * hd);
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
@@ -85,7 +86,10 @@ LayerWs layer_ws(int batch, int budget, int Hq, int Hkv, int hd, int hidden, int
   w.part = al(std::max((size_t)a.splits * M * Nqkv, (size_t)o.splits * M * hidden) * 4);
   w.q = al((size_t)M * Hq * hd * 2);
   w.o = w.q;
-  w.attn = al(tree_verify_attn_workspace_bytes(batch, budget, Hq, Hkv, hd, max_ctx, TAPS_BF16));
+  w.attn = al(page_rows ? tree_verify_attn_paged_workspace_bytes(batch, budget, Hq, Hkv, hd,
+                                                                 max_ctx, page_rows)
+                        : tree_verify_attn_workspace_bytes(batch, budget, Hq, Hkv, hd, max_ctx,
+                                                           TAPS_BF16));
   w.total = w.part + w.q + w.o + w.attn;
   return w;
 }
@@ -387,18 +391,21 @@ size_t verify_layer_workspace_bytes(int32_t batch, int32_t budget, int32_t Hq, i
   return layer_ws(batch, budget, Hq, Hkv, head_dim, hidden, max_ctx).total;
 }
 
-taps_status verify_layer(const void* X, const taps_layer_weights* w, void* K_cache,
-                         void* V_cache, const int64_t* kv_offset, const int32_t* ctx_len,
-                         const taps_tree* tree, int32_t batch, int32_t budget, int32_t Hq,
-                         int32_t Hkv, int32_t head_dim, int32_t max_ctx, float scale, void* Y,
-                         void* ws, size_t ws_bytes, hipStream_t stream) {
+// The layer over a contiguous cache (pk == nullptr) or a paged one (C20)
+static taps_status layer_run(const void* X, const taps_layer_weights* w, void* K_cache,
+                             void* V_cache, const int64_t* kv_offset, const int32_t* ctx_len,
+                             const taps_tree* tree, int32_t batch, int32_t budget, int32_t Hq,
+                             int32_t Hkv, int32_t head_dim, int32_t max_ctx, float scale,
+                             void* Y, void* ws, size_t ws_bytes, hipStream_t stream,
+                             const PagedKV* pk, int32_t page_rows) {
   if (!w) return TAPS_ERR_INVALID_ARG;
   const taps_status st = layer_check(batch, budget, Hq, Hkv, head_dim, w->hidden, max_ctx, scale);
   if (st != TAPS_OK) return st;
   if (!std::isfinite(w->rope_theta) || !(w->rope_theta > 1.0)) return TAPS_ERR_INVALID_ARG;
   if (!std::isfinite(w->norm_eps) || w->norm_eps < 0.f) return TAPS_ERR_INVALID_ARG;
   if (batch == 0) return TAPS_OK;
-  if (!X || !Y || !K_cache || !V_cache || !kv_offset || !ctx_len || !tree || !tree->parent ||
+  if (!X || !Y || !K_cache || !V_cache || (!kv_offset && !pk) || !ctx_len || !tree ||
+      !tree->parent ||
       !tree->depth || !tree->n_nodes || !w->Wq || !w->Wk || !w->Wv || !w->Wo || !w->q_norm ||
       !w->k_norm)
     return TAPS_ERR_INVALID_ARG;
@@ -407,7 +414,7 @@ taps_status verify_layer(const void* X, const taps_layer_weights* w, void* K_cac
   if ((a16 & 15) != 0 || (((uintptr_t)w->q_norm | (uintptr_t)w->k_norm) & 1) != 0)
     return TAPS_ERR_INVALID_ARG;
   const int hidden = w->hidden;
-  const LayerWs L = layer_ws(batch, budget, Hq, Hkv, head_dim, hidden, max_ctx);
+  const LayerWs L = layer_ws(batch, budget, Hq, Hkv, head_dim, hidden, max_ctx, pk ? page_rows : 0);
   if (!ws || ws_bytes < L.total || ((uintptr_t)ws & 255) != 0) return TAPS_ERR_WORKSPACE;
   const int M = batch * budget, Nq = Hq * head_dim, Nk = Hkv * head_dim;
   float* part = (float*)ws;
@@ -420,19 +427,65 @@ taps_status verify_layer(const void* X, const taps_layer_weights* w, void* K_cac
     return TAPS_ERR_HIP;
   if (launch_qkv_rope(part, a.splits, batch, budget, Hq, Hkv, w->q_norm, w->k_norm,
                       w->rope_theta, w->norm_eps, kv_offset, ctx_len, tree->depth,
-                      tree->n_nodes, max_ctx, Q, K_cache, V_cache, stream) != hipSuccess)
+                      tree->n_nodes, max_ctx, Q, K_cache, V_cache, stream, pk) != hipSuccess)
     return TAPS_ERR_HIP;
-  const AttnPlan pl = plan_attn(batch, budget, Hq, Hkv, head_dim, max_ctx);
-  if (launch_attn_bf16(Q, K_cache, V_cache, kv_offset, ctx_len, tree->parent, tree->n_nodes,
-                       batch, budget, Hq, Hkv, head_dim, max_ctx, scale, pl, O, aws,
-                       stream) != hipSuccess)
-    return TAPS_ERR_HIP;
+  if (pk) {
+    const AttnPlan pl = plan_attn(batch, budget, Hq, Hkv, head_dim, max_ctx,
+                                  paged_max_split(pk->page_shift));
+    if (launch_attn_bf16_paged(Q, K_cache, V_cache, pk->btab, pk->max_pages, pk->num_pages,
+                               pk->page_shift, ctx_len, tree->parent, tree->n_nodes, batch,
+                               budget, Hq, Hkv, max_ctx, scale, pl, O, aws, stream) !=
+        hipSuccess)
+      return TAPS_ERR_HIP;
+  } else {
+    const AttnPlan pl = plan_attn(batch, budget, Hq, Hkv, head_dim, max_ctx);
+    if (launch_attn_bf16(Q, K_cache, V_cache, kv_offset, ctx_len, tree->parent, tree->n_nodes,
+                         batch, budget, Hq, Hkv, head_dim, max_ctx, scale, pl, O, aws,
+                         stream) != hipSuccess)
+      return TAPS_ERR_HIP;
+  }
   const GemmPlan o = plan_gemm(M, hidden, Nq);
   if (launch_gemm_bf16(O, M, Nq, w->Wo, hidden, nullptr, 0, nullptr, 0, o, part, stream) !=
       hipSuccess)
     return TAPS_ERR_HIP;
   return launch_reduce_bf16(part, o.splits, M, hidden, Y, stream) == hipSuccess ? TAPS_OK
                                                                                 : TAPS_ERR_HIP;
+}
+
+taps_status verify_layer(const void* X, const taps_layer_weights* w, void* K_cache,
+                         void* V_cache, const int64_t* kv_offset, const int32_t* ctx_len,
+                         const taps_tree* tree, int32_t batch, int32_t budget, int32_t Hq,
+                         int32_t Hkv, int32_t head_dim, int32_t max_ctx, float scale, void* Y,
+                         void* ws, size_t ws_bytes, hipStream_t stream) {
+  return layer_run(X, w, K_cache, V_cache, kv_offset, ctx_len, tree, batch, budget, Hq, Hkv,
+                   head_dim, max_ctx, scale, Y, ws, ws_bytes, stream, nullptr, 0);
+}
+
+size_t verify_layer_paged_workspace_bytes(int32_t batch, int32_t budget, int32_t Hq,
+                                          int32_t Hkv, int32_t head_dim, int32_t hidden,
+                                          int32_t max_ctx, int32_t page_rows) {
+  if (layer_check(batch, budget, Hq, Hkv, head_dim, hidden, max_ctx, 1.0f) != TAPS_OK ||
+      page_shift_of(page_rows) < 0 || batch == 0)
+    return 0;
+  return layer_ws(batch, budget, Hq, Hkv, head_dim, hidden, max_ctx, page_rows).total;
+}
+
+taps_status verify_layer_paged(const void* X, const taps_layer_weights* w, void* K_pages,
+                               void* V_pages, int32_t num_pages, int32_t page_rows,
+                               const int32_t* block_table, int32_t max_pages,
+                               const int32_t* ctx_len, const taps_tree* tree, int32_t batch,
+                               int32_t budget, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                               int32_t max_ctx, float scale, void* Y, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
+  const int shift = page_shift_of(page_rows);
+  if (shift < 0 || num_pages < 1 || max_pages < 1) return TAPS_ERR_INVALID_ARG;
+  if ((int64_t)max_pages * page_rows < (int64_t)max_ctx + budget) return TAPS_ERR_INVALID_ARG;
+  if ((int64_t)num_pages * page_rows > (int64_t)UINT32_MAX) return TAPS_ERR_UNSUPPORTED;
+  if (batch > 0 && (!block_table || ((uintptr_t)block_table & 3) != 0))
+    return TAPS_ERR_INVALID_ARG;
+  const PagedKV pk{block_table, max_pages, num_pages, shift};
+  return layer_run(X, w, K_pages, V_pages, nullptr, ctx_len, tree, batch, budget, Hq, Hkv,
+                   head_dim, max_ctx, scale, Y, ws, ws_bytes, stream, &pk, page_rows);
 }
 
 }  // extern "C"

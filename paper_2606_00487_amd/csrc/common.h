@@ -132,7 +132,7 @@ hipError_t launch_qkv_rope(const float* part, int splits, int batch, int budget,
                            const void* q_norm, const void* k_norm, double theta, float eps,
                            const int64_t* off, const int32_t* ctx, const int32_t* depth,
                            const int32_t* n, int max_ctx, void* Q, void* Kc, void* Vc,
-                           hipStream_t s);
+                           hipStream_t s, const PagedKV* pk = nullptr);
 hipError_t launch_reduce_bf16(const float* part, int splits, int M, int N, void* Y,
                               hipStream_t s);
 

@@ -212,6 +212,26 @@ def test_paged_commit_validation(lib):
     assert call(sizes=(1, 64, 16, 8, 96, 8192, 0)) == _lib.TAPS_ERR_UNSUPPORTED
 
 
+def test_paged_layer_validation(lib):
+    """verify_layer_paged checks the page geometry before anything else; the workspace
+    query matches the contiguous one below the paged split cap."""
+    fake = 1 << 20
+    w = _lib.LayerWeights(fake, fake, fake, fake, fake, fake, 1e6, 1e-6, 4096)
+    t = _lib.Tree(fake, fake, fake, fake, fake, fake, fake, fake)
+
+    def call(num_pages=200, page_rows=64, max_pages=129):
+        return lib.verify_layer_paged(fake, ctypes.byref(w), fake, fake, num_pages, page_rows,
+                                      fake, max_pages, fake, ctypes.byref(t), 1, 64, 32, 8, 128,
+                                      8192, 0.088, fake, fake, 1 << 40, None)
+
+    assert call(page_rows=48) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(max_pages=128) == _lib.TAPS_ERR_INVALID_ARG
+    assert call(num_pages=0) == _lib.TAPS_ERR_INVALID_ARG
+    a = lib.verify_layer_workspace_bytes(1, 64, 32, 8, 128, 4096, 8192)
+    assert lib.verify_layer_paged_workspace_bytes(1, 64, 32, 8, 128, 4096, 8192, 64) == a > 0
+    assert lib.verify_layer_paged_workspace_bytes(1, 64, 32, 8, 128, 4096, 8192, 48) == 0
+
+
 def test_walk_validation(lib):
     assert lib.accept_walk(None, 1, 64, 16, None, None, None, None, None) == _lib.TAPS_ERR_INVALID_ARG
     assert lib.accept_walk(None, 1, 64, 33, None, None, None, None, None) == _lib.TAPS_ERR_UNSUPPORTED

@@ -331,3 +331,87 @@ def test_paged_commit_edge_paths(taps):
     for nm, g, w in zip(("K", "V", "new_ctx", "committed", "n"), got, want):
         assert g.shape == w.shape and np.array_equal(g, w), nm
     assert list(want[4]) == [1, 13, 13, 3, 2, 3, 1]
+
+
+# ------------------------------------------------------------------ paged layer slice
+def _run_layer_paged(taps, rng, B, N, H, Hq, Hkv, ctx, n, page_rows, sample_nodes=None):
+    """verify_layer_paged against the oracle's paged layer: Y within the layer tolerance, the
+    written node rows within it too, every other pool row untouched (bit for bit)."""
+    from oracle.layer import bf16_round, verify_layer_paged
+    from tests.test_gpu_layer import TOL, _bf16, _to_dev, _tree
+    hd = 128
+    X = _bf16(rng, B, N, H)
+    Wq = _bf16(rng, Hq * hd, H, scale=H ** -0.5)
+    Wk = _bf16(rng, Hkv * hd, H, scale=H ** -0.5)
+    Wv = _bf16(rng, Hkv * hd, H, scale=H ** -0.5)
+    Wo = _bf16(rng, H, Hq * hd, scale=(Hq * hd) ** -0.5)
+    qn = bf16_round(1 + 0.1 * rng.standard_normal(hd))
+    kn = bf16_round(1 + 0.1 * rng.standard_normal(hd))
+    ctx = np.array(ctx, np.int32)
+    n = np.array(n, np.int32)
+    max_ctx = int(ctx.max())
+    need = [-(-(int(ctx[b]) + N) // page_rows) for b in range(B)]
+    npages = sum(need) + 3
+    ids = rng.permutation(npages)
+    table = np.full((B, -(-(max_ctx + N) // page_rows)), -4, np.int32)
+    k = 0
+    for b in range(B):
+        table[b, :need[b]] = ids[k:k + need[b]]
+        k += need[b]
+    Kp, Vp = _bf16(rng, npages, page_rows, Hkv, hd), _bf16(rng, npages, page_rows, Hkv, hd)
+    trees = [_tree(rng, N, int(n[b])) for b in range(B)]
+    parent = np.stack([t[0] for t in trees])
+    depth = np.stack([t[1] for t in trees])
+    samples = None
+    if sample_nodes is not None:
+        samples = [(b, i, h) for b in range(B) for i in sample_nodes(b) for h in range(Hq)]
+    say(f"[layer-paged] B={B} N={N} H={H} Hq={Hq} Hkv={Hkv} ctx={ctx.tolist()} n={n.tolist()} "
+        f"page_rows={page_rows}")
+    Y, Ko, Vo, _, _ = verify_layer_paged(X, Wq, Wk, Wv, Wo, qn, kn, Kp, Vp, table, page_rows,
+                                         ctx, depth, parent, n, Hq, Hkv, hd, 1e6, 1e-6,
+                                         hd ** -0.5, samples=samples)
+    w = taps.LayerWeights(_to_dev(Wq, torch.bfloat16), _to_dev(Wk, torch.bfloat16),
+                          _to_dev(Wv, torch.bfloat16), _to_dev(Wo, torch.bfloat16),
+                          _to_dev(qn, torch.bfloat16), _to_dev(kn, torch.bfloat16))
+    tree = taps.TreeBuffers.empty(B, 1, 1, N)
+    tree.parent.copy_(torch.from_numpy(parent))
+    tree.depth.copy_(torch.from_numpy(depth))
+    tree.n_nodes.copy_(torch.from_numpy(n))
+    Kd, Vd = _to_dev(Kp, torch.bfloat16), _to_dev(Vp, torch.bfloat16)
+    lay = taps.PagedVerifyLayer(B, N, Hq, Hkv, hd, H, max_ctx, page_rows)
+    Yd = lay(_to_dev(X, torch.bfloat16), w, Kd, Vd, torch.from_numpy(table).cuda(),
+             torch.from_numpy(ctx).cuda(), tree)
+    torch.cuda.synchronize()
+    Yg = Yd.float().cpu().numpy().astype(np.float64)
+    Kg = Kd.float().cpu().numpy().astype(np.float64)
+    Vg = Vd.float().cpu().numpy().astype(np.float64)
+    written = np.zeros(Kp.shape[:2], bool)
+    for b in range(B):
+        for i in range(int(n[b])):
+            r = int(ctx[b]) + i
+            written[table[b, r // page_rows], r % page_rows] = True
+    assert np.array_equal(Kg[~written], Kp[~written]) and np.array_equal(Vg[~written], Vp[~written])
+    ek = np.abs(Kg[written] - Ko[written]).max() if written.any() else 0.0
+    ev = np.abs(Vg[written] - Vo[written]).max() if written.any() else 0.0
+    err = 0.0
+    for b in range(B):
+        for i in (range(int(n[b])) if sample_nodes is None else sample_nodes(b)):
+            err = max(err, float(np.abs(Yg[b, i] - Y[b, i]).max()))
+    ymax = max(float(np.nanmax(np.abs(Y))), 1.0)
+    say(f"[layer-paged] max-abs: Y {err:.2e} (|Y| <= {ymax:.2f}), K rows {ek:.2e}, V rows {ev:.2e}")
+    assert err <= TOL * ymax and ek <= TOL and ev <= TOL
+
+
+@pytest.mark.parametrize("page_rows", [32, 128])
+def test_paged_layer_matches_oracle(taps, page_rows):
+    """Three requests (contexts 70, 129, 5; 40-node trees, two partly filled) over pages
+    in random order, the node rows crossing page boundaries."""
+    _run_layer_paged(taps, np.random.default_rng(page_rows), B=3, N=40, H=512, Hq=8, Hkv=2,
+                     ctx=[70, 129, 5], n=[40, 23, 31], page_rows=page_rows)
+
+
+def test_paged_layer_qwen3_8b_shape(taps):
+    """The Qwen3-8B layer shape (hidden 4096, 32/8 heads, 64 nodes, context 8192) over
+    64-row pages, on sampled nodes."""
+    _run_layer_paged(taps, np.random.default_rng(88), B=1, N=64, H=4096, Hq=32, Hkv=8,
+                     ctx=[8192], n=[64], page_rows=64, sample_nodes=lambda b: [0, 1, 17, 63])

@@ -122,3 +122,49 @@ def test_layer_equals_attention_with_identity_output_projection():
     for b in range(2):
         n = int(c["n_nodes"][b])
         assert np.array_equal(Y[b, :n], O2[b, :n].reshape(n, -1))
+
+
+def test_paged_layer_equals_contiguous():
+    """The paged layer is the contiguous one seen through the block table: same Y, and the
+    pools hold the contiguous result's rows (the written node rows included); pages of no
+    request keep their contents."""
+    from oracle.layer import verify_layer, verify_layer_paged
+    rng = np.random.default_rng(31)
+    B, N, H, Hq, Hkv, hd, P = 2, 6, 64, 2, 1, 128, 4
+    ctx = np.array([5, 0], np.int32)
+    rnd = lambda *s: bf16_round(rng.standard_normal(s) * 0.5)   # noqa: E731
+    X = rnd(B, N, H)
+    Wq, Wk, Wv = rnd(Hq * hd, H), rnd(Hkv * hd, H), rnd(Hkv * hd, H)
+    Wo = rnd(H, Hq * hd)
+    qn, kn = bf16_round(1 + 0.1 * rng.standard_normal(hd)), bf16_round(1 + 0.1 * rng.standard_normal(hd))
+    parent = np.array([[-1, 0, 0, 1, 1, 2], [-1, 0, 1, 2, 3, 4]], np.int32)
+    depth = np.array([[0, 1, 1, 2, 2, 2], [0, 1, 2, 3, 4, 5]], np.int32)
+    n = np.array([6, 4], np.int32)
+    off = np.array([0, int(ctx[0]) + N], np.int64)
+    rows = int(off[-1] + ctx[-1] + N)
+    Kc, Vc = rnd(rows, Hkv, hd), rnd(rows, Hkv, hd)
+    Y, Ko, Vo, _, _ = verify_layer(X, Wq, Wk, Wv, Wo, qn, kn, Kc, Vc, off, ctx, depth, parent,
+                                   n, Hq, Hkv, hd, 1e6, 1e-6, hd ** -0.5)
+    need = [-(-(int(ctx[b]) + N) // P) for b in range(B)]
+    ids = rng.permutation(sum(need) + 3)
+    Kp = rnd(len(ids), P, Hkv, hd)
+    Vp = rnd(len(ids), P, Hkv, hd)
+    table = np.zeros((B, max(need)), np.int32)
+    k = 0
+    for b in range(B):
+        for p in range(need[b]):
+            table[b, p] = ids[k]
+            for r in range(p * P, min(int(ctx[b]) + N, (p + 1) * P)):
+                Kp[ids[k], r - p * P] = Kc[int(off[b]) + r]
+                Vp[ids[k], r - p * P] = Vc[int(off[b]) + r]
+            k += 1
+    Yp, Kp2, Vp2, _, _ = verify_layer_paged(X, Wq, Wk, Wv, Wo, qn, kn, Kp, Vp, table, P, ctx,
+                                            depth, parent, n, Hq, Hkv, hd, 1e6, 1e-6, hd ** -0.5)
+    for b in range(B):
+        assert np.array_equal(Yp[b, :n[b]], Y[b, :n[b]])
+        for r in range(int(ctx[b]) + N):
+            pg, sl = table[b, r // P], r % P
+            assert np.array_equal(Kp2[pg, sl], Ko[int(off[b]) + r])
+            assert np.array_equal(Vp2[pg, sl], Vo[int(off[b]) + r])
+    for x in ids[k:]:
+        assert np.array_equal(Kp2[x], Kp[x]) and np.array_equal(Vp2[x], Vp[x])
