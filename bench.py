@@ -64,8 +64,9 @@ def parse():
                          "(embedding 16, hidden 32)")
     ap.add_argument("--sets", type=int, default=0, help="input sets to rotate (0: enough to exceed the MALL)")
     ap.add_argument("--paged", type=int, default=0,
-                    help="the round's attention reads a paged KV cache with pages of this many "
-                         "rows (a power of two, 32..4096; pages in random order); 0: contiguous")
+                    help="the round's attention (and the kv_commit and layer passes) use a "
+                         "paged KV cache with pages of this many rows (a power of two, "
+                         "32..4096; pages in random order); 0: contiguous")
     ap.add_argument("--eager", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
@@ -240,6 +241,8 @@ def main():
     walk = taps.AcceptWalk(cfg.batch, cfg.budget, cfg.block)
     commit = taps.KVCommit(cfg.batch, cfg.budget, cfg.block, cfg.Hkv, cfg.head_dim, max_ctx,
                            dtype=cfg.dtype)
+    pcommit = taps.PagedKVCommit(cfg.batch, cfg.budget, cfg.block, cfg.Hkv, cfg.head_dim, max_ctx,
+                                 args.paged, dtype=cfg.dtype) if args.paged else None
     sets = []
     for k in range(nsets):
         inp = inp0 if k == 0 else gen_round(cfg, seed=inp0.seed + k)
@@ -405,8 +408,12 @@ def main():
             gc = torch.cuda.CUDAGraph()
             with torch.cuda.graph(gc, stream=stream):
                 for _ in range(CR):
-                    commit(s["K"], s["V"], s["off"], s["ctx"], s["tree"], walk.path,
-                           walk.path_len, walk.bonus)
+                    if pcommit is not None:
+                        pcommit(s["Kp"], s["Vp"], s["tab"], s["ctx"], s["tree"], walk.path,
+                                walk.path_len, walk.bonus)
+                    else:
+                        commit(s["K"], s["V"], s["off"], s["ctx"], s["tree"], walk.path,
+                               walk.path_len, walk.bonus)
             gc.replay()
             c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             c0.record(stream)
@@ -435,8 +442,12 @@ def main():
                                    rnd(H, cfg.Hq * hd, scale=(cfg.Hq * hd) ** -0.5),
                                    (1 + 0.1 * torch.randn(hd, generator=gen, device=dev)).to(torch.bfloat16),
                                    (1 + 0.1 * torch.randn(hd, generator=gen, device=dev)).to(torch.bfloat16))
-            lay = taps.VerifyLayer(cfg.batch, cfg.budget, cfg.Hq, cfg.Hkv, hd, H, max_ctx,
-                                   scale=cfg.scale)
+            if args.paged:
+                lay = taps.PagedVerifyLayer(cfg.batch, cfg.budget, cfg.Hq, cfg.Hkv, hd, H,
+                                            max_ctx, args.paged, scale=cfg.scale)
+            else:
+                lay = taps.VerifyLayer(cfg.batch, cfg.budget, cfg.Hq, cfg.Hkv, hd, H, max_ctx,
+                                       scale=cfg.scale)
             Xl = rnd(cfg.batch, cfg.budget, H)
             w_bytes = 2 * H * (cfg.Hq + 2 * cfg.Hkv) * hd + 2 * H * cfg.Hq * hd
             LR = 10
@@ -446,7 +457,10 @@ def main():
                 gl = torch.cuda.CUDAGraph()
                 with torch.cuda.graph(gl, stream=stream):
                     for _ in range(LR):
-                        lay(Xl, lw, sl["K"], sl["V"], sl["off"], sl["ctx"], sl["tree"])
+                        if args.paged:
+                            lay(Xl, lw, sl["Kp"], sl["Vp"], sl["tab"], sl["ctx"], sl["tree"])
+                        else:
+                            lay(Xl, lw, sl["K"], sl["V"], sl["off"], sl["ctx"], sl["tree"])
                 gl.replay()
                 c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 c0.record(stream)
@@ -476,7 +490,7 @@ def main():
     rounds_per_s = cfg.batch * args.steps / elapsed
     achieved = attn_bytes / (t_attn * 1e-6) / 1e9
     traffic = None if args.paged else measured_traffic(cfg.name)   # counters: contiguous only
-    attn_kernel = (f"attn_bf16_kernel<{'true' if args.paged else 'false'}>" if bf
+    attn_kernel = (("attn_bf16_paged_kernel" if args.paged else "attn_bf16_kernel") if bf
                    else "attn_f32_kernel")
     if bf and intensity > RIDGE:
         # more flops per byte than the machine balance: the matrix cores bound the kernel

@@ -595,21 +595,22 @@ struct GroupTag {
   static constexpr int value = KG;
 };
 
-// PAGED: K and V are page pools [num_pages][page_rows][Hkv][HD] and request b's logical
-// row r sits at page btab[b][r >> page_shift], slot r & (page_rows - 1) (offp unused);
-// otherwise Kc and Vc are the contiguous cache and request b starts at row offp[b].
+// The body of both bf16 kernels below.  PAGED: K and V are page pools
+// [num_pages][page_rows][Hkv][HD] and request b's logical row r sits at page
+// btab[b][r >> page_shift], slot r & (page_rows - 1) (offp unused); otherwise Kc and Vc are
+// the contiguous cache and request b starts at row offp[b].  The body uses the
+// buffer-resource type, which exists only in the device pass; the host pass needs no more
+// than the kernels' signatures to emit their launch stubs.
+#if defined(__HIP_DEVICE_COMPILE__)
 template <bool PAGED>
-__global__ __launch_bounds__(512) void attn_bf16_kernel(
+__device__ __attribute__((always_inline)) inline void attn_bf16_body(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc,
     const uint16_t* __restrict__ Vc, const int64_t* __restrict__ offp,
     const int32_t* __restrict__ ctxp, const int32_t* __restrict__ parentp,
     const int32_t* __restrict__ nnp, int N, int Hq, int Hkv, int max_ctx, float scale_log2,
     int split_len, int splits, int mtiles, int pairs, int mrows_pad, uint16_t* __restrict__ wsO,
     float2* __restrict__ wsML, DivMagic dm, int batch, int target_pairs, int lcap,
-    int2* __restrict__ tab, PagedKV pk) {
-  // the body uses the buffer-resource type, which exists only in the device pass; the
-  // host pass needs no more than the signature to emit the launch stub
-#if defined(__HIP_DEVICE_COMPILE__)
+    int2* __restrict__ tab, const PagedKV& pk) {
   constexpr int HD = 128;
   constexpr int NT = 512;
   constexpr int ROWB = HD * 2;        // bytes per K/V row
@@ -1116,6 +1117,39 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(
     ml2.y = Ls;
     __builtin_nontemporal_store(ml2, (f32x2*)(wsML + obase + qr));
   }
+}
+#endif
+
+// Contiguous cache: the kernel keeps exactly the arguments it had before the paged mode
+// existed (a longer argument block measured 0.3 us slower per launch, same code).
+__global__ __launch_bounds__(512) void attn_bf16_kernel(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc,
+    const uint16_t* __restrict__ Vc, const int64_t* __restrict__ offp,
+    const int32_t* __restrict__ ctxp, const int32_t* __restrict__ parentp,
+    const int32_t* __restrict__ nnp, int N, int Hq, int Hkv, int max_ctx, float scale_log2,
+    int split_len, int splits, int mtiles, int pairs, int mrows_pad, uint16_t* __restrict__ wsO,
+    float2* __restrict__ wsML, DivMagic dm, int batch, int target_pairs, int lcap,
+    int2* __restrict__ tab) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  attn_bf16_body<false>(Q, Kc, Vc, offp, ctxp, parentp, nnp, N, Hq, Hkv, max_ctx, scale_log2, split_len,
+                       splits, mtiles, pairs, mrows_pad, wsO, wsML, dm, batch, target_pairs, lcap,
+                       tab, PagedKV{nullptr, 0, 1, 5});
+#endif
+}
+
+// Paged cache (C20 of the readings: tree_verify_attn_paged)
+__global__ __launch_bounds__(512) void attn_bf16_paged_kernel(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc,
+    const uint16_t* __restrict__ Vc, const int64_t* __restrict__ offp,
+    const int32_t* __restrict__ ctxp, const int32_t* __restrict__ parentp,
+    const int32_t* __restrict__ nnp, int N, int Hq, int Hkv, int max_ctx, float scale_log2,
+    int split_len, int splits, int mtiles, int pairs, int mrows_pad, uint16_t* __restrict__ wsO,
+    float2* __restrict__ wsML, DivMagic dm, int batch, int target_pairs, int lcap,
+    int2* __restrict__ tab, PagedKV pk) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  attn_bf16_body<true>(Q, Kc, Vc, offp, ctxp, parentp, nnp, N, Hq, Hkv, max_ctx, scale_log2, split_len,
+                       splits, mtiles, pairs, mrows_pad, wsO, wsML, dm, batch, target_pairs, lcap,
+                       tab, pk);
 #endif
 }
 
@@ -1409,17 +1443,28 @@ static hipError_t launch_attn_bf16_impl(const void* Q, const void* K, const void
     const dim3 block8(512u);
     const DivMagic dm{DivMagic::make(pl.mtiles), DivMagic::make(pl.splits), DivMagic::make(Hkv),
                       DivMagic::make(Hq / Hkv)};
-    if (ev_begin || ev_end)
-      hipExtLaunchKernelGGL(attn_bf16_kernel<PAGED>, grid, block8, 0, s, ev_begin, ev_end, 0, q,
-                            k, v, off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2,
-                            pl.split_len, pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML, dm,
-                            batch, pl.target_pairs, pl.lcap, tab, pk);
-    else
-      attn_bf16_kernel<PAGED><<<grid, block8, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq,
-                                                      Hkv, max_ctx, sl2, pl.split_len,
-                                                      pl.splits, pl.mtiles, pairs, mrows_pad,
-                                                      wsO, wsML, dm, batch, pl.target_pairs,
-                                                      pl.lcap, tab, pk);
+    if constexpr (PAGED) {
+      if (ev_begin || ev_end)
+        hipExtLaunchKernelGGL(attn_bf16_paged_kernel, grid, block8, 0, s, ev_begin, ev_end, 0,
+                              q, k, v, off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2,
+                              pl.split_len, pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML,
+                              dm, batch, pl.target_pairs, pl.lcap, tab, pk);
+      else
+        attn_bf16_paged_kernel<<<grid, block8, 0, s>>>(
+            q, k, v, off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2, pl.split_len, pl.splits,
+            pl.mtiles, pairs, mrows_pad, wsO, wsML, dm, batch, pl.target_pairs, pl.lcap, tab, pk);
+    } else {
+      if (ev_begin || ev_end)
+        hipExtLaunchKernelGGL(attn_bf16_kernel, grid, block8, 0, s, ev_begin, ev_end, 0, q, k,
+                              v, off, ctx, parent, n, budget, Hq, Hkv, max_ctx, sl2,
+                              pl.split_len, pl.splits, pl.mtiles, pairs, mrows_pad, wsO, wsML,
+                              dm, batch, pl.target_pairs, pl.lcap, tab);
+      else
+        attn_bf16_kernel<<<grid, block8, 0, s>>>(q, k, v, off, ctx, parent, n, budget, Hq, Hkv,
+                                                 max_ctx, sl2, pl.split_len, pl.splits,
+                                                 pl.mtiles, pairs, mrows_pad, wsO, wsML, dm,
+                                                 batch, pl.target_pairs, pl.lcap, tab);
+    }
   } else if constexpr (!PAGED) {
     if (ev_begin || ev_end)
       hipExtLaunchKernelGGL(attn_bf16_w4_kernel<64>, grid, block, 0, s, ev_begin, ev_end, 0, q,

@@ -23,13 +23,13 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // the gather is the same in logical rows, and the request's rows sit in distinct pages,
 // so the in-place argument carries over.  Page ids outside the pool are clamped into it.
 template <bool PAGED>
-__global__ __launch_bounds__(kCommitThreads) void commit_kernel(
+__device__ __attribute__((always_inline)) inline void commit_body(
     unsigned char* __restrict__ Kc, unsigned char* __restrict__ Vc,
     const int64_t* __restrict__ offp, const int32_t* __restrict__ ctxp,
     const int32_t* __restrict__ token, const int32_t* __restrict__ path,
     const int32_t* __restrict__ plen, const int32_t* __restrict__ bonus, int N, int D,
     int max_ctx, int row_chunks, int32_t* __restrict__ new_ctx, int32_t* __restrict__ committed,
-    int32_t* __restrict__ n_committed, PagedKV pk) {
+    int32_t* __restrict__ n_committed, const PagedKV& pk) {
   const int b = blockIdx.y;
   const int c = blockIdx.x * kCommitThreads + threadIdx.x;
   const int32_t* pb = path + (size_t)b * (D + 1);
@@ -53,6 +53,8 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(
     const int cc = c < row_chunks ? c : c - row_chunks;
     const size_t row_bytes = (size_t)row_chunks * 16;
     // this thread's chunk of tree row r (logical cache row ctx + r)
+    unsigned char* col = nullptr;     // contiguous: the chunk of the request's first tree row
+    if constexpr (!PAGED) col = cache + (size_t)(offp[b] + ctx) * row_bytes + (size_t)cc * 16;
     auto rowp = [&](int r) -> unsigned char* {
       if constexpr (PAGED) {
         const int L = ctx + r;
@@ -61,7 +63,7 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(
         const size_t phys = ((size_t)pg << pk.page_shift) | (size_t)(L & ((1 << pk.page_shift) - 1));
         return cache + phys * row_bytes + (size_t)cc * 16;
       } else {
-        return cache + (size_t)(offp[b] + ctx + r) * row_bytes + (size_t)cc * 16;
+        return col + (size_t)r * row_bytes;
       }
     };
     // entries past the path read the root's row (always the request's own) and are not
@@ -88,6 +90,27 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(
   }
 }
 
+// the contiguous cache keeps the kernel's original arguments; the paged one adds the table
+__global__ __launch_bounds__(kCommitThreads) void commit_kernel(
+    unsigned char* __restrict__ Kc, unsigned char* __restrict__ Vc,
+    const int64_t* __restrict__ offp, const int32_t* __restrict__ ctxp,
+    const int32_t* __restrict__ token, const int32_t* __restrict__ path,
+    const int32_t* __restrict__ plen, const int32_t* __restrict__ bonus, int N, int D,
+    int max_ctx, int row_chunks, int32_t* __restrict__ new_ctx, int32_t* __restrict__ committed,
+    int32_t* __restrict__ n_committed) {
+  commit_body<false>(Kc, Vc, offp, ctxp, token, path, plen, bonus, N, D, max_ctx, row_chunks, new_ctx, committed, n_committed, PagedKV{nullptr, 0, 1, 5});
+}
+
+__global__ __launch_bounds__(kCommitThreads) void commit_paged_kernel(
+    unsigned char* __restrict__ Kc, unsigned char* __restrict__ Vc,
+    const int64_t* __restrict__ offp, const int32_t* __restrict__ ctxp,
+    const int32_t* __restrict__ token, const int32_t* __restrict__ path,
+    const int32_t* __restrict__ plen, const int32_t* __restrict__ bonus, int N, int D,
+    int max_ctx, int row_chunks, int32_t* __restrict__ new_ctx, int32_t* __restrict__ committed,
+    int32_t* __restrict__ n_committed, PagedKV pk) {
+  commit_body<true>(Kc, Vc, offp, ctxp, token, path, plen, bonus, N, D, max_ctx, row_chunks, new_ctx, committed, n_committed, pk);
+}
+
 }  // namespace
 
 hipError_t launch_commit(void* K, void* V, const int64_t* off, const int32_t* ctx,
@@ -101,13 +124,13 @@ hipError_t launch_commit(void* K, void* V, const int64_t* off, const int32_t* ct
   const dim3 grid((unsigned)((2 * row_chunks + kCommitThreads - 1) / kCommitThreads),
                   (unsigned)batch);
   if (pk != nullptr)
-    commit_kernel<true><<<grid, kCommitThreads, 0, s>>>(
+    commit_paged_kernel<<<grid, kCommitThreads, 0, s>>>(
         (unsigned char*)K, (unsigned char*)V, off, ctx, token, path, path_len, bonus, budget,
         block, max_ctx, row_chunks, new_ctx, committed, n_committed, *pk);
   else
-    commit_kernel<false><<<grid, kCommitThreads, 0, s>>>(
+    commit_kernel<<<grid, kCommitThreads, 0, s>>>(
         (unsigned char*)K, (unsigned char*)V, off, ctx, token, path, path_len, bonus, budget,
-        block, max_ctx, row_chunks, new_ctx, committed, n_committed, PagedKV{nullptr, 0, 1, 5});
+        block, max_ctx, row_chunks, new_ctx, committed, n_committed);
   return hipGetLastError();
 }
 

@@ -203,16 +203,16 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
 // rotary pair; the wave's heads share the node's rotation, computed once.  SP = the
 // projection's K splits: every load of the wave (the request's sizes, the node's depth and
 // cache offset, and all SP partials of its heads) is issued before any of them is used, so
-// the kernel waits for memory once.  With a block table (pk.btab), the node's cache row is
+// the kernel waits for memory once.  In the paged kernel (PAGED), the node's cache row is
 // logical row ctx + i of the request's pages (its page id needs ctx: one more round trip).
 // Page ids outside the pool are clamped into it.
-template <int SP, int HPW>
-__global__ __launch_bounds__(256) void qkv_rope_kernel(
+template <int SP, int HPW, bool PAGED>
+__device__ __attribute__((always_inline)) inline void qkv_rope_body(
     const float* __restrict__ part, int M, int budget, int Hq, int Hkv,
     const uint16_t* __restrict__ q_norm, const uint16_t* __restrict__ k_norm, double theta,
     float eps, const int64_t* __restrict__ off, const int32_t* __restrict__ ctxp,
     const int32_t* __restrict__ depthp, const int32_t* __restrict__ np_, int max_ctx,
-    uint16_t* __restrict__ Q, uint16_t* __restrict__ Kc, uint16_t* __restrict__ Vc, PagedKV pk) {
+    uint16_t* __restrict__ Q, uint16_t* __restrict__ Kc, uint16_t* __restrict__ Vc, const PagedKV& pk) {
   constexpr int HD = 128;
   const int row = blockIdx.x, b = row / budget, i = row - b * budget;
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
@@ -221,7 +221,8 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(
   if (h0 >= H) return;
   const int N = H * HD;
   const int n_raw = np_[b], ctx_raw = ctxp[b], d_raw = depthp[(size_t)b * budget + i];
-  const int64_t kv0 = pk.btab ? 0 : off[b];
+  int64_t kv0 = 0;
+  if constexpr (!PAGED) kv0 = off[b];
   float p0[HPW][SP], p1[HPW][SP];
 #pragma unroll
   for (int j = 0; j < HPW; ++j) {
@@ -238,7 +239,7 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(
   const int ctx = min(max(ctx_raw, 0), max_ctx);
   const int pos = ctx + max(d_raw, 0);
   size_t crow;                                          // first head of the node's cache row
-  if (pk.btab) {
+  if constexpr (PAGED) {
     const int L = ctx + i;
     int pg = pk.btab[(size_t)b * pk.max_pages + min(L >> pk.page_shift, pk.max_pages - 1)];
     pg = min(max(pg, 0), pk.num_pages - 1);
@@ -282,6 +283,26 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(
       dst[lane + 64] = f32_to_bf16(z1);
     }
   }
+}
+
+template <int SP, int HPW>
+__global__ __launch_bounds__(256) void qkv_rope_kernel(
+    const float* __restrict__ part, int M, int budget, int Hq, int Hkv,
+    const uint16_t* __restrict__ q_norm, const uint16_t* __restrict__ k_norm, double theta,
+    float eps, const int64_t* __restrict__ off, const int32_t* __restrict__ ctxp,
+    const int32_t* __restrict__ depthp, const int32_t* __restrict__ np_, int max_ctx,
+    uint16_t* __restrict__ Q, uint16_t* __restrict__ Kc, uint16_t* __restrict__ Vc) {
+  qkv_rope_body<SP, HPW, false>(part, M, budget, Hq, Hkv, q_norm, k_norm, theta, eps, off, ctxp, depthp, np_, max_ctx, Q, Kc, Vc, PagedKV{nullptr, 0, 1, 5});
+}
+
+template <int SP, int HPW>
+__global__ __launch_bounds__(256) void qkv_rope_paged_kernel(
+    const float* __restrict__ part, int M, int budget, int Hq, int Hkv,
+    const uint16_t* __restrict__ q_norm, const uint16_t* __restrict__ k_norm, double theta,
+    float eps, const int64_t* __restrict__ off, const int32_t* __restrict__ ctxp,
+    const int32_t* __restrict__ depthp, const int32_t* __restrict__ np_, int max_ctx,
+    uint16_t* __restrict__ Q, uint16_t* __restrict__ Kc, uint16_t* __restrict__ Vc, PagedKV pk) {
+  qkv_rope_body<SP, HPW, true>(part, M, budget, Hq, Hkv, q_norm, k_norm, theta, eps, off, ctxp, depthp, np_, max_ctx, Q, Kc, Vc, pk);
 }
 
 // Adds the output projection's SP split partials in order and rounds to bf16: four
@@ -361,20 +382,27 @@ hipError_t launch_qkv_rope(const float* part, int splits, int batch, int budget,
                            const int64_t* off, const int32_t* ctx, const int32_t* depth,
                            const int32_t* n, int max_ctx, void* Q, void* Kc, void* Vc,
                            hipStream_t s, const PagedKV* pk) {
-  const PagedKV pkv = pk ? *pk : PagedKV{nullptr, 0, 1, 5};
+
   const int M = batch * budget, H = Hq + 2 * Hkv;
   // four heads per wave once there are many (node, head) pairs: the fp64 rotation is then
   // computed once per four heads, and the grid still holds thousands of waves
   const int hpw = (long long)M * H > 8192 ? 4 : 1;
   const dim3 grid((unsigned)M, (unsigned)((H + 4 * hpw - 1) / (4 * hpw)));
 #define TAPS_ROPE(SP, HPW)                                                                    \
-  qkv_rope_kernel<SP, HPW><<<grid, 256, 0, s>>>(part, M, budget, Hq, Hkv,                     \
-                                                (const uint16_t*)q_norm, (const uint16_t*)k_norm, \
-                                                theta, eps, off, ctx, depth, n, max_ctx,        \
-                                                (uint16_t*)Q, (uint16_t*)Kc, (uint16_t*)Vc, pkv)
+  if (pk)                                                                                     \
+    qkv_rope_paged_kernel<SP, HPW><<<grid, 256, 0, s>>>(                                      \
+        part, M, budget, Hq, Hkv, (const uint16_t*)q_norm, (const uint16_t*)k_norm, theta, eps, \
+        off, ctx, depth, n, max_ctx, (uint16_t*)Q, (uint16_t*)Kc, (uint16_t*)Vc, *pk);        \
+  else                                                                                        \
+    qkv_rope_kernel<SP, HPW><<<grid, 256, 0, s>>>(                                            \
+        part, M, budget, Hq, Hkv, (const uint16_t*)q_norm, (const uint16_t*)k_norm, theta, eps, \
+        off, ctx, depth, n, max_ctx, (uint16_t*)Q, (uint16_t*)Kc, (uint16_t*)Vc)
 #define TAPS_ROPE_SP(SP)                \
-  if (hpw == 4) TAPS_ROPE(SP, 4);       \
-  else TAPS_ROPE(SP, 1)
+  if (hpw == 4) {                       \
+    TAPS_ROPE(SP, 4);                   \
+  } else {                              \
+    TAPS_ROPE(SP, 1);                   \
+  }
   switch (splits) {   // the GEMM plan's split counts
     case 1: TAPS_ROPE_SP(1); break;
     case 2: TAPS_ROPE_SP(2); break;
