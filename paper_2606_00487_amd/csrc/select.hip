@@ -239,8 +239,10 @@ struct Level {                 // expanded trie nodes, stored depth by depth
   double q[kCap];
   uint64_t u[kCap];            // utility bits
   int meta[kCap];              // parent index << 16 | depth << 8 | rank
-  int newidx[kCap];
-  int mlist[kCap];             // members of the boundary bin, in stored order
+  union {
+    int newidx[kCap];          // output position of each kept node
+    uint64_t mkey[kCap];       // utility bits of the boundary bin's members, stored order
+  };
   int hist[kBins];             // nodes per utility bin
   int chist[kCoarse];          // nodes per group of 16 bins
 };
@@ -256,6 +258,7 @@ union Scratch {
   Level l;
   Seq s;
 };
+static_assert(kBins * 32 >= kCap, "one bit per boundary-bin member fits the histogram");
 
 struct Shared {
   uint64_t top[TAPS_MAX_BLOCK][TAPS_MAX_K];
@@ -929,28 +932,34 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
     const int room = N - 1 - c_hi;   // places left for members of bin b*
     uint32_t kmask = amask | bmask;
     if (c_b > room) {                // uniform: the members of bin b* are ranked
+      // The members' utility bits go to a list in stored order, so that a member's list
+      // position orders equal utilities like its stored index, i.e. like (depth, rank
+      // path).  A member is kept if fewer than `room` members beat it under (u desc,
+      // position asc).  One member per thread, all threads reading the same list entries;
+      // the losers are marked in a bitmask (over the histogram, no longer needed).
       int mpos = pre2 >> 16;
-      for (uint32_t m = bmask; m; m &= m - 1) L.mlist[mpos++] = j0 + __ffs(m) - 1;
+      for (uint32_t m = bmask; m; m &= m - 1) L.mkey[mpos++] = L.u[j0 + __ffs(m) - 1];
+      for (int w = tid; w < (c_b + 31) / 32; w += kThreads) L.hist[w] = 0;
       __syncthreads();
-      // a member is kept if fewer than `room` members beat it under (u desc, stored index
-      // asc): the stored index orders equal utilities exactly like (depth, rank path)
-      for (uint32_t m = bmask; m; m &= m - 1) {
-        const int k = __ffs(m) - 1, j = j0 + k;
-        const uint64_t uj = L.u[j];
+      for (int m = tid; m < c_b; m += kThreads) {
+        const uint64_t um = L.mkey[m];
         int rank = 0;
         for (int k0 = 0; k0 < c_b; k0 += 8) {
-          uint64_t ukv[8];
-          int jk[8];
+          uint64_t uk[8];
 #pragma unroll
-          for (int t = 0; t < 8; ++t) jk[t] = L.mlist[min(k0 + t, c_b - 1)];
+          for (int t = 0; t < 8; ++t) uk[t] = L.mkey[min(k0 + t, c_b - 1)];
 #pragma unroll
-          for (int t = 0; t < 8; ++t) ukv[t] = L.u[jk[t]];
-#pragma unroll
-          for (int t = 0; t < 8; ++t)
-            rank += (k0 + t < c_b && (ukv[t] > uj || (ukv[t] == uj && jk[t] < j))) ? 1 : 0;
+          for (int t = 0; t < 8; ++t) {
+            const int k = k0 + t;
+            rank += (k < c_b && (uk[t] > um || (uk[t] == um && k < m))) ? 1 : 0;
+          }
         }
-        if (rank >= room) kmask &= ~(1u << k);
+        if (rank >= room) atomicOr(&L.hist[m >> 5], (int)(1u << (m & 31)));
       }
+      __syncthreads();
+      int mp = pre2 >> 16;
+      for (uint32_t m = bmask; m; m &= m - 1, ++mp)
+        if ((L.hist[mp >> 5] >> (mp & 31)) & 1) kmask &= ~(1u << (__ffs(m) - 1));
     }
     // breadth-first compaction: stored order is already (depth, rank path)
     int total;
