@@ -233,7 +233,7 @@ __device__ inline uint32_t wave_min_u32(uint32_t v) {
 // ------------------------------------------------------------------ shared memory layout
 struct PhaseA {
   uint64_t rowc[kWavesA][kRowCap];
-  uint64_t heads[kWavesA][kWave];
+  uint64_t heads[kWavesA][kWave + 2];   // two rows per wave: 33 entries per half
 };
 struct Level {                 // expanded trie nodes, stored depth by depth
   double q[kCap];
@@ -674,9 +674,134 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
         sh.c[i][lane] = ok ? sh.e[i][lane] / Z : 0.0;
       }
     };
-    for (int i = wave; i < D; i += kWavesA) {
-      if (CK <= 4 * kWave) merge_row(IntC<4>(), i);
-      else merge_row(IntC<16>(), i);
+    // Two rows per wave, one per 32-lane half (row 2p + h in half h), for the common
+    // shapes: K <= 8 (at most K*K <= 64 entries reach the threshold, two per lane), at
+    // most 32 chunks (one head per lane) and 256 list entries, and the scorers whose
+    // q_cond needs only the row's own top-K.  Same steps and arithmetic as merge_row;
+    // every instruction serves two rows, which halves the issue work of this phase.
+    auto merge_pair = [&](auto jm_tag, int pr) __attribute__((always_inline)) {
+      constexpr int JM = decltype(jm_tag)::value;   // 32-entry slices of a row's lists
+      const int h = lane >> 5, hl = lane & 31;
+      const int i = 2 * pr + h;
+      const bool rv = i < D;                        // a half past the last row idles
+      const uint64_t* rc = cand + ((size_t)b * D + (rv ? i : D - 1)) * CK;
+      uint64_t v[JM];
+#pragma unroll
+      for (int j = 0; j < JM; ++j) {
+        const int e = j * 32 + hl;
+        const uint64_t x = rc[min(e, CK - 1)];
+        v[j] = rv && e < CK ? x : 0ull;
+      }
+      const uint64_t hx = rc[(size_t)min(hl, chunks - 1) * K];
+      const uint64_t head = rv && hl < chunks ? hx : 0ull;
+      uint64_t* hd = &A.heads[wave][h * 33];
+      hd[hl] = head;
+      wave_fence();
+      int beat = 0;
+      for (int t0 = 0; t0 < chunks; t0 += 8) {
+        uint64_t hv[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) hv[t] = hd[t0 + t];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) beat += hv[t] > head ? 1 : 0;
+      }
+      // the K-th largest head of each half (fewer than K heads: every entry counts)
+      const uint64_t nz = __ballot(head != 0ull);
+      const uint64_t kth = __ballot(head != 0ull && beat == K - 1);
+      uint64_t T0 = 1ull, T1 = 1ull;
+      if (__popc((uint32_t)nz) >= K) T0 = read_lane_u64(head, __ffs((uint32_t)kth) - 1);
+      if (__popc((uint32_t)(nz >> 32)) >= K)
+        T1 = read_lane_u64(head, 31 + __ffs((uint32_t)(kth >> 32)));
+      const uint64_t T = h ? T1 : T0;
+      // compact each half's entries >= T (at most K*K <= 64) in order
+      uint64_t* rw = &A.rowc[wave][h * 64];
+      int total = 0;
+#pragma unroll
+      for (int j = 0; j < JM; ++j) {
+        const bool keep = v[j] >= T;
+        const uint64_t m = __ballot(keep);
+        const uint32_t mlo = (uint32_t)m, mhi = (uint32_t)(m >> 32);
+        const int pos = total + (int)__builtin_amdgcn_mbcnt_hi(h ? mhi : 0u,
+                                                              __builtin_amdgcn_mbcnt_lo(h ? 0u : mlo, 0u));
+        if (keep) rw[pos] = v[j];
+        total += __popc(h ? mhi : mlo);
+      }
+      wave_fence();
+      const int tmax = max(__builtin_amdgcn_readlane(total, 0), __builtin_amdgcn_readlane(total, 32));
+      // exact ranks of the candidates (lane hl holds entries hl and 32 + hl of its half)
+      const size_t orow = ((size_t)b * D + i) * K;
+      {
+        const uint64_t x0 = rw[hl], x1 = rw[32 + hl];
+        const uint64_t c0 = hl < total ? x0 : 0ull, c1 = 32 + hl < total ? x1 : 0ull;
+        int r0 = 0, r1 = 0;
+        for (int t0 = 0; t0 < tmax; t0 += 8) {
+          uint64_t rv8[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) {
+            const uint64_t x = rw[t0 + t];
+            rv8[t] = t0 + t < total ? x : 0ull;
+          }
+#pragma unroll
+          for (int t = 0; t < 8; ++t) r0 += rv8[t] > c0 ? 1 : 0;
+          if (tmax > 32) {   // uniform
+#pragma unroll
+            for (int t = 0; t < 8; ++t) r1 += rv8[t] > c1 ? 1 : 0;
+          }
+        }
+        if (rv && hl < total && r0 < K) {
+          sh.top[i][r0] = c0;
+          o_tidx[orow + r0] = (int32_t)cand_index(c0);
+          if (o_tval) o_tval[orow + r0] = value_from_key((uint32_t)(c0 >> 32));
+        }
+        if (rv && 32 + hl < total && r1 < K) {
+          sh.top[i][r1] = c1;
+          o_tidx[orow + r1] = (int32_t)cand_index(c1);
+          if (o_tval) o_tval[orow + r1] = value_from_key((uint32_t)(c1 >> 32));
+        }
+      }
+      if (rv && total + hl < K) {   // a row with fewer than K entries
+        const int r = total + hl;
+        sh.top[i][r] = 0ull;
+        o_tidx[orow + r] = -1;
+        if (o_tval) o_tval[orow + r] = value_from_key(0u);
+      }
+      wave_fence();
+      // Eq. 1 for each half's row (lane hl < K)
+      if (rv && hl < K) {
+        const uint64_t k = sh.top[i][hl];
+        const double x = k ? (double)value_from_key((uint32_t)(k >> 32)) : (double)__uint_as_float(0x7FC00000u);
+        double e;
+        if (kind == TAPS_LOGITS) {
+          const uint64_t k0 = sh.top[i][0];
+          const double x0 = k0 ? (double)value_from_key((uint32_t)(k0 >> 32)) : x;
+          e = spec_exp(beta * (x - x0));
+        } else {
+          e = x > 0.0 ? x : 0.0;
+        }
+        sh.e[i][hl] = e;
+      }
+      wave_fence();
+      if (rv && hl < K) {
+        if (kind == TAPS_PROBS && marginal) {
+          sh.c[i][hl] = fmin(sh.e[i][hl], 1.0);
+        } else {
+          double Z = 0.0;
+          for (int j = 0; j < K; ++j) Z = Z + sh.e[i][j];
+          const bool ok = Z > 0.0 && Z <= 1.7976931348623157e308;
+          sh.c[i][hl] = ok ? sh.e[i][hl] / Z : 0.0;
+        }
+      }
+    };
+    if (K <= 8 && chunks <= 32 && CK <= 8 * 32 && !spart && !zpart) {
+      for (int pr = wave; 2 * pr < D; pr += kWavesA) {
+        if (CK <= 4 * 32) merge_pair(IntC<4>(), pr);
+        else merge_pair(IntC<8>(), pr);
+      }
+    } else {
+      for (int i = wave; i < D; i += kWavesA) {
+        if (CK <= 4 * kWave) merge_row(IntC<4>(), i);
+        else merge_row(IntC<16>(), i);
+      }
     }
   }
   // Eq. 3 denominators lambda1 + lambda2 * depth
