@@ -164,6 +164,16 @@ __device__ inline int64_t wave_sum_i64(int64_t v) {
   return v;
 }
 
+// sum of a 64-bit integer over each 32-lane half of a wave (exact), in every lane of it
+__device__ inline int64_t half_sum_i64(int64_t v) {
+#pragma unroll
+  for (int m = 16; m >= 1; m >>= 1) {
+    const uint32_t lo = __shfl_xor((uint32_t)v, m), hi = __shfl_xor((uint32_t)((uint64_t)v >> 32), m);
+    v += (int64_t)(((uint64_t)hi << 32) | lo);
+  }
+  return v;
+}
+
 // inclusive prefix sum within each row of 16 lanes
 __device__ inline int row_inclusive_sum(int v) {
   v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
@@ -676,9 +686,9 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
     };
     // Two rows per wave, one per 32-lane half (row 2p + h in half h), for the common
     // shapes: K <= 8 (at most K*K <= 64 entries reach the threshold, two per lane), at
-    // most 32 chunks (one head per lane) and 256 list entries, and the scorers whose
-    // q_cond needs only the row's own top-K.  Same steps and arithmetic as merge_row;
-    // every instruction serves two rows, which halves the issue work of this phase.
+    // most 32 chunks (one head per lane) and 256 list entries.  Same steps and arithmetic
+    // as merge_row; every instruction serves two rows, which halves the issue work of this
+    // phase.
     auto merge_pair = [&](auto jm_tag, int pr) __attribute__((always_inline)) {
       constexpr int JM = decltype(jm_tag)::value;   // 32-entry slices of a row's lists
       const int h = lane >> 5, hl = lane & 31;
@@ -694,6 +704,23 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
       }
       const uint64_t hx = rc[(size_t)min(hl, chunks - 1) * K];
       const uint64_t head = rv && hl < chunks ? hx : 0ull;
+      // the normaliser partials of the marginal and learned scorers (at most 4 per lane):
+      // loaded with the lists, since they do not depend on the merge
+      const int zn = chunks * kZSub;
+      int64_t zp = 0, sp = 0;
+      if (zpart) {   // uniform
+        const size_t zo = ((size_t)b * D + (rv ? i : D - 1)) * zn;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c0 = q * 32 + hl;
+          const int64_t z = zpart[zo + min(c0, zn - 1)];
+          zp += c0 < zn ? z : 0;
+          if (spart) {
+            const int64_t t = spart[zo + min(c0, zn - 1)];
+            sp += c0 < zn ? t : 0;
+          }
+        }
+      }
       uint64_t* hd = &A.heads[wave][h * 33];
       hd[hl] = head;
       wave_fence();
@@ -781,7 +808,23 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
         sh.e[i][hl] = e;
       }
       wave_fence();
-      if (rv && hl < K) {
+      if (spart) {
+        // learned scorer: LOG(Z) and the entropy LOG(Z) - S / Z of the row from the exact
+        // sums of its integer partials (multiples of 2^-42); q_cond comes later
+        const int64_t zi = half_sum_i64(zp), si = half_sum_i64(sp);
+        if (rv && hl == 0) {
+          const double Z = (double)zi * 0x1p-42, S = (double)si * 0x1p-42;
+          const double lz = zi > 0 ? spec_log(Z) : __longlong_as_double(0x7FF8000000000000ll);
+          sh.lz[i] = lz;
+          sh.ent[i] = lz - S / Z;
+        }
+      } else if (zpart) {
+        // marginal scorer, logits (beta is 1): the full-vocabulary normaliser is the exact
+        // sum of the row's integer partials (multiples of 2^-42)
+        const int64_t zi = half_sum_i64(zp);
+        const double Z = (double)zi * 0x1p-42;
+        if (rv && hl < K) sh.c[i][hl] = Z > 0.0 ? sh.e[i][hl] / Z : 0.0;
+      } else if (rv && hl < K) {
         if (kind == TAPS_PROBS && marginal) {
           sh.c[i][hl] = fmin(sh.e[i][hl], 1.0);
         } else {
@@ -792,7 +835,7 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
         }
       }
     };
-    if (K <= 8 && chunks <= 32 && CK <= 8 * 32 && !spart && !zpart) {
+    if (K <= 8 && chunks <= 32 && CK <= 8 * 32) {
       for (int pr = wave; 2 * pr < D; pr += kWavesA) {
         if (CK <= 4 * 32) merge_pair(IntC<4>(), pr);
         else merge_pair(IntC<8>(), pr);
