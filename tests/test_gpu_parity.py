@@ -209,6 +209,38 @@ def test_select_learned_large_tables(taps, D, K, mode):
     U.assert_tree_equal(gpu, trees, cfg)
 
 
+@pytest.mark.parametrize("B,D,V,K,scorer,kind,mode", [
+    (1, 16, 65536, 8, 0, LOGITS, "plain"),    # 32 chunks of 8 entries: the largest two-row shape
+    (1, 16, 65536, 8, 1, LOGITS, "ties"),     # the same, marginal scorer (integer normaliser)
+    (1, 16, 65536, 8, 2, LOGITS, "deep"),     # the same, learned scorer
+    (1, 15, 67584, 8, 0, LOGITS, "plain"),    # 33 chunks: one row per wave
+    (2, 3, 4099, 8, 1, PROBS, "specials"),    # 3 chunks, odd D, the probability marginal
+    (1, 31, 151936, 1, 0, LOGITS, "plain"),   # K = 1, odd D: the last wave's second half idles
+    (2, 1, 1001, 7, 2, LOGITS, "ties"),       # one row of one chunk, learned scorer
+])
+def test_select_pair_rows(taps, B, D, V, K, scorer, kind, mode):
+    """The row merge at the edges of its two-rows-per-wave form (K <= 8, at most 32 chunks
+    and 256 list entries per row) and just past them, for each scorer.  The vocabulary scan
+    cuts these rows into 32, 32, 32, 33, 3, 10 and 1 chunks."""
+    from oracle.scorer import random_scorer
+    rng = np.random.default_rng(1500 + D + V + K + scorer)
+    dtype = FP32 if kind == PROBS else BF16
+    N = 64
+    cfg = _fuzz_cfg(rng, dtype, kind, V, D, K, N, B=B)
+    say(f"[pair-rows] B={B} D={D} V={V} K={K} scorer={scorer} kind={kind} mode={mode}")
+    m = _fuzz_marginals(rng, cfg, mode)
+    mlp = random_scorer(rng, V, 16, 32, B) if scorer == 2 else None
+    from workloads import bf16_bits_to_f32
+    x = bf16_bits_to_f32(m).astype(np.float64) if dtype == BF16 else m.astype(np.float64)
+    trees = [oracle.select_request(x[b], K, N, kind=kind, lambda2=0.125, tau=0.0,
+                                   scorer=scorer, mlp=mlp, req=b) for b in range(B)]
+    sel = taps.Selector(B, D, V, K, N, dtype=dtype, kind=kind, lambda2=0.125, tau=0.0,
+                        scorer=scorer, mlp=_learned_weights(taps, mlp) if mlp else None)
+    gpu = sel(U.to_dev(m, dtype == BF16))
+    torch.cuda.synchronize()
+    U.assert_tree_equal(gpu, trees, cfg)
+
+
 @pytest.mark.parametrize("seed", range(24))
 def test_select_fuzz(taps, seed):
     rng = np.random.default_rng(500 + seed)
