@@ -995,6 +995,7 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
   // uniform state: stored nodes [p0, p1) form the current depth, base nodes are stored
   int parity = 0;
   int p0 = 0, p1 = 1, base = 1, bstar = 0;
+  bool bstar_due = false;   // the histograms hold a level whose pruning bin is not taken yet
   bool fallback = false;
   for (int d = 0; d < D && N > 1; ++d) {
     const int items = (p1 - p0) * K;
@@ -1018,16 +1019,32 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
       auto eval = [&](auto ni_tag) __attribute__((always_inline)) {
         constexpr int NI = decltype(ni_tag)::value;
         int pp = p0 + q0, rr = it0 - q0 * K;   // (parent, rank) of the first item
+        uint64_t puv[NI];
+        double qpv[NI], crv[NI];
+        int pv[NI], rv[NI];
 #pragma unroll
         for (int k = 0; k < NI; ++k) {
-          const int it = it0 + k;
           const int p = pp, r = rr;
           if (++rr == K) { rr = 0; ++pp; }
           const int pc = min(p, p1 - 1);
-          const uint64_t pu = L.u[pc];
-          const double qp = L.q[pc];
-          const double cr = c3 ? c3[(d * K + (L.meta[pc] & 0xFF)) * K + r] : sh.c[d][r];
-          const double q = qp * cr;
+          puv[k] = L.u[pc];
+          qpv[k] = L.q[pc];
+          crv[k] = c3 ? c3[(d * K + (L.meta[pc] & 0xFF)) * K + r] : sh.c[d][r];
+          pv[k] = p;
+          rv[k] = r;
+        }
+        // the pruning bin of the previous level, read from its histograms while the
+        // loads above are in flight
+        if (bstar_due) {   // uniform
+          bstar = find_bstar(L, N);
+          bstar_due = false;
+        }
+#pragma unroll
+        for (int k = 0; k < NI; ++k) {
+          const int it = it0 + k;
+          const int p = pv[k], r = rv[k];
+          const uint64_t pu = puv[k];
+          const double q = qpv[k] * crv[k];
           const double u = q / den1;
           const int bn = ubin(u);
           // non-short-circuit: no branch may separate a load from the others
@@ -1074,8 +1091,9 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
     __syncthreads();   // the level's nodes and histogram counts are complete
     p0 = p1;
     p1 = base;
-    if (base >= N - 1) bstar = find_bstar(L, N);
+    bstar_due = base >= N - 1;
   }
+  if (bstar_due && !fallback) bstar = find_bstar(L, N);
   int n;
   if (!fallback) {
     // ---- final cut: keep bins > b*; members of bin b* compete for the places left.
