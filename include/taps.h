@@ -389,11 +389,14 @@ size_t verify_layer_paged_workspace_bytes(int32_t batch, int32_t budget, int32_t
                                           int32_t Hkv, int32_t head_dim, int32_t hidden,
                                           int32_t max_ctx, int32_t page_rows);
 
-/* verify_layer over a paged KV cache (the layout of tree_verify_attn_paged): node i's key
- * and value go to logical row ctx + i of request b, i.e. row (ctx + i) % page_rows of page
+/* verify_layer over a paged KV cache, for batched serving (Sec. 4.1 Stage 3 and Sec. 4.3
+ * for the layer's tree attention; the Limitations leave cache management to the serving
+ * system), in the layout of tree_verify_attn_paged: node i's key and value go to logical
+ * row ctx + i of request b, i.e. row (ctx + i) % page_rows of page
  * block_table[b][(ctx + i) / page_rows]; the attention reads the pages.  K_pages, V_pages,
- * num_pages, page_rows, block_table and max_pages as for tree_verify_attn_paged; the other
- * arguments as for verify_layer (no kv_offset). */
+ * num_pages, page_rows, block_table and max_pages as for tree_verify_attn_paged (same
+ * validation and errors); the other arguments as for verify_layer (no kv_offset).  Only
+ * the nodes' rows of the pools are written. */
 taps_status verify_layer_paged(const void *X, const taps_layer_weights *w, void *K_pages,
                                void *V_pages, int32_t num_pages, int32_t page_rows,
                                const int32_t *block_table, int32_t max_pages,
