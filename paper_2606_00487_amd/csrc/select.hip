@@ -310,8 +310,9 @@ struct ScorerArgs {
 };
 
 // Working set of the learned scorer in the scratch area: float counts of the weight block
-// (W1, b1, w2) and of the embedding block (row stride ES), the parent slots np and all
-// slots S of the hidden-unit parts, and the units KC per chunk (below 1: does not fit)
+// (W1, b1, w2) and of the embedding block (row stride ES), then four doubles per hidden unit
+// (its three edge-feature weights and its w2), the parent slots np and all slots S of the
+// hidden-unit parts, and the units KC per chunk (below 1: does not fit)
 struct LearnedLayout {
   int wsz, ES, esz, np, S, KC;
 };
@@ -322,7 +323,7 @@ __host__ __device__ inline LearnedLayout learned_layout(int D, int K, int d, int
   l.esz = ((D * K + 1) * l.ES + 1) & ~1;
   l.np = 1 + (D - 1) * K;
   l.S = l.np + D * K;
-  const long long left = (long long)sizeof(Scratch) - 4ll * (l.wsz + l.esz);
+  const long long left = (long long)sizeof(Scratch) - 4ll * (l.wsz + l.esz) - 32ll * h;
   const long long kc = left > 0 ? left / (8ll * l.S) : 0;
   l.KC = (int)(kc < h ? kc : h);
   return l;
@@ -858,19 +859,27 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
     const int edges = D * K * K, DK = D * K;
     // The scratch area (free until Phase C) holds, in order: the weights (W1, b1, w2 as
     // fp32), the embeddings of the root's token (slot 0) and of each candidate (slot
-    // 1 + i*K + r; zeros for no token) at an odd row stride, and per hidden unit k the
-    // parent part b1[k] + P_k of each possible parent (0: the root, 1 + (i-1)*K + pr: the
-    // rank-pr candidate of row i-1) followed by the child part C_k of each candidate, for
-    // a chunk of KC units at a time.  Each edge then adds its five terms per unit.
+    // 1 + i*K + r; zeros for no token) at an odd row stride, each unit's three edge-feature
+    // weights and its w2 widened to fp64 (so that the edges read them two at a time and
+    // convert nothing), and per hidden unit k the parent part b1[k] + P_k of each possible
+    // parent (0: the root, 1 + (i-1)*K + pr: the rank-pr candidate of row i-1) followed by
+    // the child part C_k of each candidate, for a chunk of KC units at a time.  Each edge
+    // then adds its five terms per unit.
     const LearnedLayout lay = learned_layout(D, K, d, h);
     float* Ws = reinterpret_cast<float*>(&sh.x);
     const int ES = lay.ES, np = lay.np, S = lay.S, KC = lay.KC;
     float* Es = Ws + lay.wsz;
-    double* part = reinterpret_cast<double*>(Es + lay.esz);
+    double* Wd = reinterpret_cast<double*>(Es + lay.esz);
+    double* part = Wd + 4 * h;
     for (int j = tid; j < h * F; j += kThreadsA) Ws[j] = mlp.W1[j];
     for (int j = tid; j < h; j += kThreadsA) {
+      const float w2j = mlp.w2[j];
       Ws[h * F + j] = mlp.b1[j];
-      Ws[h * F + h + j] = mlp.w2[j];
+      Ws[h * F + h + j] = w2j;
+      Wd[4 * j] = (double)mlp.W1[j * F + 2 * d];
+      Wd[4 * j + 1] = (double)mlp.W1[j * F + 2 * d + 1];
+      Wd[4 * j + 2] = (double)mlp.W1[j * F + 2 * d + 2];
+      Wd[4 * j + 3] = (double)w2j;
     }
     for (int j = tid; j < (DK + 1) * d; j += kThreadsA) {
       const int es = j / d, jj = j - es * d;
@@ -929,20 +938,21 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
         const int ps = i == 0 ? 0 : 1 + (i - 1) * K + pr, cs = np + i * K + r;
         double logit = c3[ed];
         for (int kk = 0; kk < kn; kk += 4) {
-          double av[4];
+          double av[4], w2v[4];
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
             const int k = min(kk + u, kn - 1);
-            const float* w = Ws + (k0 + k) * F + 2 * d;
+            const double* w = Wd + 4 * (k0 + k);
             double a = part[k * S + ps] + part[k * S + cs];
-            a = a + (double)w[0] * depth;
-            a = a + (double)w[1] * lp;
-            a = a + (double)w[2] * H;
+            a = a + w[0] * depth;
+            a = a + w[1] * lp;
+            a = a + w[2] * H;
             av[u] = a > 0.0 ? a : 0.0;
+            w2v[u] = w[3];
           }
 #pragma unroll
           for (int u = 0; u < 4; ++u)
-            if (kk + u < kn) logit = logit + (double)Ws[h * F + h + k0 + kk + u] * av[u];
+            if (kk + u < kn) logit = logit + w2v[u] * av[u];
         }
         c3[ed] = logit;
       }
