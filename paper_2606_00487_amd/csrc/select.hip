@@ -345,7 +345,9 @@ __device__ inline double qcond(const Shared& sh, const double* c3, int K, int d,
 // l, l + 64, ... (slot s: node s * 64 + l); head[s] holds the utility bits + 1 of that
 // node's next child (0: none left), nxt[s] its position in the node's child order.
 template <int SLOTS>
-__device__ int select_sequential(Shared& sh, const double* c3, int D, int K, int N, double tau) {
+__device__ __attribute__((always_inline)) inline int select_sequential(Shared& sh, const double* c3,
+                                                                     int D, int K, int N,
+                                                                     double tau) {
   Seq& S = sh.x.s;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   if (wave == 0) {
@@ -499,7 +501,9 @@ __device__ int select_sequential(Shared& sh, const double* c3, int D, int K, int
   return n;
 }
 
-template <int SLOTS>
+// LEARNED: the learned scorer's instance (its q_cond table and Phase B2); the other
+// scorers run an instance without that code, so their kernel stays smaller.
+template <int SLOTS, bool LEARNED>
 __global__ __launch_bounds__(kThreadsA) void select_kernel(
     int D, int K, int N, int kind, double lambda1, double lambda2, double tau, double beta,
     int chunks, int marginal, const uint64_t* __restrict__ cand,
@@ -511,6 +515,7 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
   __shared__ Shared sh;
   const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const bool learned = LEARNED && spart != nullptr;   // the entropy partials come with it
 
   // ---------------- Phase A: row merge (one wave per row)
   // Loads below take clamped (in-bounds) addresses and are issued unconditionally, the
@@ -647,7 +652,7 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
         sh.e[i][lane] = e;
       }
       wave_fence();
-      if (spart) {
+      if (learned) {
         // learned scorer: LOG(Z) and the entropy LOG(Z) - S / Z of the row from the exact
         // sums of its integer partials (multiples of 2^-42); q_cond comes later
         const int zn = chunks * kZSub;
@@ -716,7 +721,7 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
           const int c0 = q * 32 + hl;
           const int64_t z = zpart[zo + min(c0, zn - 1)];
           zp += c0 < zn ? z : 0;
-          if (spart) {
+          if (learned) {
             const int64_t t = spart[zo + min(c0, zn - 1)];
             sp += c0 < zn ? t : 0;
           }
@@ -809,7 +814,7 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
         sh.e[i][hl] = e;
       }
       wave_fence();
-      if (spart) {
+      if (learned) {
         // learned scorer: LOG(Z) and the entropy LOG(Z) - S / Z of the row from the exact
         // sums of its integer partials (multiples of 2^-42); q_cond comes later
         const int64_t zi = half_sum_i64(zp), si = half_sum_i64(sp);
@@ -853,8 +858,8 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
   __syncthreads();
   // ---------------- learned scorer: q_cond table c3[i][parent rank][child rank] (all waves)
   extern __shared__ double s_c3[];
-  double* c3 = spart ? s_c3 : nullptr;
-  if (c3) {
+  double* c3 = learned ? s_c3 : nullptr;
+  if (learned) {
     const int F = 2 * mlp.d + 3, d = mlp.d, h = mlp.h;
     const int edges = D * K * K, DK = D * K;
     // The scratch area (free until Phase C) holds, in order: the weights (W1, b1, w2 as
@@ -1311,16 +1316,21 @@ hipError_t launch_select(const void* /*marg*/, const taps_select_params& p, cons
     mlp = ScorerArgs{w.emb, w.W1, w.b1, w.w2, w.b2, w.root_token, w.emb_dim, w.hidden, p.vocab};
     dyn = (size_t)p.block * p.K * p.K * sizeof(double);
   }
-#define TAPS_SEL(SL)                                                                          \
+#define TAPS_SEL_L(SL, LR)                                                                    \
   do {                                                                                        \
-    if (dyn && hipFuncSetAttribute((const void*)select_kernel<SL>,                            \
+    if (dyn && hipFuncSetAttribute((const void*)select_kernel<SL, LR>,                        \
                                    hipFuncAttributeMaxDynamicSharedMemorySize,                \
                                    (int)dyn) != hipSuccess)                                    \
       return hipErrorInvalidValue;                                                            \
-    select_kernel<SL><<<grid, block, dyn, s>>>(                                               \
+    select_kernel<SL, LR><<<grid, block, dyn, s>>>(                                           \
         p.block, p.K, p.budget, p.kind, p.lambda1, p.lambda2, p.tau, p.beta, plan.chunks,     \
         marginal, cand, zpart, spart, mlp, out.parent, out.token, out.depth, out.rank,        \
         out.q_reach, out.n_nodes, out.topk_idx, out.topk_val);                                \
+  } while (0)
+#define TAPS_SEL(SL)                                                                          \
+  do {                                                                                        \
+    if (spart) TAPS_SEL_L(SL, true);                                                          \
+    else TAPS_SEL_L(SL, false);                                                               \
   } while (0)
   static_assert(TAPS_MAX_BUDGET <= 8 * kWave, "at most eight frontier slots per lane");
   switch (slots) {
@@ -1331,6 +1341,7 @@ hipError_t launch_select(const void* /*marg*/, const taps_select_params& p, cons
     default: TAPS_SEL(8); break;
   }
 #undef TAPS_SEL
+#undef TAPS_SEL_L
   return hipGetLastError();
 }
 
