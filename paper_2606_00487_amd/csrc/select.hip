@@ -690,7 +690,7 @@ __global__ __launch_bounds__(kThreadsA) void select_kernel(
         sh.c[i][lane] = ok ? sh.e[i][lane] / Z : 0.0;
       }
     };
-    // Two rows per wave, one per 32-lane half (row 2p + h in half h), for the common
+    // Two rows per wave, one per 32-lane half (row 2 pr + h in half h), for the common
     // shapes: K <= 8 (at most K*K <= 64 entries reach the threshold, two per lane), at
     // most 32 chunks (one head per lane) and 256 list entries.  Same steps and arithmetic
     // as merge_row; every instruction serves two rows, which halves the issue work of this
