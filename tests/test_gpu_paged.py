@@ -165,29 +165,31 @@ def test_paged_tree_rows_dominate_at_full_size(taps):
     U.attention_error(U.gpu_o_as_f64(O), ref, BF16, "paged tree-dominant qwen3_8b")
 
 
-def test_paged_serve16_full_size(taps):
+@pytest.mark.parametrize("name,page_rows,samples", [("serve16", 64, 384), ("stress", 256, 192)])
+def test_paged_full_size(taps, name, page_rows, samples):
     """The 16-request serving shape (contexts of 512 to 16K rows, 128 nodes each, the ragged
-    work list) over 64-row pages in random order, on 384 sampled (node, head) rows plus the
-    root and the deepest node of every request."""
-    inp = gen_round("serve16")
+    work list) and the 4-request stress shape (32K-row contexts, 256 nodes: four-word
+    ancestor masks) over pages in random order, on sampled (node, head) rows plus the root
+    and the deepest node of every request."""
+    inp = gen_round(name)
     c = inp.cfg
     trees = U.oracle_trees(inp)
     rng = np.random.default_rng(80)
-    say("[paged-serve16] 16 requests, 64-row pages")
-    Kp, Vp, table = to_pages(inp.K, inp.V, inp.kv_offset, inp.ctx_len, c.budget, 64, rng)
+    say(f"[paged-full] {name}, {page_rows}-row pages")
+    Kp, Vp, table = to_pages(inp.K, inp.V, inp.kv_offset, inp.ctx_len, c.budget, page_rows, rng)
     parents = [t.parent for t in trees]
     n = [t.n for t in trees]
-    O = run_paged(taps, inp.Q, Kp, Vp, table, 64, inp.ctx_len, parents, n, c.Hq, c.Hkv,
+    O = run_paged(taps, inp.Q, Kp, Vp, table, page_rows, inp.ctx_len, parents, n, c.Hq, c.Hkv,
                   int(inp.ctx_len.max()))
     pick = []
-    for _ in range(384):
+    for _ in range(samples):
         b = int(rng.integers(0, c.batch))
         pick.append((b, int(rng.integers(0, trees[b].n)), int(rng.integers(0, c.Hq))))
     for b, t in enumerate(trees):
         pick.append((b, 0, 0))
         pick.append((b, int(np.argmax(t.depth[:t.n])), c.Hq - 1))
-    ref = paged_ref(inp.Q, Kp, Vp, table, 64, inp.ctx_len, parents, n, samples=pick)
-    U.attention_error(U.gpu_o_as_f64(O), ref, BF16, "paged serve16")
+    ref = paged_ref(inp.Q, Kp, Vp, table, page_rows, inp.ctx_len, parents, n, samples=pick)
+    U.attention_error(U.gpu_o_as_f64(O), ref, BF16, f"paged {name}")
 
 
 @pytest.mark.parametrize("seed", range(4))
