@@ -641,11 +641,15 @@ __device__ __attribute__((always_inline)) inline void attn_bf16_body(
     asm volatile("" ::"s"(pk.btab), "s"(pk.max_pages), "s"(pk.num_pages), "s"(pk.page_shift));
   // ---- which (request, KV head, split, row tile) this workgroup owns.  The row tiles of a
   // pair are 8 block ids apart (one XCD, which shares the pair's K/V in its L2).  One
-  // request (tab == nullptr): pair = (KV head) * splits + split, fixed by the host; several:
-  // the ragged list of ragged_pick.  The split's partial results go to slot `pair`.
+  // request (tab == nullptr): pair = (KV head) * splits + split, fixed by the host, and each
+  // XCD takes a run of consecutive pairs, so that the splits of a KV head, which all read
+  // its query tile, share that tile in one L2; several: the ragged list of ragged_pick, its
+  // pairs interleaved over the XCDs (the host sizes the grid for the most pairs there can
+  // be).  The split's partial results go to slot `pair`.
   const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
   const int sq = dm.div(slot, mtiles, dm.mt);
-  const int mt = slot - sq * mtiles, pair = sq * 8 + xcd;
+  const int mt = slot - sq * mtiles;
+  const int pair = tab == nullptr ? xcd * ((pairs + 7) >> 3) + sq : sq * 8 + xcd;
   if (pair >= pairs) return;
   int b, g, split;
   if (tab == nullptr) {
